@@ -1,0 +1,222 @@
+"""Benchmark of the MI355X FP8 FFN (one transformer layer's FFN per step).
+
+A step is one call of the whole hot path, lacache_ffn_fp8: fused RMSNorm +
+1x128 e4m3 quantization, FP8 gate/up GEMM with fused SwiGLU re-quantization,
+FP8 down GEMM to bf16. Inputs are seeded synthetic activations and weights
+(LLaDA-8B FFN shapes, H=4096, I=12288), resident in HBM before timing.
+Weights rotate over several independently drawn layers, more bytes than the
+256 MB Infinity Cache holds, so every step streams its weights from HBM.
+
+Prints one JSON line. The default workload is the 32-token decode block
+(M=32); --workload selects another. Besides the whole-step throughput the
+line carries the dominant kernel's roofline figures (timed live with HIP
+events around that kernel alone) and the CPU oracle's throughput on a bounded
+sample of the same workload.
+
+  python bench.py [--gpus 1] [--steps 50] [--warmup 10] [--workload block32_h4096_i12288]
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "FP8 FFN TFLOP/s + tokens/s per layer (H=4096,I=12288); % FP8 MFMA / HBM peak"
+PEAK_HBM_GBPS = 8000.0
+PEAK_FP8_TFLOPS = 5033.0  # dense FP8 MFMA: 256 CU x 2.4 GHz x 8192 FLOP/clk
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pmc_traffic.json")
+KERNEL_SOURCES = {
+    "gateup_skinny": ["gemm_skinny.hip", "device.h"],
+    "down_skinny": ["gemm_skinny.hip", "device.h"],
+    "gateup_tiled": ["gemm_tiled.hip", "device.h"],
+    "down_tiled": ["gemm_tiled.hip", "device.h"],
+}
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--workload", default="block32_h4096_i12288")
+    p.add_argument("--weight-sets", type=int, default=4)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--profile-only", action="store_true",
+                   help="run warmup + timed steps only (for rocprofv3), print the line without the CPU leg")
+    return p.parse_args()
+
+
+def source_sha(kernel):
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, "paper_2607_16339_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def stage_bytes(M, H, I):
+    """Algorithmic HBM bytes per launch of each stage (each operand read once,
+    each result written once)."""
+    g = 128
+    return {
+        "norm": 2 * M * H + 2 * H + M * H + 4 * M * H // g,
+        "gateup": 2 * I * H + 4 * (2 * I // g) * (H // g) + M * H + 4 * M * H // g + M * I + 4 * M * I // g,
+        "down": H * I + 4 * (H // g) * (I // g) + M * I + 4 * M * I // g + 2 * M * H,
+    }
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (the FFN shards by rows with no "
+              "exchange; see DESIGN.md). Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2607_16339_amd as lc
+    import synth
+
+    w = synth.WORKLOADS[args.workload]
+    M, H, I = w.M, w.H, w.I
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    lc.lib()  # fails loudly when the HIP library is missing
+
+    def dev_bf16(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16).copy()).view(torch.bfloat16).to(dev)
+
+    # ---- weights: several layers, quantized on the GPU; bf16 copies freed
+    sets = []
+    for layer in range(1, args.weight_sets + 1):
+        b = synth.make_weights(w, layer)
+        wgu = dev_bf16(np.concatenate([b["w_gate"], b["w_up"]], axis=0))
+        wgu_q, wgu_s = lc.quantize_weights(wgu)
+        del wgu
+        wd = dev_bf16(b["w_down"])
+        wd_q, wd_s = lc.quantize_weights(wd)
+        del wd
+        x = dev_bf16(synth.make_x(w, layer=layer, step=layer - 1))
+        sets.append(dict(norm_w=dev_bf16(b["norm_w"]), wgu_q=wgu_q, wgu_s=wgu_s, wd_q=wd_q, wd_s=wd_s, x=x))
+    torch.cuda.synchronize()
+    out = torch.empty((M, H), dtype=torch.bfloat16, device=dev)
+    S = len(sets)
+
+    def step(i):
+        s = sets[i % S]
+        lc.lacache_ffn_fp8(s["x"], s["norm_w"], s["wgu_q"], s["wgu_s"], s["wd_q"], s["wd_s"], out)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    e0.record(stream)
+    for i in range(args.steps):
+        step(i)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    ms = e0.elapsed_time(e1) / args.steps
+
+    flop = 6.0 * M * H * I
+    tflops = flop / (ms * 1e-3) / 1e12
+    tok_s = M / (ms * 1e-3)
+    bytes_min = 3 * H * I + 4 * (3 * I // 128) * (H // 128) + 2 * H + 4 * M * H
+    gbps = bytes_min / (ms * 1e-3) / 1e9
+
+    # ---- dominant kernel, timed alone: the stage calls launch the same kernels
+    skinny = M <= 64
+    xq = torch.empty((M, H), dtype=torch.uint8, device=dev)
+    xs = torch.empty((H // 128, M), dtype=torch.float32, device=dev)
+    hq = torch.empty((M, I), dtype=torch.uint8, device=dev)
+    hs = torch.empty((I // 128, M), dtype=torch.float32, device=dev)
+    sb = stage_bytes(M, H, I)
+    kt = {"gateup": [], "down": []}
+    reps = max(args.steps, 20)
+    for i in range(args.warmup + reps):
+        s = sets[i % S]
+        lc.lacache_rmsnorm_quant(s["x"], s["norm_w"], xq, xs)
+        a0, a1, b1 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+        a0.record(stream)
+        lc.lacache_gateup_swiglu_quant(xq, xs, s["wgu_q"], s["wgu_s"], hq, hs)
+        a1.record(stream)
+        lc.lacache_down_proj(hq, hs, s["wd_q"], s["wd_s"], out)
+        b1.record(stream)
+        if i >= args.warmup:
+            kt["gateup"].append((a0, a1))
+            kt["down"].append((a1, b1))
+    torch.cuda.synchronize()
+    k_ms = {k: float(np.mean([a.elapsed_time(b) for a, b in v])) for k, v in kt.items()}
+    dom = "gateup"
+    kname = dom + ("_skinny" if skinny else "_tiled")
+    if skinny:
+        achieved = sb[dom] / (k_ms[dom] * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBPS, 4)}
+    else:
+        achieved = 4.0 * M * H * I / (k_ms[dom] * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_FP8_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_FP8_TFLOPS, 4)}
+    roof["kernel"] = kname
+    roof["kernel_ms"] = round(k_ms[dom], 5)
+    roof["traffic"] = None
+    try:
+        with open(TRAFFIC_FILE) as f:
+            tr = json.load(f).get(kname + ":" + args.workload)
+        if tr and tr.get("source_sha") == source_sha(kname):
+            roof["traffic"] = tr["hbm_bytes_per_launch"]
+    except (OSError, ValueError):
+        pass
+
+    line = {
+        "metric": METRIC, "value": round(tflops, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "fp8_e4m3 (fp32 accumulate)", "data": "synthetic",
+        "config": {"workload": args.workload, "M": M, "H": H, "I": I, "group": 128, "weight_sets": S,
+                   "path": "skinny" if skinny else "tiled"},
+        "tokens_per_s": round(tok_s, 1), "hbm_GBps_min_bytes": round(gbps, 1),
+        "frac_hbm_peak": round(gbps / PEAK_HBM_GBPS, 4), "frac_fp8_peak": round(tflops / PEAK_FP8_TFLOPS, 4),
+        "stage_ms": {k: round(v, 5) for k, v in k_ms.items()}, "wall_s_timed": round(t_wall, 4),
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline and not args.profile_only:
+        line["cpu_baseline"] = cpu_baseline(w, sets, out, dev)
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(w, sets, out, dev):
+    """The oracle, as it stands, on a bounded sample of the same workload."""
+    import numpy as np
+    import oracle.ffn as O
+    import synth
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # noqa: BLE001
+        threads = os.cpu_count() or 1
+    s = sets[0]
+    rows = min(w.M, 32)
+    xb = synth.make_x(w, layer=1, step=0)[:rows]
+    host = [t.cpu().numpy() for t in (s["wgu_q"], s["wgu_s"], s["wd_q"], s["wd_s"])]
+    norm_w = s["norm_w"].view(__import__("torch").int16).cpu().numpy().view(np.uint16)
+    t0 = time.perf_counter()
+    O.ffn(xb, norm_w, host[0], host[1], host[2], host[3], w.I)
+    t = time.perf_counter() - t0
+    flop = 6.0 * rows * w.H * w.I
+    return {"value": round(flop / t / 1e12, 6), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": "%d of %d rows, one layer (the FFN is row-independent): %.2f s" % (rows, w.M, t),
+            "tokens_per_s": round(rows / t, 3)}
+
+
+if __name__ == "__main__":
+    main()

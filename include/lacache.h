@@ -1,0 +1,164 @@
+/*
+ * lacache.h -- C ABI of the MI355X (gfx950) per-group FP8 FFN.
+ *
+ * The library implements the mixed-precision FFN that LaCache (arxiv
+ * 2607.16339) applies to every transformer layer except the first (Sec. 3.4):
+ *
+ *   x (bf16) -> RMSNorm fused with 1x128 e4m3 quantization     (Sec. 3.4, "AddNorm")
+ *            -> FP8 gate/up GEMM with per-group dequantization  (Sec. 3.4, Eqs. 7-8)
+ *            -> SwiGLU fused with 1x128 e4m3 re-quantization    (Sec. 3.4, "Swiglu")
+ *            -> FP8 down GEMM with per-group dequantization -> out (bf16)
+ *
+ * Activations are quantized in groups of 128 consecutive elements of a row
+ * and weights in 128x128 blocks (Sec. 3.4): scale = max|x| / 448 (Eq. 8),
+ * code = e4m3(x / scale) with clipping to +-448 (Eq. 7). FP8 is OCP e4m3fn
+ * (bias 7, max 448, no infinities); rounding is to nearest, ties to even; the
+ * scale is an fp32 value rounded once from amax / 448 and x / scale is a
+ * correctly rounded fp32 division. A group whose scale is 0 gets codes 0x00.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Pointers are device pointers on the current HIP device, unless stated.
+ *   bf16 values are passed as uint16_t bit patterns, e4m3 codes as uint8_t,
+ *   scales as fp32. Row-major, last index contiguous.
+ * - stream is a hipStream_t passed as void*; NULL means the null stream.
+ *   Every call is asynchronous on that stream: it returns after enqueueing,
+ *   with no host or device synchronization.
+ * - group must be 128 (the paper fixes 1x128 and 128x128); any other value
+ *   returns LACACHE_ERR_UNSUPPORTED. Dimensions H, I (and N, K) must be
+ *   positive multiples of 128; M >= 0. M == 0 (n == 0) returns LACACHE_OK after
+ *   the shape checks, launches nothing and does not look at the pointers.
+ *   Size limits: H <= 16384, I <= 65536, M <= 2^24.
+ * - Every argument is checked on the host before anything is launched; on
+ *   error nothing is launched and no output is written. Pointers must be
+ *   non-NULL (except the optional *_tap outputs) and 16-byte aligned.
+ *   Outputs must not overlap inputs.
+ * - The caller owns every buffer it passes. The library owns only the
+ *   intermediate workspace of lacache_ffn_fp8 (see below).
+ * - Results are deterministic: the same inputs give the same output bytes
+ *   (no floating-point atomics).
+ * - A failed HIP launch or allocation returns LACACHE_ERR_HIP or
+ *   LACACHE_ERR_ALLOC; lacache_status_string() names any status.
+ */
+#ifndef LACACHE_H
+#define LACACHE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  LACACHE_OK = 0,
+  LACACHE_ERR_INVALID_ARG = -1, /* null/misaligned pointer, bad shape, overlap */
+  LACACHE_ERR_UNSUPPORTED = -2, /* group != 128, or a size above the limits */
+  LACACHE_ERR_HIP = -3,         /* a HIP runtime call or kernel launch failed */
+  LACACHE_ERR_ALLOC = -4        /* the library could not allocate its workspace */
+} lacache_status;
+
+/*
+ * 128x128 block quantization of a bf16 weight (Sec. 3.4, Eqs. 7-8).
+ *   w   [N x K] bf16               (input)
+ *   w_q [N x K] e4m3 codes         (output)
+ *   w_s [N/128 x K/128] fp32       (output) block (nb, kb) covers rows
+ *                                  nb*128.. and columns kb*128..
+ * For the FFN, the gate/up weight is the row concatenation [W_gate; W_up]
+ * ([2I x H], gate rows first) and the down weight is W_down [H x I].
+ */
+int lacache_quant_weights(void* stream, const uint16_t* w, uint8_t* w_q, float* w_s,
+                          int64_t N, int64_t K, int group);
+
+/*
+ * Fused RMSNorm + 1x128 activation quantization (Sec. 3.4: quantization fused
+ * with the norm before the gate-up linear).
+ *   x      [M x H] bf16            (input, the post-residual hidden state)
+ *   norm_w [H] bf16                (input)
+ *   xq     [M x H] e4m3            (output)
+ *   xs     [H/128 x M] fp32        (output) scale of row m, group kb at xs[kb*M + m]
+ * y = RN32(RN32(x * w) * r), r = RN32(1 / sqrt(sum(x^2) / H + 1e-5)), the sum
+ * taken in fp64 in a fixed order: element i goes to partial (i/8) mod 64,
+ * each partial adds in increasing i, and the partials combine by a xor
+ * butterfly over offsets 32, 16, 8, 4, 2, 1.
+ */
+int lacache_rmsnorm_quant(void* stream, const uint16_t* x, const uint16_t* norm_w, uint8_t* xq, float* xs,
+                          int64_t M, int64_t H, int group);
+
+/*
+ * FP8 gate/up GEMM with per-group dequantization, fused SwiGLU and 1x128
+ * re-quantization (Sec. 3.4: quantization fused with the SwiGLU before the
+ * ffout linear).
+ *   xq, xs  as produced by lacache_rmsnorm_quant                   (input)
+ *   wgu_q   [2I x H] e4m3, wgu_s [2I/128 x H/128] fp32             (input)
+ *   hq      [M x I] e4m3, hs [I/128 x M] fp32                      (output)
+ *   h_tap   [M x I] fp32 or NULL: if non-NULL, also receives the fp32 h that
+ *           was quantized (a test hook; same kernel, one more store)
+ * acc[m,n] = sum_kb (xs[kb,m] * wgu_s[n/128,kb]) * dot_kb(xq[m,:], wgu_q[n,:])
+ * accumulated in fp32; h = SiLU(acc[:, j]) * acc[:, I + j].
+ */
+int lacache_gateup_swiglu_quant(void* stream, const uint8_t* xq, const float* xs, const uint8_t* wgu_q,
+                                const float* wgu_s, uint8_t* hq, float* hs, float* h_tap,
+                                int64_t M, int64_t H, int64_t I, int group);
+
+/*
+ * FP8 down (ffout) GEMM with per-group dequantization to bf16 (Sec. 3.4).
+ *   hq, hs  as produced by lacache_gateup_swiglu_quant             (input)
+ *   wd_q    [H x I] e4m3, wd_s [H/128 x I/128] fp32                (input)
+ *   out     [M x H] bf16, rounded to nearest-even from fp32         (output)
+ *   out_tap [M x H] fp32 or NULL: if non-NULL, also receives the fp32 value
+ *           that was rounded (test hook)
+ */
+int lacache_down_proj(void* stream, const uint8_t* hq, const float* hs, const uint8_t* wd_q, const float* wd_s,
+                      uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I, int group);
+
+/*
+ * The whole FP8 FFN of one layer: the three stages above in one call.
+ *   x [M x H] bf16, norm_w [H] bf16, wgu_q/wgu_s and wd_q/wd_s as produced by
+ *   lacache_quant_weights, out [M x H] bf16.
+ * The intermediates (xq, xs, hq, hs and partial sums) live in a workspace
+ * that the library allocates on first use per device, grows when a larger
+ * call needs it, and keeps until lacache_release_workspace(). Calls that
+ * share a device must therefore be serialized (one stream, or the caller's
+ * own ordering); concurrent callers use lacache_ffn_fp8_ws instead.
+ */
+int lacache_ffn_fp8(void* stream, const uint16_t* x, const uint16_t* norm_w, const uint8_t* wgu_q,
+                    const float* wgu_s, const uint8_t* wd_q, const float* wd_s, uint16_t* out,
+                    int64_t M, int64_t H, int64_t I, int group);
+
+/* Bytes of workspace lacache_ffn_fp8_ws needs for this shape (0 on bad arguments). */
+size_t lacache_ffn_workspace_bytes(int64_t M, int64_t H, int64_t I, int group);
+
+/* lacache_ffn_fp8 with a caller-owned workspace of at least
+ * lacache_ffn_workspace_bytes() bytes (256-byte aligned device memory). */
+int lacache_ffn_fp8_ws(void* stream, const uint16_t* x, const uint16_t* norm_w, const uint8_t* wgu_q,
+                       const float* wgu_s, const uint8_t* wd_q, const float* wd_s, uint16_t* out,
+                       int64_t M, int64_t H, int64_t I, int group, void* workspace, size_t ws_bytes);
+
+/* Residual add between stacked layers: x[i] = RNE_bf16(float(x[i]) + float(y[i])), i < n. */
+int lacache_add_bf16(void* stream, uint16_t* x_inout, const uint16_t* y, int64_t n);
+
+/* Test hook: the device e4m3 encoder applied elementwise, codes[i] = E(v[i]),
+ * i < n (E clips to +-448 and rounds to nearest-even; NaN inputs give NaN codes). */
+int lacache_encode_e4m3(void* stream, const float* v, uint8_t* codes, int64_t n);
+
+/*
+ * Kernel-path policy for the GEMM stages, process-wide:
+ *   0 = automatic (the skinny weight-streaming kernels for M <= 64, the tiled
+ *       MFMA kernels above), 1 = always skinny (M <= 64 only; larger M returns
+ *       LACACHE_ERR_UNSUPPORTED), 2 = always tiled.
+ * Returns the previous policy, or LACACHE_ERR_INVALID_ARG for other values.
+ */
+int lacache_set_path_policy(int policy);
+
+/* Human-readable name of a status code (static string). */
+const char* lacache_status_string(int status);
+
+/* Frees the library-owned workspace of every device (synchronizes each). */
+void lacache_release_workspace(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LACACHE_H */

@@ -1,0 +1,150 @@
+"""MI355X (gfx950) per-group FP8 FFN of LaCache (arxiv 2607.16339, Sec. 3.4).
+
+The Python functions carry the names of the C ABI (include/lacache.h) and take
+torch device tensors; they check dtypes, devices and shapes, derive the sizes,
+pass raw pointers and the current HIP stream, and raise ``LacacheError`` on a
+non-OK status. Every step of the FFN runs in the library's HIP kernels.
+"""
+
+import torch
+
+from ._lib import (LACACHE_ERR_ALLOC, LACACHE_ERR_HIP, LACACHE_ERR_INVALID_ARG, LACACHE_ERR_UNSUPPORTED,  # noqa: F401
+                   LACACHE_OK, LacacheError, check, lib, status_string)
+
+GROUP = 128
+_U8 = (torch.uint8, torch.float8_e4m3fn)
+_BF16 = (torch.bfloat16, torch.int16, torch.uint16)
+
+
+def _stream(stream, *tensors):
+    if stream is not None:
+        return int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
+    dev = tensors[0].device if tensors else None
+    return int(torch.cuda.current_stream(dev).cuda_stream)
+
+
+def _ptr(t, dtypes, name, shape=None, optional=False):
+    if t is None:
+        if optional:
+            return None
+        raise ValueError("%s is required" % name)
+    if t.device.type != "cuda":
+        raise ValueError("%s must be a device tensor" % name)
+    if t.dtype not in dtypes:
+        raise ValueError("%s: dtype %s not in %s" % (name, t.dtype, dtypes))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError("%s: shape %s, expected %s" % (name, tuple(t.shape), tuple(shape)))
+    return t.data_ptr()
+
+
+def lacache_quant_weights(w, w_q, w_s, group=GROUP, stream=None):
+    """128x128 block quantization: w [N, K] bf16 -> w_q [N, K] e4m3, w_s [N/128, K/128] fp32."""
+    N, K = w.shape
+    check(lib().lacache_quant_weights(
+        _stream(stream, w), _ptr(w, _BF16, "w"), _ptr(w_q, _U8, "w_q", (N, K)),
+        _ptr(w_s, (torch.float32,), "w_s", (N // group, K // group)), N, K, group), "lacache_quant_weights")
+
+
+def lacache_rmsnorm_quant(x, norm_w, xq, xs, group=GROUP, stream=None):
+    """x [M, H] bf16, norm_w [H] -> xq [M, H] e4m3, xs [H/128, M] fp32."""
+    M, H = x.shape
+    check(lib().lacache_rmsnorm_quant(
+        _stream(stream, x), _ptr(x, _BF16, "x"), _ptr(norm_w, _BF16, "norm_w", (H,)), _ptr(xq, _U8, "xq", (M, H)),
+        _ptr(xs, (torch.float32,), "xs", (H // group, M)), M, H, group), "lacache_rmsnorm_quant")
+
+
+def lacache_gateup_swiglu_quant(xq, xs, wgu_q, wgu_s, hq, hs, h_tap=None, group=GROUP, stream=None):
+    """xq [M, H], wgu_q [2I, H] -> hq [M, I] e4m3, hs [I/128, M] fp32 (h_tap [M, I] fp32 optional)."""
+    M, H = xq.shape
+    I = wgu_q.shape[0] // 2
+    check(lib().lacache_gateup_swiglu_quant(
+        _stream(stream, xq), _ptr(xq, _U8, "xq"), _ptr(xs, (torch.float32,), "xs", (H // group, M)),
+        _ptr(wgu_q, _U8, "wgu_q", (2 * I, H)), _ptr(wgu_s, (torch.float32,), "wgu_s", (2 * I // group, H // group)),
+        _ptr(hq, _U8, "hq", (M, I)), _ptr(hs, (torch.float32,), "hs", (I // group, M)),
+        _ptr(h_tap, (torch.float32,), "h_tap", (M, I), optional=True), M, H, I, group),
+        "lacache_gateup_swiglu_quant")
+
+
+def lacache_down_proj(hq, hs, wd_q, wd_s, out, out_tap=None, group=GROUP, stream=None):
+    """hq [M, I], wd_q [H, I] -> out [M, H] bf16 (out_tap [M, H] fp32 optional)."""
+    M, I = hq.shape
+    H = wd_q.shape[0]
+    check(lib().lacache_down_proj(
+        _stream(stream, hq), _ptr(hq, _U8, "hq"), _ptr(hs, (torch.float32,), "hs", (I // group, M)),
+        _ptr(wd_q, _U8, "wd_q", (H, I)), _ptr(wd_s, (torch.float32,), "wd_s", (H // group, I // group)),
+        _ptr(out, _BF16, "out", (M, H)), _ptr(out_tap, (torch.float32,), "out_tap", (M, H), optional=True),
+        M, H, I, group), "lacache_down_proj")
+
+
+def _ffn_args(x, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, group):
+    M, H = x.shape
+    I = wd_q.shape[1]
+    return [_ptr(x, _BF16, "x"), _ptr(norm_w, _BF16, "norm_w", (H,)), _ptr(wgu_q, _U8, "wgu_q", (2 * I, H)),
+            _ptr(wgu_s, (torch.float32,), "wgu_s", (2 * I // group, H // group)), _ptr(wd_q, _U8, "wd_q", (H, I)),
+            _ptr(wd_s, (torch.float32,), "wd_s", (H // group, I // group)), _ptr(out, _BF16, "out", (M, H)),
+            M, H, I, group]
+
+
+def lacache_ffn_fp8(x, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, group=GROUP, stream=None):
+    """The whole FP8 FFN of one layer: x [M, H] bf16 -> out [M, H] bf16."""
+    check(lib().lacache_ffn_fp8(_stream(stream, x), *_ffn_args(x, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, group)),
+          "lacache_ffn_fp8")
+
+
+def lacache_ffn_workspace_bytes(M, H, I, group=GROUP):
+    return int(lib().lacache_ffn_workspace_bytes(M, H, I, group))
+
+
+def lacache_ffn_fp8_ws(x, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, workspace, group=GROUP, stream=None):
+    """lacache_ffn_fp8 with a caller-owned uint8 workspace tensor."""
+    check(lib().lacache_ffn_fp8_ws(_stream(stream, x), *_ffn_args(x, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, group),
+                                   _ptr(workspace, (torch.uint8,), "workspace"), workspace.numel()),
+          "lacache_ffn_fp8_ws")
+
+
+def lacache_add_bf16(x_inout, y, stream=None):
+    """x_inout += y in bf16 (fp32 add, nearest-even rounding)."""
+    check(lib().lacache_add_bf16(_stream(stream, x_inout), _ptr(x_inout, _BF16, "x_inout"),
+                                 _ptr(y, _BF16, "y", tuple(x_inout.shape)), x_inout.numel()), "lacache_add_bf16")
+
+
+def lacache_encode_e4m3(v, codes, stream=None):
+    """Device e4m3 encoder (test hook): codes = E(v), elementwise."""
+    check(lib().lacache_encode_e4m3(_stream(stream, v), _ptr(v, (torch.float32,), "v"),
+                                    _ptr(codes, _U8, "codes", tuple(v.shape)), v.numel()), "lacache_encode_e4m3")
+
+
+def lacache_set_path_policy(policy):
+    """0 = automatic, 1 = skinny kernels (M <= 64), 2 = tiled kernels. Returns the previous policy."""
+    r = lib().lacache_set_path_policy(int(policy))
+    if r < 0:
+        raise LacacheError(r, "lacache_set_path_policy")
+    return r
+
+
+def lacache_status_string(status):
+    return status_string(status)
+
+
+def lacache_release_workspace():
+    lib().lacache_release_workspace()
+
+
+# ---- allocation conveniences (torch allocates; the library computes) -------
+
+def quantize_weights(w, group=GROUP, stream=None):
+    """Returns (w_q uint8 [N, K], w_s fp32 [N/128, K/128]) for a bf16 weight."""
+    N, K = w.shape
+    w_q = torch.empty((N, K), dtype=torch.uint8, device=w.device)
+    w_s = torch.empty((N // group, K // group), dtype=torch.float32, device=w.device)
+    lacache_quant_weights(w, w_q, w_s, group, stream)
+    return w_q, w_s
+
+
+def ffn_fp8(x, norm_w, wgu_q, wgu_s, wd_q, wd_s, group=GROUP, stream=None):
+    """Allocates out and runs lacache_ffn_fp8."""
+    out = torch.empty(x.shape, dtype=torch.bfloat16, device=x.device)
+    lacache_ffn_fp8(x, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, group, stream)
+    return out

@@ -1,0 +1,379 @@
+// C ABI of the FP8 FFN library (declared in include/lacache.h): host-side
+// argument validation, the library-owned workspace and kernel-path dispatch.
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cstdint>
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+#include <vector>
+
+#include "../../include/lacache.h"
+#include "launch.h"
+
+namespace {
+
+using namespace lacache;
+
+constexpr int64_t kGroup = 128;  // the only supported group size (1x128 and 128x128)
+constexpr int64_t kMaxH = 16384;
+constexpr int64_t kMaxI = 65536;
+constexpr int64_t kMaxM = int64_t(1) << 24;
+constexpr int64_t kMaxN = 2 * kMaxI;
+
+std::atomic<int> g_policy{0};
+
+size_t align256(size_t b) { return (b + 255) / 256 * 256; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+struct Range {
+  uintptr_t lo, hi;  // [lo, hi)
+};
+Range rng(const void* p, size_t bytes) {
+  const uintptr_t a = reinterpret_cast<uintptr_t>(p);
+  return {a, a + bytes};
+}
+bool overlap(Range a, Range b) { return a.lo < b.hi && b.lo < a.hi; }
+
+// Outputs must not overlap inputs (or each other).
+bool disjoint(std::initializer_list<Range> outs, std::initializer_list<Range> ins) {
+  std::vector<Range> o(outs), i(ins);
+  for (size_t a = 0; a < o.size(); ++a) {
+    if (o[a].hi == o[a].lo) continue;
+    for (const Range& b : i)
+      if (b.hi != b.lo && overlap(o[a], b)) return false;
+    for (size_t b = a + 1; b < o.size(); ++b)
+      if (o[b].hi != o[b].lo && overlap(o[a], o[b])) return false;
+  }
+  return true;
+}
+
+int check_group(int group) { return group == kGroup ? LACACHE_OK : LACACHE_ERR_UNSUPPORTED; }
+
+int check_dim(int64_t d, int64_t max) {
+  if (d <= 0 || d % kGroup != 0) return LACACHE_ERR_INVALID_ARG;
+  if (d > max) return LACACHE_ERR_UNSUPPORTED;
+  return LACACHE_OK;
+}
+
+int check_m(int64_t M) {
+  if (M < 0) return LACACHE_ERR_INVALID_ARG;
+  if (M > kMaxM) return LACACHE_ERR_UNSUPPORTED;
+  return LACACHE_OK;
+}
+
+#define RETURN_IF(x)                  \
+  do {                                \
+    const int s_ = (x);               \
+    if (s_ != LACACHE_OK) return s_;  \
+  } while (0)
+
+bool ptrs_ok(std::initializer_list<const void*> ps) {
+  for (const void* p : ps)
+    if (p == nullptr || !aligned16(p)) return false;
+  return true;
+}
+bool opt_ptr_ok(const void* p) { return p == nullptr || aligned16(p); }
+
+int hip_status(hipError_t e) { return e == hipSuccess ? LACACHE_OK : LACACHE_ERR_HIP; }
+
+// Kernel path for the GEMM stages.
+enum class Path { kSkinny, kTiled };
+int choose_path(int64_t M, Path* p) {
+  const int pol = g_policy.load();
+  if (pol == 1) {
+    if (M > kSkinnyMaxM) return LACACHE_ERR_UNSUPPORTED;
+    *p = Path::kSkinny;
+  } else if (pol == 2) {
+    *p = Path::kTiled;
+  } else {
+    *p = M <= kSkinnyMaxM ? Path::kSkinny : Path::kTiled;
+  }
+  return LACACHE_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Library-owned workspace: one grow-only device buffer per device, zero-filled
+// when (re)allocated.
+// ---------------------------------------------------------------------------
+struct DeviceWs {
+  void* ptr = nullptr;
+  size_t bytes = 0;
+};
+std::mutex g_ws_mu;
+std::vector<DeviceWs> g_ws;
+
+__global__ void zero_fill_kernel(uint32_t* p, size_t n) {
+  const size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0u;
+}
+
+hipError_t zero_fill(hipStream_t st, void* p, size_t bytes) {
+  const size_t n = bytes / 4;
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(zero_fill_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, st,
+                     static_cast<uint32_t*>(p), n);
+  return hipGetLastError();
+}
+
+// Returns a workspace of at least `bytes` on the current device.
+int get_workspace(hipStream_t st, size_t bytes, void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return LACACHE_ERR_HIP;
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  if (static_cast<size_t>(dev) >= g_ws.size()) g_ws.resize(dev + 1);
+  DeviceWs& w = g_ws[dev];
+  if (w.bytes < bytes) {
+    const char* force_fail = std::getenv("LACACHE_TEST_FAIL_ALLOC");
+    if (force_fail != nullptr && force_fail[0] == '1') return LACACHE_ERR_ALLOC;
+    if (w.ptr != nullptr) {
+      // earlier calls on any stream may still use the old buffer
+      if (hipDeviceSynchronize() != hipSuccess) return LACACHE_ERR_HIP;
+      if (hipFree(w.ptr) != hipSuccess) return LACACHE_ERR_HIP;
+      w.ptr = nullptr;
+      w.bytes = 0;
+    }
+    void* p = nullptr;
+    if (hipMalloc(&p, bytes) != hipSuccess) return LACACHE_ERR_ALLOC;
+    if (zero_fill(st, p, bytes) != hipSuccess) {
+      (void)hipFree(p);
+      return LACACHE_ERR_HIP;
+    }
+    w.ptr = p;
+    w.bytes = bytes;
+  }
+  *out = w.ptr;
+  return LACACHE_OK;
+}
+
+// Workspace layout (every region 256-byte aligned):
+//   [skinny counters: kSkinnyCounterBytes, always present, always at offset 0]
+//   [skinny h buffer: M x I fp32, only when M <= kSkinnyMaxM]
+//   [xq: M x H][xs: H/128 x M fp32][hq: M x I][hs: I/128 x M fp32]
+// The counters sit at the same place for every shape, so the library-owned
+// workspace keeps them zero between calls (zero-filled on allocation, re-armed
+// by the kernel); a caller-owned workspace is cleared by the norm kernel.
+struct FfnWs {
+  void* skinny;  // counters followed by the h buffer
+  uint8_t* xq;
+  float* xs;
+  uint8_t* hq;
+  float* hs;
+  size_t total;
+};
+FfnWs ffn_layout(void* base, int64_t M, int64_t H, int64_t I) {
+  FfnWs w{};
+  char* b = static_cast<char*>(base);
+  size_t off = 0;
+  w.skinny = b;
+  off += M <= kSkinnyMaxM ? skinny_gateup_ws_bytes(M, I) : kSkinnyCounterBytes;
+  w.xq = reinterpret_cast<uint8_t*>(b + off);
+  off += align256(static_cast<size_t>(M * H));
+  w.xs = reinterpret_cast<float*>(b + off);
+  off += align256(static_cast<size_t>(H / kGroup * M) * 4);
+  w.hq = reinterpret_cast<uint8_t*>(b + off);
+  off += align256(static_cast<size_t>(M * I));
+  w.hs = reinterpret_cast<float*>(b + off);
+  off += align256(static_cast<size_t>(I / kGroup * M) * 4);
+  w.total = off;
+  return w;
+}
+
+int run_gateup(hipStream_t st, Path path, const uint8_t* xq, const float* xs, const uint8_t* wq, const float* ws,
+               uint8_t* hq, float* hs, float* tap, int64_t M, int64_t H, int64_t I, void* skinny_ws) {
+  if (path == Path::kSkinny)
+    return hip_status(launch_gateup_skinny(st, xq, xs, wq, ws, hq, hs, tap, M, H, I, skinny_ws));
+  return hip_status(launch_gateup_tiled(st, xq, xs, wq, ws, hq, hs, tap, M, H, I));
+}
+
+int run_down(hipStream_t st, Path path, const uint8_t* hq, const float* hs, const uint8_t* wq, const float* ws,
+             uint16_t* out, float* tap, int64_t M, int64_t H, int64_t I) {
+  if (path == Path::kSkinny) return hip_status(launch_down_skinny(st, hq, hs, wq, ws, out, tap, M, H, I));
+  return hip_status(launch_down_tiled(st, hq, hs, wq, ws, out, tap, M, H, I));
+}
+
+int validate_ffn(const uint16_t* x, const uint16_t* norm_w, const uint8_t* wgu_q, const float* wgu_s,
+                 const uint8_t* wd_q, const float* wd_s, uint16_t* out, int64_t M, int64_t H, int64_t I, int group) {
+  RETURN_IF(check_group(group));
+  RETURN_IF(check_m(M));
+  RETURN_IF(check_dim(H, kMaxH));
+  RETURN_IF(check_dim(I, kMaxI));
+  if (M == 0) return LACACHE_OK;  // nothing to read or write: pointers are not looked at
+  if (!ptrs_ok({x, norm_w, wgu_q, wgu_s, wd_q, wd_s, out})) return LACACHE_ERR_INVALID_ARG;
+  const size_t mh = static_cast<size_t>(M * H);
+  if (!disjoint({rng(out, mh * 2)},
+                {rng(x, mh * 2), rng(norm_w, H * 2), rng(wgu_q, 2 * I * H), rng(wgu_s, (2 * I / 128) * (H / 128) * 4),
+                 rng(wd_q, H * I), rng(wd_s, (H / 128) * (I / 128) * 4)}))
+    return LACACHE_ERR_INVALID_ARG;
+  return LACACHE_OK;
+}
+
+int ffn_core(hipStream_t st, const uint16_t* x, const uint16_t* norm_w, const uint8_t* wgu_q, const float* wgu_s,
+             const uint8_t* wd_q, const float* wd_s, uint16_t* out, int64_t M, int64_t H, int64_t I, Path path,
+             const FfnWs& w) {
+  // The norm kernel clears the skinny gate/up counters on its way (a
+  // caller-owned workspace may hold anything).
+  uint32_t* clear = path == Path::kSkinny ? static_cast<uint32_t*>(w.skinny) : nullptr;
+  if (launch_rmsnorm_quant(st, x, norm_w, w.xq, w.xs, M, H, clear, static_cast<int>(I / kGroup)) != hipSuccess)
+    return LACACHE_ERR_HIP;
+  RETURN_IF(run_gateup(st, path, w.xq, w.xs, wgu_q, wgu_s, w.hq, w.hs, nullptr, M, H, I, w.skinny));
+  return run_down(st, path, w.hq, w.hs, wd_q, wd_s, out, nullptr, M, H, I);
+}
+
+}  // namespace
+
+extern "C" {
+
+int lacache_quant_weights(void* stream, const uint16_t* w, uint8_t* w_q, float* w_s, int64_t N, int64_t K,
+                          int group) {
+  RETURN_IF(check_group(group));
+  RETURN_IF(check_dim(N, kMaxN));
+  RETURN_IF(check_dim(K, kMaxN));
+  if (!ptrs_ok({w, w_q, w_s})) return LACACHE_ERR_INVALID_ARG;
+  if (!disjoint({rng(w_q, N * K), rng(w_s, (N / 128) * (K / 128) * 4)}, {rng(w, N * K * 2)}))
+    return LACACHE_ERR_INVALID_ARG;
+  return hip_status(launch_quant_weights(static_cast<hipStream_t>(stream), w, w_q, w_s, N, K));
+}
+
+int lacache_rmsnorm_quant(void* stream, const uint16_t* x, const uint16_t* norm_w, uint8_t* xq, float* xs,
+                          int64_t M, int64_t H, int group) {
+  RETURN_IF(check_group(group));
+  RETURN_IF(check_m(M));
+  RETURN_IF(check_dim(H, kMaxH));
+  if (M == 0) return LACACHE_OK;
+  if (!ptrs_ok({x, norm_w, xq, xs})) return LACACHE_ERR_INVALID_ARG;
+  if (!disjoint({rng(xq, M * H), rng(xs, (H / 128) * M * 4)}, {rng(x, M * H * 2), rng(norm_w, H * 2)}))
+    return LACACHE_ERR_INVALID_ARG;
+  return hip_status(launch_rmsnorm_quant(static_cast<hipStream_t>(stream), x, norm_w, xq, xs, M, H));
+}
+
+int lacache_gateup_swiglu_quant(void* stream, const uint8_t* xq, const float* xs, const uint8_t* wgu_q,
+                                const float* wgu_s, uint8_t* hq, float* hs, float* h_tap, int64_t M, int64_t H,
+                                int64_t I, int group) {
+  RETURN_IF(check_group(group));
+  RETURN_IF(check_m(M));
+  RETURN_IF(check_dim(H, kMaxH));
+  RETURN_IF(check_dim(I, kMaxI));
+  Path path;
+  RETURN_IF(choose_path(M, &path));
+  if (M == 0) return LACACHE_OK;
+  if (!ptrs_ok({xq, xs, wgu_q, wgu_s, hq, hs}) || !opt_ptr_ok(h_tap)) return LACACHE_ERR_INVALID_ARG;
+  if (!disjoint({rng(hq, M * I), rng(hs, (I / 128) * M * 4), rng(h_tap, h_tap ? M * I * 4 : 0)},
+                {rng(xq, M * H), rng(xs, (H / 128) * M * 4), rng(wgu_q, 2 * I * H),
+                 rng(wgu_s, (2 * I / 128) * (H / 128) * 4)}))
+    return LACACHE_ERR_INVALID_ARG;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  void* skinny = nullptr;
+  if (path == Path::kSkinny) {
+    // counters at offset 0 of the library workspace: zero since allocation,
+    // re-armed by every skinny gate/up kernel
+    RETURN_IF(get_workspace(st, skinny_gateup_ws_bytes(M, I), &skinny));
+  }
+  return run_gateup(st, path, xq, xs, wgu_q, wgu_s, hq, hs, h_tap, M, H, I, skinny);
+}
+
+int lacache_down_proj(void* stream, const uint8_t* hq, const float* hs, const uint8_t* wd_q, const float* wd_s,
+                      uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I, int group) {
+  RETURN_IF(check_group(group));
+  RETURN_IF(check_m(M));
+  RETURN_IF(check_dim(H, kMaxH));
+  RETURN_IF(check_dim(I, kMaxI));
+  Path path;
+  RETURN_IF(choose_path(M, &path));
+  if (M == 0) return LACACHE_OK;
+  if (!ptrs_ok({hq, hs, wd_q, wd_s, out}) || !opt_ptr_ok(out_tap)) return LACACHE_ERR_INVALID_ARG;
+  if (!disjoint({rng(out, M * H * 2), rng(out_tap, out_tap ? M * H * 4 : 0)},
+                {rng(hq, M * I), rng(hs, (I / 128) * M * 4), rng(wd_q, H * I), rng(wd_s, (H / 128) * (I / 128) * 4)}))
+    return LACACHE_ERR_INVALID_ARG;
+  return run_down(static_cast<hipStream_t>(stream), path, hq, hs, wd_q, wd_s, out, out_tap, M, H, I);
+}
+
+size_t lacache_ffn_workspace_bytes(int64_t M, int64_t H, int64_t I, int group) {
+  if (check_group(group) != LACACHE_OK || check_m(M) != LACACHE_OK || check_dim(H, kMaxH) != LACACHE_OK ||
+      check_dim(I, kMaxI) != LACACHE_OK)
+    return 0;
+  return ffn_layout(nullptr, M, H, I).total;
+}
+
+int lacache_ffn_fp8(void* stream, const uint16_t* x, const uint16_t* norm_w, const uint8_t* wgu_q,
+                    const float* wgu_s, const uint8_t* wd_q, const float* wd_s, uint16_t* out, int64_t M, int64_t H,
+                    int64_t I, int group) {
+  RETURN_IF(validate_ffn(x, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, M, H, I, group));
+  Path path;
+  RETURN_IF(choose_path(M, &path));
+  if (M == 0) return LACACHE_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  void* base = nullptr;
+  RETURN_IF(get_workspace(st, ffn_layout(nullptr, M, H, I).total, &base));
+  return ffn_core(st, x, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, M, H, I, path, ffn_layout(base, M, H, I));
+}
+
+int lacache_ffn_fp8_ws(void* stream, const uint16_t* x, const uint16_t* norm_w, const uint8_t* wgu_q,
+                       const float* wgu_s, const uint8_t* wd_q, const float* wd_s, uint16_t* out, int64_t M,
+                       int64_t H, int64_t I, int group, void* workspace, size_t ws_bytes) {
+  RETURN_IF(validate_ffn(x, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, M, H, I, group));
+  Path path;
+  RETURN_IF(choose_path(M, &path));
+  if (M == 0) return LACACHE_OK;
+  const FfnWs lay = ffn_layout(workspace, M, H, I);
+  if (workspace == nullptr || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0 || ws_bytes < lay.total)
+    return LACACHE_ERR_INVALID_ARG;
+  const size_t mh = static_cast<size_t>(M * H);
+  if (!disjoint({rng(workspace, lay.total)},
+                {rng(x, mh * 2), rng(out, mh * 2), rng(norm_w, H * 2), rng(wgu_q, 2 * I * H),
+                 rng(wgu_s, (2 * I / 128) * (H / 128) * 4), rng(wd_q, H * I), rng(wd_s, (H / 128) * (I / 128) * 4)}))
+    return LACACHE_ERR_INVALID_ARG;
+  return ffn_core(static_cast<hipStream_t>(stream), x, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, M, H, I, path, lay);
+}
+
+int lacache_add_bf16(void* stream, uint16_t* x_inout, const uint16_t* y, int64_t n) {
+  if (n < 0) return LACACHE_ERR_INVALID_ARG;
+  if (n == 0) return LACACHE_OK;
+  if (!ptrs_ok({x_inout, y})) return LACACHE_ERR_INVALID_ARG;
+  if (overlap(rng(x_inout, n * 2), rng(y, n * 2))) return LACACHE_ERR_INVALID_ARG;
+  return hip_status(launch_add_bf16(static_cast<hipStream_t>(stream), x_inout, y, n));
+}
+
+int lacache_encode_e4m3(void* stream, const float* v, uint8_t* codes, int64_t n) {
+  if (n < 0) return LACACHE_ERR_INVALID_ARG;
+  if (n > (int64_t(1) << 32)) return LACACHE_ERR_UNSUPPORTED;
+  if (n == 0) return LACACHE_OK;
+  if (!ptrs_ok({v, codes})) return LACACHE_ERR_INVALID_ARG;
+  if (overlap(rng(v, n * 4), rng(codes, n))) return LACACHE_ERR_INVALID_ARG;
+  return hip_status(launch_encode_e4m3(static_cast<hipStream_t>(stream), v, codes, n));
+}
+
+int lacache_set_path_policy(int policy) {
+  if (policy < 0 || policy > 2) return LACACHE_ERR_INVALID_ARG;
+  return g_policy.exchange(policy);
+}
+
+const char* lacache_status_string(int status) {
+  switch (status) {
+    case LACACHE_OK: return "LACACHE_OK";
+    case LACACHE_ERR_INVALID_ARG: return "LACACHE_ERR_INVALID_ARG";
+    case LACACHE_ERR_UNSUPPORTED: return "LACACHE_ERR_UNSUPPORTED";
+    case LACACHE_ERR_HIP: return "LACACHE_ERR_HIP";
+    case LACACHE_ERR_ALLOC: return "LACACHE_ERR_ALLOC";
+    default: return "LACACHE_UNKNOWN_STATUS";
+  }
+}
+
+void lacache_release_workspace(void) {
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  int cur = 0;
+  const bool have_cur = hipGetDevice(&cur) == hipSuccess;
+  for (size_t d = 0; d < g_ws.size(); ++d) {
+    if (g_ws[d].ptr == nullptr) continue;
+    if (hipSetDevice(static_cast<int>(d)) == hipSuccess) {
+      (void)hipDeviceSynchronize();
+      (void)hipFree(g_ws[d].ptr);
+    }
+    g_ws[d] = DeviceWs{};
+  }
+  if (have_cur) (void)hipSetDevice(cur);
+}
+
+}  // extern "C"

@@ -1,0 +1,81 @@
+// Device helpers for the gfx950 FP8 FFN kernels: e4m3 encoding, bf16
+// conversion, the FP8 MFMA and wavefront reductions.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lacache {
+
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+constexpr int kGroup = 128;      // quantization group (1x128 activations, 128x128 weights)
+constexpr float kE4M3Max = 448.0f;
+
+// ---------------------------------------------------------------------------
+// e4m3fn encoding: clip to [-448, 448] (Eq. 7), then the hardware's
+// round-to-nearest-even conversion. The conversion itself does not saturate
+// (values above 464 become the NaN code), so the clip must come first. The
+// clip keeps the sign of zero, so -0 encodes to 0x80.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float clip448(float v) {
+  return __builtin_fminf(__builtin_fmaxf(v, -kE4M3Max), kE4M3Max);
+}
+
+// Four values -> four codes packed little-endian into one 32-bit word.
+__device__ __forceinline__ uint32_t enc4_e4m3(float a, float b, float c, float d) {
+  int w = __builtin_amdgcn_cvt_pk_fp8_f32(clip448(a), clip448(b), 0, false);
+  w = __builtin_amdgcn_cvt_pk_fp8_f32(clip448(c), clip448(d), w, true);
+  return static_cast<uint32_t>(w);
+}
+
+__device__ __forceinline__ uint32_t enc1_e4m3(float a) {
+  return static_cast<uint32_t>(__builtin_amdgcn_cvt_pk_fp8_f32(clip448(a), 0.0f, 0, false)) & 0xFFu;
+}
+
+// Group quantizer step for one value: code = E(RN32(y / s)), s > 0. The
+// division is IEEE-correctly rounded (the library is compiled with correctly
+// rounded fp32 division).
+__device__ __forceinline__ float qdiv(float y, float s) { return y / s; }
+
+// ---------------------------------------------------------------------------
+// bf16 <-> fp32
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float bf16lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// Round to nearest, ties to even; NaN -> quiet NaN.
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return 0x7FC0u;
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return f32_to_bf16(lo) | (f32_to_bf16(hi) << 16);
+}
+
+// ---------------------------------------------------------------------------
+// FP8 x FP8 -> fp32 MFMA, 16x16 output, 128-deep K (exactly one K-group).
+// Operand layout (per lane l of the wavefront): A row l%16, B column l%16,
+// 32 bytes of K each; A and B must place K identically. Output: lane l holds
+// D[4*(l/16) + r][l%16] in element r. Zero scale operands select the
+// unscaled FP8 (e4m3, format 0) instruction.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ v4f mfma_fp8_16x16x128(v8i a, v8i b, v4f c) {
+  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
+}
+
+// ---------------------------------------------------------------------------
+// Wavefront reductions (max is exact, so order does not matter)
+// ---------------------------------------------------------------------------
+template <int kWidth>
+__device__ __forceinline__ float max_xor(float v) {
+#pragma unroll
+  for (int o = kWidth / 2; o >= 1; o >>= 1) v = __builtin_fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+}  // namespace lacache

@@ -1,0 +1,196 @@
+// Quantization kernels: 128x128 weight blocks, the fused RMSNorm + 1x128
+// activation quantizer, the residual add and the encoder test hook.
+// Paper: LaCache (arxiv 2607.16339), Sec. 3.4, Eqs. 7-8.
+#include "device.h"
+#include "launch.h"
+
+namespace lacache {
+
+// ---------------------------------------------------------------------------
+// 128x128 block weight quantization. One workgroup (256 threads) per block:
+// thread t owns row t/2 of the block, 64 consecutive elements (128 bytes).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void quant_weights_kernel(const uint16_t* __restrict__ w, uint8_t* __restrict__ wq,
+                                                            float* __restrict__ ws, int64_t K) {
+  __shared__ float red[4];
+  const int t = threadIdx.x;
+  const int64_t kb = blockIdx.x, nb = blockIdx.y;
+  const int64_t row = nb * kGroup + (t >> 1);
+  const int64_t col = kb * kGroup + (t & 1) * 64;
+  const uint4* src = reinterpret_cast<const uint4*>(w + row * K + col);
+  uint4 v[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = src[i];
+  float amax = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const uint32_t q[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      amax = __builtin_fmaxf(amax, __builtin_fmaxf(__builtin_fabsf(bf16lo(q[e])), __builtin_fabsf(bf16hi(q[e]))));
+  }
+  amax = max_xor<64>(amax);
+  if ((t & 63) == 0) red[t >> 6] = amax;
+  __syncthreads();
+  amax = __builtin_fmaxf(__builtin_fmaxf(red[0], red[1]), __builtin_fmaxf(red[2], red[3]));
+  const float s = amax / kE4M3Max;  // Eq. 8, rounded once to fp32
+  uint32_t out[16];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const uint32_t q[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      if (s == 0.0f) {
+        out[2 * i + h] = 0u;
+      } else {
+        out[2 * i + h] = enc4_e4m3(qdiv(bf16lo(q[2 * h]), s), qdiv(bf16hi(q[2 * h]), s),
+                                   qdiv(bf16lo(q[2 * h + 1]), s), qdiv(bf16hi(q[2 * h + 1]), s));
+      }
+    }
+  }
+  uint4* dst = reinterpret_cast<uint4*>(wq + row * K + col);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) dst[i] = make_uint4(out[4 * i], out[4 * i + 1], out[4 * i + 2], out[4 * i + 3]);
+  if (t == 0) ws[nb * (K / kGroup) + kb] = s;
+}
+
+hipError_t launch_quant_weights(hipStream_t st, const uint16_t* w, uint8_t* wq, float* ws, int64_t N, int64_t K) {
+  dim3 grid(static_cast<unsigned>(K / kGroup), static_cast<unsigned>(N / kGroup));
+  hipLaunchKernelGGL(quant_weights_kernel, grid, dim3(256), 0, st, w, wq, ws, K);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Fused RMSNorm + 1x128 quantization. One wavefront per row; lane l holds
+// chunks c = 64 t + l (8 bf16 each) for t < T, so a 128-wide group is the
+// 16 lanes 16g'..16g'+15 of one pass. The fp64 sum of squares follows the
+// fixed order: per-lane partials in increasing element index, then a xor
+// butterfly over offsets 32..1 (every lane ends with the same bits).
+// ---------------------------------------------------------------------------
+template <int T>
+__global__ __launch_bounds__(256) void rmsnorm_quant_kernel(const uint16_t* __restrict__ x,
+                                                            const uint16_t* __restrict__ nw,
+                                                            uint8_t* __restrict__ xq, float* __restrict__ xs,
+                                                            int64_t M, int H, uint32_t* __restrict__ clear,
+                                                            int clear_n) {
+  // Optional: zero a small counter block for the kernel that runs next.
+  if (clear != nullptr && blockIdx.x == 0)
+    for (int i = threadIdx.x; i < clear_n; i += 256) clear[i] = 0u;
+  const int lane = threadIdx.x & 63;
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (row >= M) return;  // uniform per wavefront; no workgroup barrier below
+  const int nchunk = H >> 3;
+  const uint4* xr = reinterpret_cast<const uint4*>(x + row * H);
+  const uint4* wr = reinterpret_cast<const uint4*>(nw);
+  uint4 xv[T];
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    const int c = t * 64 + lane;
+    xv[t] = c < nchunk ? xr[c] : make_uint4(0u, 0u, 0u, 0u);
+  }
+  double p = 0.0;
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    const uint32_t q[4] = {xv[t].x, xv[t].y, xv[t].z, xv[t].w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const double a = bf16lo(q[e]), b = bf16hi(q[e]);
+      p = p + a * a;  // the square of a bf16 value is exact in fp64
+      p = p + b * b;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) p = p + __shfl_xor(p, o, 64);
+  const float r = static_cast<float>(1.0 / __builtin_sqrt(p / static_cast<double>(H) + 1e-5));
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    const int c = t * 64 + lane;
+    const bool valid = c < nchunk;  // whole 16-lane groups share validity (H % 128 == 0)
+    const uint4 wv = valid ? wr[c] : make_uint4(0u, 0u, 0u, 0u);
+    const uint32_t q[4] = {xv[t].x, xv[t].y, xv[t].z, xv[t].w};
+    const uint32_t g[4] = {wv.x, wv.y, wv.z, wv.w};
+    float y[8];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      y[2 * e] = (bf16lo(q[e]) * bf16lo(g[e])) * r;  // x*w is exact in fp32; one rounding for *r
+      y[2 * e + 1] = (bf16hi(q[e]) * bf16hi(g[e])) * r;
+    }
+    float amax = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) amax = __builtin_fmaxf(amax, __builtin_fabsf(y[e]));
+    amax = max_xor<16>(amax);
+    const float s = amax / kE4M3Max;
+    uint32_t lo = 0u, hi = 0u;
+    if (s != 0.0f) {
+      lo = enc4_e4m3(qdiv(y[0], s), qdiv(y[1], s), qdiv(y[2], s), qdiv(y[3], s));
+      hi = enc4_e4m3(qdiv(y[4], s), qdiv(y[5], s), qdiv(y[6], s), qdiv(y[7], s));
+    }
+    if (valid) {
+      *reinterpret_cast<uint2*>(xq + row * H + 8 * c) = make_uint2(lo, hi);
+      if ((lane & 15) == 0) xs[static_cast<int64_t>(c >> 4) * M + row] = s;
+    }
+  }
+}
+
+hipError_t launch_rmsnorm_quant(hipStream_t st, const uint16_t* x, const uint16_t* nw, uint8_t* xq, float* xs,
+                                int64_t M, int64_t H, uint32_t* clear, int clear_n) {
+  const int T = static_cast<int>((H + 511) / 512);
+  dim3 grid(static_cast<unsigned>((M + 3) / 4)), block(256);
+  const int h = static_cast<int>(H);
+  if (T <= 1) hipLaunchKernelGGL(rmsnorm_quant_kernel<1>, grid, block, 0, st, x, nw, xq, xs, M, h, clear, clear_n);
+  else if (T <= 2) hipLaunchKernelGGL(rmsnorm_quant_kernel<2>, grid, block, 0, st, x, nw, xq, xs, M, h, clear, clear_n);
+  else if (T <= 4) hipLaunchKernelGGL(rmsnorm_quant_kernel<4>, grid, block, 0, st, x, nw, xq, xs, M, h, clear, clear_n);
+  else if (T <= 8) hipLaunchKernelGGL(rmsnorm_quant_kernel<8>, grid, block, 0, st, x, nw, xq, xs, M, h, clear, clear_n);
+  else if (T <= 16) hipLaunchKernelGGL(rmsnorm_quant_kernel<16>, grid, block, 0, st, x, nw, xq, xs, M, h, clear, clear_n);
+  else hipLaunchKernelGGL(rmsnorm_quant_kernel<32>, grid, block, 0, st, x, nw, xq, xs, M, h, clear, clear_n);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Residual add: x = RNE_bf16(float(x) + float(y)). 8 elements per thread.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void add_bf16_kernel(uint16_t* __restrict__ x, const uint16_t* __restrict__ y,
+                                                       int64_t n) {
+  const int64_t i8 = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 8;
+  if (i8 + 8 <= n) {
+    uint4 a = *reinterpret_cast<const uint4*>(x + i8);
+    const uint4 b = *reinterpret_cast<const uint4*>(y + i8);
+    uint32_t* pa = reinterpret_cast<uint32_t*>(&a);
+    const uint32_t* pb = reinterpret_cast<const uint32_t*>(&b);
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      pa[e] = pack_bf16x2(bf16lo(pa[e]) + bf16lo(pb[e]), bf16hi(pa[e]) + bf16hi(pb[e]));
+    *reinterpret_cast<uint4*>(x + i8) = a;
+  } else {
+    for (int64_t i = i8; i < n; ++i)
+      x[i] = static_cast<uint16_t>(f32_to_bf16(bf16lo(x[i]) + bf16lo(y[i])));
+  }
+}
+
+hipError_t launch_add_bf16(hipStream_t st, uint16_t* x, const uint16_t* y, int64_t n) {
+  const int64_t threads = (n + 7) / 8;
+  hipLaunchKernelGGL(add_bf16_kernel, dim3(static_cast<unsigned>((threads + 255) / 256)), dim3(256), 0, st, x, y, n);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Encoder test hook: codes[i] = E(v[i]).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void encode_kernel(const float* __restrict__ v, uint8_t* __restrict__ codes,
+                                                     int64_t n) {
+  const int64_t i4 = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 4;
+  if (i4 + 4 <= n) {
+    const float4 f = *reinterpret_cast<const float4*>(v + i4);
+    *reinterpret_cast<uint32_t*>(codes + i4) = enc4_e4m3(f.x, f.y, f.z, f.w);
+  } else {
+    for (int64_t i = i4; i < n; ++i) codes[i] = static_cast<uint8_t>(enc1_e4m3(v[i]));
+  }
+}
+
+hipError_t launch_encode_e4m3(hipStream_t st, const float* v, uint8_t* codes, int64_t n) {
+  const int64_t threads = (n + 3) / 4;
+  hipLaunchKernelGGL(encode_kernel, dim3(static_cast<unsigned>((threads + 255) / 256)), dim3(256), 0, st, v, codes, n);
+  return hipGetLastError();
+}
+
+}  // namespace lacache

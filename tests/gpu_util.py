@@ -1,0 +1,185 @@
+"""Helpers shared by the GPU parity tests: host<->device bf16 moves, seeded
+layers, and the acceptance checks against the oracle."""
+
+import numpy as np
+import torch
+
+import oracle.ffn as O
+import paper_2607_16339_amd as lc
+import synth
+from oracle.bf16 import rne_bf16
+from oracle.e4m3 import e4m3_decode, e4m3_encode
+
+DEV = torch.device("cuda:0")
+
+
+def dev_bf16(bits):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16).copy()).view(torch.bfloat16).to(DEV)
+
+
+def host_bf16(t):
+    return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def host(t):
+    return t.cpu().numpy()
+
+
+class Layer:
+    """Seeded bf16 weights of one layer, quantized by the library on the GPU."""
+
+    def __init__(self, w, layer=1, quantize=True):
+        self.w = w
+        self.bits = synth.make_weights(w, layer)
+        self.wgu_bits = np.concatenate([self.bits["w_gate"], self.bits["w_up"]], axis=0)
+        self.norm_w = dev_bf16(self.bits["norm_w"])
+        if quantize:
+            self.wgu_q, self.wgu_s = lc.quantize_weights(dev_bf16(self.wgu_bits))
+            self.wd_q, self.wd_s = lc.quantize_weights(dev_bf16(self.bits["w_down"]))
+            torch.cuda.synchronize()
+
+    def host_weights(self):
+        return host(self.wgu_q), host(self.wgu_s), host(self.wd_q), host(self.wd_s)
+
+
+def run_stages(x, layer, M, H, I, sentinel=True):
+    """Runs the three stage entry points with taps; returns device tensors."""
+    fill = 0xFF if sentinel else 0
+    t = {
+        "xq": torch.full((M, H), fill, dtype=torch.uint8, device=DEV),
+        "xs": torch.full((H // 128, M), float("nan"), dtype=torch.float32, device=DEV),
+        "hq": torch.full((M, I), fill, dtype=torch.uint8, device=DEV),
+        "hs": torch.full((I // 128, M), float("nan"), dtype=torch.float32, device=DEV),
+        "h_tap": torch.full((M, I), float("nan"), dtype=torch.float32, device=DEV),
+        "out": torch.full((M, H), float("nan"), dtype=torch.bfloat16, device=DEV),
+        "out_tap": torch.full((M, H), float("nan"), dtype=torch.float32, device=DEV),
+    }
+    lc.lacache_rmsnorm_quant(x, layer.norm_w, t["xq"], t["xs"])
+    lc.lacache_gateup_swiglu_quant(t["xq"], t["xs"], layer.wgu_q, layer.wgu_s, t["hq"], t["hs"], t["h_tap"])
+    lc.lacache_down_proj(t["hq"], t["hs"], layer.wd_q, layer.wd_s, t["out"], t["out_tap"])
+    torch.cuda.synchronize()
+    return t
+
+
+def check_norm_exact(xb_rows, norm_w_bits, xq_rows, xs_cols):
+    """xq / xs of the given rows equal the oracle's bit for bit."""
+    rxq, rxs = O.rmsnorm_quant(xb_rows, norm_w_bits)
+    assert np.array_equal(xq_rows, rxq), "xq differs in %d codes" % int((xq_rows != rxq).sum())
+    assert np.array_equal(xs_cols.view(np.uint32), rxs.view(np.uint32)), "xs differs"
+
+
+def check_requant_exact(h_tap_rows, hq_rows, hs_cols):
+    """The fused re-quantization equals the oracle's quantizer applied to the kernel's own fp32 h."""
+    assert np.all(np.isfinite(h_tap_rows)), "h tap has unwritten elements"
+    rhq, rhs = O.requant(h_tap_rows)
+    assert np.array_equal(hq_rows, rhq), "hq differs from requant(h_tap) in %d codes" % int((hq_rows != rhq).sum())
+    assert np.array_equal(hs_cols.view(np.uint32), rhs.view(np.uint32)), "hs differs from requant(h_tap)"
+
+
+# ---------------------------------------------------------------------------
+# Error model of the FP8 MFMA's 128-term dot product (measured on gfx950):
+# products are summed exactly only within chunks of 8 consecutive K; inside a
+# chunk each product is truncated toward zero to a multiple of
+# 2^(Emax - 13), Emax the chunk's largest exponent sum; chunk sums then add
+# with at least fp32 precision and the result is rounded to fp32. The bound
+# below takes the largest exponents over 16-wide K spans (each holds two
+# chunks), which can only over-estimate.
+# ---------------------------------------------------------------------------
+MFMA_WINDOW = 13
+MFMA_SPAN = 16
+
+
+def e4m3_exponent(codes):
+    """Unbiased exponent of each code's value (-6 for subnormals), -inf for zeros."""
+    c = np.asarray(codes, dtype=np.uint8) & np.uint8(0x7F)
+    e = (c >> 3).astype(np.float64)
+    ex = np.where(e == 0, -6.0, e - 7.0)
+    return np.where(c == 0, -np.inf, ex)
+
+
+def mfma_dot_bound(aq, bq):
+    """Per K-group bound on |P_hw - P_exact| (before fp32 rounding), a list of [M, N] arrays."""
+    M, K = aq.shape
+    N = bq.shape[0]
+    ea = np.exp2(e4m3_exponent(aq).reshape(M, K // MFMA_SPAN, MFMA_SPAN).max(axis=2))
+    eb = np.exp2(e4m3_exponent(bq).reshape(N, K // MFMA_SPAN, MFMA_SPAN).max(axis=2))
+    per = 128 // MFMA_SPAN
+    return [MFMA_SPAN * 2.0 ** -MFMA_WINDOW * (ea[:, kb * per:(kb + 1) * per] @ eb[:, kb * per:(kb + 1) * per].T)
+            for kb in range(K // 128)]
+
+
+def gemm_error_bound(aq, as_, bq, bs, extra_adds=16):
+    """Bound on |acc_gpu - acc_exact| for the per-group scaled GEMM: MFMA chunk
+    truncation, the fp32 rounding of each group result and of its scale
+    product, and the fp32 accumulation (KB adds plus extra_adds more)."""
+    M, K = aq.shape
+    KB = K // 128
+    dots = mfma_dot_bound(aq, bq)
+    bound = np.zeros((M, bq.shape[0]))
+    mag = np.zeros_like(bound)
+    for kb in range(KB):
+        cols = slice(kb * 128, (kb + 1) * 128)
+        P = np.abs(O.dequant_codes(aq[:, cols]) @ O.dequant_codes(bq[:, cols]).T)
+        s = np.abs(as_[kb].astype(np.float64))[:, None] * np.repeat(np.abs(bs[:, kb].astype(np.float64)), 128)[None, :]
+        bound += s * (dots[kb] + 2.0 ** -24 * P)
+        mag += s * P
+    return bound + (KB + extra_adds) * 2.0 ** -24 * mag
+
+
+SILU_LIP = 1.1  # max |SiLU'| = 1.0998
+
+
+def check_gateup_explained(xq_rows, xs_cols, wgu_q, wgu_s, I, hq_rows, hs_cols):
+    """Against the independent oracle (exact fp64 dot products): the GPU's
+    scales and codes must be those of some h within the error bound of the
+    exact h. Returns the fraction of codes that differ from the oracle's."""
+    r = O.gateup_swiglu_quant(xq_rows, xs_cols, wgu_q, wgu_s, I)
+    dacc = gemm_error_bound(xq_rows, xs_cols, wgu_q, wgu_s)
+    g, u = r["acc64"][:, :I], r["acc64"][:, I:]
+    dg, du = dacc[:, :I], dacc[:, I:]
+    h = r["h64"]
+    dh = SILU_LIP * dg * (np.abs(u) + du) + np.abs(O.silu(g)) * du
+    dh = dh + 2.0 ** -20 * (np.abs(h) + dh)  # fp32 SiLU/product in the epilogue
+    M = h.shape[0]
+    G = I // 128
+    ah = np.abs(h).reshape(M, G, 128)
+    dhg = dh.reshape(M, G, 128)
+    s_lo = np.maximum(ah - dhg, 0).max(axis=2) / 448 * (1 - 2.0 ** -23)
+    s_hi = (ah + dhg).max(axis=2) / 448 * (1 + 2.0 ** -23)
+    s_g = hs_cols.T.astype(np.float64)
+    assert np.all((s_g >= s_lo) & (s_g <= s_hi)), "group scale outside the error bound"
+    diff = hq_rows != r["hq"]
+    if diff.any():
+        s_lo_e = np.repeat(np.maximum(s_lo, 1e-300), 128, axis=1)
+        s_hi_e = np.repeat(s_hi, 128, axis=1)
+        h_lo, h_hi = h - dh, h + dh
+        # extreme quotients of h in [h_lo, h_hi] by s in [s_lo, s_hi]
+        cands = np.stack([h_lo / s_lo_e, h_lo / s_hi_e, h_hi / s_lo_e, h_hi / s_hi_e])
+        c_lo, c_hi = cands.min(axis=0), cands.max(axis=0)
+        v_lo = np.clip(c_lo - np.abs(c_lo) * 2.0 ** -22, -448, 448)  # the fp32 division's rounding
+        v_hi = np.clip(c_hi + np.abs(c_hi) * 2.0 ** -22, -448, 448)
+        lo = e4m3_decode(e4m3_encode(v_lo))
+        hi = e4m3_decode(e4m3_encode(v_hi))
+        got = e4m3_decode(hq_rows)
+        bad = diff & ~((got >= lo) & (got <= hi))
+        assert not bad.any(), "%d unexplained code mismatches (of %d) in %d rows" % (int(bad.sum()), int(diff.sum()), M)
+    return float(diff.mean())
+
+
+def check_down_same_operands(hq_rows, hs_cols, wd_q, wd_s, out_tap_rows, out_bits_rows, tol=2e-3):
+    """G4: on the GPU's own hq/hs, the fp32 result is within tol of the fp64
+    oracle (row-max normalised), the bf16 output is RNE of that fp32 result,
+    and the tap-free bound holds. Returns the error."""
+    out64, _ = O.down_proj(hq_rows, hs_cols, wd_q, wd_s)
+    o32 = out_tap_rows.astype(np.float64)
+    assert np.all(np.isfinite(o32)), "out tap has unwritten elements"
+    rowmax = np.maximum(np.abs(out64).max(axis=1, keepdims=True), 1e-300)
+    e = float((np.abs(o32 - out64) / rowmax).max())
+    assert e <= tol, e
+    assert np.array_equal(out_bits_rows, rne_bf16(out_tap_rows)), "bf16 store is not RNE of the fp32 result"
+    ob = out_bits_rows.astype(np.uint32) << 16
+    of = ob.view(np.float32).astype(np.float64)
+    _, ex = np.frexp(np.abs(out64))
+    ulp = np.exp2(np.maximum(ex, -125) - 8.0)
+    assert np.all(np.abs(of - out64) <= ulp + tol * rowmax)
+    return e

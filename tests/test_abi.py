@@ -1,0 +1,154 @@
+"""The C ABI on the host: every declared symbol is exported, and argument
+validation returns the documented status before anything touches a GPU.
+
+These run without a GPU: every call here fails validation (or is an M == 0
+no-op), which the library decides before its first HIP call. The pointers are
+fake, 16-byte aligned, non-overlapping addresses that are never dereferenced.
+"""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_16339_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+OK, INVALID, UNSUP = _lib.LACACHE_OK, _lib.LACACHE_ERR_INVALID_ARG, _lib.LACACHE_ERR_UNSUPPORTED
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(_lib.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    return _lib.lib()
+
+
+def _declared_symbols():
+    src = open(os.path.join(ROOT, "include", "lacache.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(lacache_\w+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = _declared_symbols()
+    assert len(names) >= 12
+    for n in names:
+        assert hasattr(L, n), n
+        assert n in _lib.SIGNATURES, n
+
+
+class Fake:
+    """Distinct aligned fake device addresses, 1 GiB apart."""
+
+    def __init__(self):
+        self.n = 0
+
+    def __call__(self):
+        self.n += 1
+        return 0x10000000000 + self.n * (1 << 30)
+
+
+def _ffn(L, M=32, H=4096, I=12288, group=128, **over):
+    f = Fake()
+    a = dict(x=f(), norm_w=f(), wgu_q=f(), wgu_s=f(), wd_q=f(), wd_s=f(), out=f())
+    a.update(over)
+    return L.lacache_ffn_fp8(None, a["x"], a["norm_w"], a["wgu_q"], a["wgu_s"], a["wd_q"], a["wd_s"], a["out"],
+                             M, H, I, group)
+
+
+def test_ffn_validation(L):
+    assert _ffn(L, group=64) == UNSUP
+    assert _ffn(L, H=4000) == INVALID
+    assert _ffn(L, I=100) == INVALID
+    assert _ffn(L, H=0) == INVALID
+    assert _ffn(L, M=-1) == INVALID
+    assert _ffn(L, H=16384 + 128) == UNSUP
+    assert _ffn(L, M=(1 << 24) + 1) == UNSUP
+    assert _ffn(L, x=None) == INVALID
+    assert _ffn(L, out=0x10000000008) == INVALID  # misaligned
+    x = 0x20000000000
+    assert _ffn(L, x=x, out=x + 1024) == INVALID  # out overlaps x
+    assert _ffn(L, M=0) == OK                    # no-op, nothing launched
+
+
+def test_stage_validation(L):
+    f = Fake()
+    p = [f() for _ in range(8)]
+    assert L.lacache_rmsnorm_quant(None, p[0], p[1], p[2], p[3], 4, 130, 128) == INVALID
+    assert L.lacache_rmsnorm_quant(None, p[0], p[1], p[2], p[3], 0, 256, 128) == OK
+    assert L.lacache_rmsnorm_quant(None, p[0], p[1], p[2], None, 4, 256, 128) == INVALID
+    assert L.lacache_gateup_swiglu_quant(None, p[0], p[1], p[2], p[3], p[4], p[5], None, 4, 256, 768, 256) == UNSUP
+    assert L.lacache_gateup_swiglu_quant(None, p[0], p[1], p[2], p[3], p[4], p[5], 0x8, 4, 256, 768, 128) == INVALID
+    assert L.lacache_gateup_swiglu_quant(None, p[0], p[1], p[2], p[3], p[4], p[5], None, 0, 256, 768, 128) == OK
+    # hq overlapping the weights
+    assert L.lacache_gateup_swiglu_quant(None, p[0], p[1], p[2], p[3], p[2] + 4096, p[5], None, 4, 256, 768, 128) == INVALID
+    assert L.lacache_down_proj(None, p[0], p[1], p[2], p[3], p[4], None, 4, 256, 700, 128) == INVALID
+    assert L.lacache_down_proj(None, p[0], p[1], p[2], p[3], p[4], None, 0, 256, 768, 128) == OK
+    assert L.lacache_quant_weights(None, p[0], p[1], p[2], 256, 200, 128) == INVALID
+    assert L.lacache_quant_weights(None, p[0], p[0], p[2], 256, 256, 128) == INVALID  # w_q aliases w
+    assert L.lacache_add_bf16(None, p[0], p[0], 16) == INVALID
+    assert L.lacache_add_bf16(None, p[0], p[1], 0) == OK
+    assert L.lacache_add_bf16(None, p[0], p[1], -1) == INVALID
+    assert L.lacache_encode_e4m3(None, p[0], p[1], 0) == OK
+    assert L.lacache_encode_e4m3(None, p[0], None, 4) == INVALID
+
+
+def test_path_policy(L):
+    assert L.lacache_set_path_policy(7) == INVALID
+    prev = L.lacache_set_path_policy(1)
+    try:
+        f = Fake()
+        p = [f() for _ in range(8)]
+        # skinny kernels only take M <= 64
+        assert L.lacache_gateup_swiglu_quant(None, p[0], p[1], p[2], p[3], p[4], p[5], None, 65, 256, 768, 128) == UNSUP
+        assert L.lacache_down_proj(None, p[0], p[1], p[2], p[3], p[4], None, 65, 256, 768, 128) == UNSUP
+        assert L.lacache_set_path_policy(2) == 1
+    finally:
+        L.lacache_set_path_policy(prev)
+
+
+def test_workspace_bytes_and_status_strings(L):
+    def a256(b):
+        return (b + 255) // 256 * 256
+    M, H, I = 32, 4096, 12288
+    skinny = 2048 + a256(M * I * 4)  # counter block + fp32 h buffer
+    want = skinny + a256(M * H) + a256(H // 128 * M * 4) + a256(M * I) + a256(I // 128 * M * 4)
+    assert L.lacache_ffn_workspace_bytes(M, H, I, 128) == want
+    M = 512
+    want = 2048 + a256(M * H) + a256(H // 128 * M * 4) + a256(M * I) + a256(I // 128 * M * 4)
+    assert L.lacache_ffn_workspace_bytes(M, H, I, 128) == want
+    assert L.lacache_ffn_workspace_bytes(M, H, I, 64) == 0
+    assert L.lacache_ffn_workspace_bytes(-1, H, I, 128) == 0
+    for s, name in [(0, "LACACHE_OK"), (-1, "LACACHE_ERR_INVALID_ARG"), (-2, "LACACHE_ERR_UNSUPPORTED"),
+                    (-3, "LACACHE_ERR_HIP"), (-4, "LACACHE_ERR_ALLOC")]:
+        assert L.lacache_status_string(s).decode() == name
+
+
+def test_ws_variant_checks_workspace(L):
+    f = Fake()
+    p = [f() for _ in range(8)]
+    args = [None] + p[:7] + [32, 4096, 12288, 128]
+    need = L.lacache_ffn_workspace_bytes(32, 4096, 12288, 128)
+    assert L.lacache_ffn_fp8_ws(*args, None, need) == INVALID
+    assert L.lacache_ffn_fp8_ws(*args, f(), need - 1) == INVALID
+    assert L.lacache_ffn_fp8_ws(*args, f() + 16, need) == INVALID  # not 256-byte aligned
+    assert L.lacache_ffn_fp8_ws(*args, p[0], need) == INVALID      # overlaps x
+    args0 = [None] + p[:7] + [0, 4096, 12288, 128]
+    assert L.lacache_ffn_fp8_ws(*args0, None, 0) == OK             # M == 0: nothing to do
+
+
+def test_binding_refuses_host_tensors():
+    import torch
+    import paper_2607_16339_amd as lc
+    x = torch.zeros(4, 256, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        lc.lacache_rmsnorm_quant(x, torch.zeros(256, dtype=torch.bfloat16), torch.zeros(4, 256, dtype=torch.uint8),
+                                 torch.zeros(2, 4), stream=0)
+
+
+def test_ctypes_signatures_cover_header():
+    assert set(_declared_symbols()) == set(_lib.SIGNATURES)
+    assert ctypes.sizeof(ctypes.c_void_p) == 8
