@@ -28,6 +28,8 @@ FLAGS = [
     "-fhip-fp32-correctly-rounded-divide-sqrt",
     # packed fp32 instructions are not used
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA results in VGPRs, where the per-group scale FMAs read them directly
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-I", os.path.join(ROOT, "include"),
     "-Wall",
     "-Wno-unused-command-line-argument",

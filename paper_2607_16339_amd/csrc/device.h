@@ -69,6 +69,22 @@ __device__ __forceinline__ v4f mfma_fp8_16x16x128(v8i a, v8i b, v4f c) {
 }
 
 // ---------------------------------------------------------------------------
+// Direct global -> LDS copies (gfx950). Lane l of the wavefront writes its
+// 16 (or 4) bytes to lds + 16*l (4*l); `lds` must be wave-uniform. Counted by
+// vmcnt. Wrapped in plain functions so that kernel templates stay valid in
+// the host compilation pass.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void lds_dma16(const void* src, void* lds) {
+  __builtin_amdgcn_global_load_lds(src, lds, 16, 0, 0);
+}
+__device__ __forceinline__ void lds_dma4(const void* src, void* lds) {
+  __builtin_amdgcn_global_load_lds(src, lds, 4, 0, 0);
+}
+
+// An int the compiler can see is the same in every lane of the wavefront.
+__device__ __forceinline__ int wave_uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// ---------------------------------------------------------------------------
 // Wavefront reductions (max is exact, so order does not matter)
 // ---------------------------------------------------------------------------
 template <int kWidth>

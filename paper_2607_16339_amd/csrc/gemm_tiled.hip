@@ -2,33 +2,38 @@
 //   gate/up: x[M x H] . Wgu[2I x H]^T, fused SwiGLU and 1x128 re-quantization
 //   down:    h[M x I] . Wd[H x I]^T -> bf16
 //
-// A workgroup (4 wavefronts) computes a 128-row x 256-weight-row tile and
-// walks K one 128-wide group at a time: the group's fp8 tiles are staged in
-// LDS, every 16x16 output sub-tile gets one 16x16x128 FP8 MFMA (exactly one
-// K-group), and its fp32 result is added to the accumulator times
-// RN32(x_scale[row] * w_scale[block]).
+// A workgroup of BM/32 wavefronts computes a BM-row x 256-weight-row tile.
+// Each wavefront owns 64 rows x 128 weight rows (4 x 8 sub-tiles of 16x16).
+// K is walked one 128-wide group at a time:
+//   * the group's fp8 tiles (A: BM x 128 B, B: 256 x 128 B) and the BM
+//     activation scales go global -> LDS with direct-to-LDS loads into one of
+//     two LDS stages, issued one group ahead, so no registers hold staging
+//     data and the copy of group kb+1 overlaps the MFMAs of group kb;
+//   * every 16x16 sub-tile gets one 16x16x128 FP8 MFMA (exactly one K-group)
+//     and its fp32 result is added to the accumulator times
+//     RN32(x_scale[row] * w_scale[block]): four VALU FMAs per MFMA, which the
+//     VALU issues while the matrix core works.
+// One workgroup barrier per K-group.
 //
 // For gate/up the tile's 256 weight rows are the 128 gate rows and the 128
 // matching up rows of one h-group, so each lane holds gate and up values of
-// the same (row, column) and the whole 128-wide h-group of a row lives in
-// one workgroup: SwiGLU, the row amax and the e4m3 encoding happen before
-// anything is written; h never reaches memory in 16 or 32 bits.
+// the same (row, column) and a row's whole 128-wide h-group lives in one
+// workgroup: SwiGLU, the row amax and the e4m3 encoding happen in registers
+// and LDS before anything is written; h never reaches memory.
 #include "device.h"
 #include "launch.h"
 
 namespace lacache {
 namespace {
 
-constexpr int BM = 128;   // activation rows per workgroup
-constexpr int BNR = 256;  // weight rows per workgroup
-constexpr int kThreads = 256;
+constexpr int BNR = 256;           // weight rows per workgroup
+constexpr int kMaxKGroups = 512;   // K <= 65536
 
 // LDS tiles are [rows][128 bytes]; the eight 16-byte chunks of a row are
-// permuted by an xor with a row hash so that 16 consecutive rows read at the
-// same logical chunk fall into distinct banks.
-__device__ __forceinline__ int lds_off(int row, int chunk) {
-  return row * 128 + ((chunk ^ ((row ^ (row >> 3)) & 7)) << 4);
-}
+// permuted by an xor with a row hash so that the 16 rows an MFMA operand read
+// touches at one logical chunk fall into distinct banks.
+__device__ __forceinline__ int swz(int row) { return (row ^ (row >> 3)) & 7; }
+__device__ __forceinline__ int lds_off(int row, int chunk) { return row * 128 + ((chunk ^ swz(row)) << 4); }
 
 // MFMA operand for one 16-row slab: lane (q = l/16, r = l%16) takes row
 // base + r, logical chunks q and 4 + q (the same K placement for A and B).
@@ -41,82 +46,86 @@ __device__ __forceinline__ v8i load_frag(const uint8_t* tile, int row, int q) {
   return f;
 }
 
-template <bool kGateUp>
-__global__ __launch_bounds__(kThreads) void gemm_tiled_kernel(
+// One LDS stage: A tile, B tile, activation scales.
+template <int BM>
+struct Stage {
+  uint8_t a[BM * 128];
+  uint8_t b[BNR * 128];
+  float xs[BM + 64];  // BM scales + a spare slot for redundant copies
+};
+
+__device__ __forceinline__ void wait_vm0() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+}  // namespace
+
+template <bool kGateUp, int BM>
+__global__ __launch_bounds__(BM / 32 * 64) void gemm_tiled_kernel(
     const uint8_t* __restrict__ aq, const float* __restrict__ as,  // [M x K] codes, [K/128 x M] scales
     const uint8_t* __restrict__ bq, const float* __restrict__ bs,  // [N x K] codes, [N/128 x K/128] scales
     uint8_t* __restrict__ hq, float* __restrict__ hs, float* __restrict__ h_tap,
     uint16_t* __restrict__ out, float* __restrict__ out_tap, int64_t M, int64_t K, int64_t N, int64_t I) {
-  __shared__ __align__(16) uint8_t sA[BM * 128];
-  __shared__ __align__(16) uint8_t sB[BNR * 128];
-  __shared__ __align__(16) float sXs[BM];
+  constexpr int NW = BM / 32;  // wavefronts: BM/64 along rows x 2 along weight rows
+  static_assert(NW == 4 || NW == 8, "BM must be 128 or 256");
+  __shared__ Stage<BM> st0, st1;
   __shared__ float sRed[2][BM];
+  __shared__ float sW[2][kMaxKGroups];  // the two weight-block scale rows used by this workgroup
 
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int wm = wave & 1, wn = wave >> 1;
+  const int t = threadIdx.x, lane = t & 63;
+  // wavefront index made visibly uniform: scale loads and LDS bases go scalar
+  const int wave = wave_uniform(t >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
   const int q = lane >> 4, lr = lane & 15;
   const int64_t m0 = static_cast<int64_t>(blockIdx.x) * BM;
   const int64_t by = blockIdx.y;  // gate/up: h-group; down: 256-column tile
   const int64_t KB = K / 128;
+  const int64_t n0 = kGateUp ? 0 : by * BNR;
 
-  // ---- global -> register mapping: thread t loads tile rows (t/8) + 32u, chunk t%8
-  const int lrow = t >> 3, lch = t & 7;
-  const int64_t stride32 = 32 * K;
-  const uint8_t* a_base = aq + (m0 + lrow) * K + lch * 16;
-  const uint8_t* b_base;
-  const uint8_t* b_base_hi;  // gate/up: up rows; down: unused
-  int64_t n0 = 0;
-  if (kGateUp) {
-    b_base = bq + (by * 128 + lrow) * K + lch * 16;
-    b_base_hi = b_base + I * K;
-  } else {
-    n0 = by * BNR;
-    b_base = bq + (n0 + lrow) * K + lch * 16;
-    b_base_hi = b_base;
+  // ---- direct-to-LDS copy plan. A wave's load instruction fills 64
+  // consecutive 16-byte LDS slots (8 tile rows); lane l fills slot l, i.e.
+  // row 8g + l/8, physical chunk l%8, so it fetches logical chunk
+  // (l%8) ^ swz(row) of that row. Rows past M (or N) fetch a clamped row;
+  // their results are never stored. Per-lane offsets are 32-bit, relative to
+  // workgroup-uniform bases.
+  constexpr int kAInst = BM / 8 / NW;  // per wave
+  constexpr int kBInst = BNR / 8 / NW;
+  const uint8_t* a_base = aq + m0 * K;
+  uint32_t a_off[kAInst], b_off[kBInst];
+#pragma unroll
+  for (int u = 0; u < kAInst; ++u) {
+    const int row = (wave * kAInst + u) * 8 + (lane >> 3);
+    const int64_t r = m0 + row < M ? row : M - 1 - m0;
+    a_off[u] = static_cast<uint32_t>(r * K + ((lane & 7) ^ swz(row)) * 16);
   }
-  uint4 ra[4], rb[8];
-  float rxs = 0.0f;
-  const uint4 z4 = make_uint4(0u, 0u, 0u, 0u);
+  // gate/up: rows 0..127 of the tile come from the gate block, 128..255 from
+  // the up block (base b_base_hi); down: one contiguous 256-row block
+  const uint8_t* b_base = kGateUp ? bq + by * 128 * K : bq + n0 * K;
+  const uint8_t* b_base_hi = kGateUp ? bq + (I + by * 128 - 128) * K : b_base;
+#pragma unroll
+  for (int u = 0; u < kBInst; ++u) {
+    const int row = (wave * kBInst + u) * 8 + (lane >> 3);
+    const int64_t r = (kGateUp || n0 + row < N) ? row : N - 1 - n0;
+    b_off[u] = static_cast<uint32_t>(r * K + ((lane & 7) ^ swz(row)) * 16);
+  }
+  // activation scales: waves 0..BM/64-1 copy rows 64w..64w+63 (one float per
+  // lane); the other waves copy the same rows into a spare slot
+  const int xw = wave % (BM / 64);
+  const uint32_t xs_off = static_cast<uint32_t>(m0 + xw * 64 + lane < M ? xw * 64 + lane : M - 1 - m0);
+  const int xs_dst = wave < BM / 64 ? wave * 64 : BM;
+  const float* xs_base = as + m0;
 
-  auto gload = [&](int64_t kb) {
-    const int64_t ko = kb * 128;
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-      ra[u] = (m0 + lrow + 32 * u < M) ? *reinterpret_cast<const uint4*>(a_base + u * stride32 + ko) : z4;
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      if (kGateUp) {
-        const uint8_t* p = (u < 4 ? b_base + u * stride32 : b_base_hi + (u - 4) * stride32) + ko;
-        rb[u] = *reinterpret_cast<const uint4*>(p);
-      } else {
-        rb[u] = (n0 + lrow + 32 * u < N) ? *reinterpret_cast<const uint4*>(b_base + u * stride32 + ko) : z4;
-      }
+  // (down: the wave's 128 columns may lie past N in the last column tile)
+  const bool nb_ok = kGateUp || n0 + 128 * wn < N;
+  // The workgroup's weight-block scales for all K-groups, staged in LDS once:
+  // gate/up rows {gate block, up block}; down rows {block of wn = 0, wn = 1}.
+  {
+    const int64_t r0 = kGateUp ? by : n0 / 128;
+    const int64_t r1 = kGateUp ? I / 128 + by : (n0 + 128 < N ? n0 / 128 + 1 : r0);
+    for (int64_t i = t; i < 2 * KB; i += NW * 64) {
+      const int64_t row = i < KB ? r0 : r1;
+      sW[i < KB ? 0 : 1][i < KB ? i : i - KB] = bs[row * KB + (i < KB ? i : i - KB)];
     }
-    if (t < BM) rxs = (m0 + t < M) ? as[kb * M + m0 + t] : 0.0f;
-  };
-  auto sstore = [&]() {
-#pragma unroll
-    for (int u = 0; u < 4; ++u) *reinterpret_cast<uint4*>(sA + lds_off(lrow + 32 * u, lch)) = ra[u];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) *reinterpret_cast<uint4*>(sB + lds_off(lrow + 32 * u, lch)) = rb[u];
-    if (t < BM) sXs[t] = rxs;
-  };
-
-  // weight-block scale rows used by this wavefront
-  int64_t nb0, nb1;
-  bool nb_ok = true;
-  if (kGateUp) {
-    nb0 = by;             // gate block
-    nb1 = I / 128 + by;   // up block
-  } else {
-    nb0 = (n0 + 128 * wn) / 128;
-    nb1 = nb0;
-    nb_ok = n0 + 128 * wn < N;
   }
-  auto brow = [&](int j) -> int {
-    if (kGateUp) return j < 4 ? 64 * wn + 16 * j : 128 + 64 * wn + 16 * (j - 4);
-    return 128 * wn + 16 * j;
-  };
+  const int wsel0 = kGateUp ? 0 : wn, wsel1 = kGateUp ? 1 : wn;
 
   float acc[4][8][4];
 #pragma unroll
@@ -126,43 +135,68 @@ __global__ __launch_bounds__(kThreads) void gemm_tiled_kernel(
 #pragma unroll
       for (int r = 0; r < 4; ++r) acc[i][j][r] = 0.0f;
 
-  gload(0);
-  sstore();
-  __syncthreads();
-  for (int64_t kb = 0; kb < KB; ++kb) {
-    if (kb + 1 < KB) gload(kb + 1);
-    const float w0 = nb_ok ? bs[nb0 * KB + kb] : 0.0f;
-    const float w1 = nb_ok ? bs[nb1 * KB + kb] : 0.0f;
+  // Copies K-group kn into stage `nxt` (asynchronously) and multiplies K-group
+  // kb from stage `cur`. The two stages never alias; the restrict qualifiers
+  // let the compiler see that, so reading `cur` does not wait for the copy.
+  auto step = [&](const Stage<BM>* __restrict__ cur, Stage<BM>* __restrict__ nxt, int64_t kb, int64_t kn) {
+    const int64_t ko = kn * 128;
+#pragma unroll
+    for (int u = 0; u < kAInst; ++u)
+      lds_dma16(a_base + ko + a_off[u], nxt->a + (wave * kAInst + u) * 1024);
+#pragma unroll
+    for (int u = 0; u < kBInst; ++u) {
+      const uint8_t* base = (kGateUp && (wave * kBInst + u) * 8 >= 128) ? b_base_hi : b_base;
+      lds_dma16(base + ko + b_off[u], nxt->b + (wave * kBInst + u) * 1024);
+    }
+    lds_dma4(xs_base + kn * M + xs_off, nxt->xs + xs_dst);
+
+    const float w0 = nb_ok ? sW[wsel0][kb] : 0.0f;
+    const float w1 = nb_ok ? sW[wsel1][kb] : 0.0f;
     v8i af[4];
-    float sc0[4][4], sc1[4][4];
+    float xa[4][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      af[i] = load_frag(sA, 64 * wm + 16 * i + lr, q);
-      const float4 xv = *reinterpret_cast<const float4*>(sXs + 64 * wm + 16 * i + 4 * q);
-      const float xa[4] = {xv.x, xv.y, xv.z, xv.w};
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        sc0[i][r] = xa[r] * w0;  // RN32(x_scale * w_scale)
-        sc1[i][r] = xa[r] * w1;
-      }
+      af[i] = load_frag(cur->a, 64 * wm + 16 * i + lr, q);
+      const float4 xv = *reinterpret_cast<const float4*>(cur->xs + 64 * wm + 16 * i + 4 * q);
+      xa[i][0] = xv.x; xa[i][1] = xv.y; xa[i][2] = xv.z; xa[i][3] = xv.w;
     }
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      const v8i bf = load_frag(sB, brow(j) + lr, q);
+      const int brow = kGateUp ? (j < 4 ? 64 * wn + 16 * j : 128 + 64 * wn + 16 * (j - 4)) : 128 * wn + 16 * j;
+      const v8i bf = load_frag(cur->b, brow + lr, q);
+      const float w = (kGateUp && j >= 4) ? w1 : w0;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const v4f zero = {0.0f, 0.0f, 0.0f, 0.0f};
         const v4f p = mfma_fp8_16x16x128(af[i], bf, zero);
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          acc[i][j][r] = __builtin_fmaf(p[r], (kGateUp && j >= 4) ? sc1[i][r] : sc0[i][r], acc[i][j][r]);
+        for (int r = 0; r < 4; ++r) acc[i][j][r] = __builtin_fmaf(p[r], xa[i][r] * w, acc[i][j][r]);
       }
     }
+    wait_vm0();
     __syncthreads();
-    if (kb + 1 < KB) {
-      sstore();
-      __syncthreads();
+  };
+
+  // ---- main loop: two LDS stages, the copy of the next group in flight. The
+  // last step re-fetches its own group into the idle stage (never read).
+  {
+    const int64_t ko = 0;
+#pragma unroll
+    for (int u = 0; u < kAInst; ++u)
+      lds_dma16(a_base + ko + a_off[u], st0.a + (wave * kAInst + u) * 1024);
+#pragma unroll
+    for (int u = 0; u < kBInst; ++u) {
+      const uint8_t* base = (kGateUp && (wave * kBInst + u) * 8 >= 128) ? b_base_hi : b_base;
+      lds_dma16(base + ko + b_off[u], st0.b + (wave * kBInst + u) * 1024);
     }
+    lds_dma4(xs_base + xs_off, st0.xs + xs_dst);
+    wait_vm0();
+    __syncthreads();
+  }
+  for (int64_t kb = 0; kb < KB; kb += 2) {
+    step(&st0, &st1, kb, kb + 1 < KB ? kb + 1 : kb);
+    if (kb + 1 >= KB) break;
+    step(&st1, &st0, kb + 1, kb + 2 < KB ? kb + 2 : kb + 1);
   }
 
   if (kGateUp) {
@@ -190,7 +224,8 @@ __global__ __launch_bounds__(kThreads) void gemm_tiled_kernel(
         for (int r = 0; r < 4; ++r) sRed[wn][64 * wm + 16 * i + 4 * q + r] = am[i][r];
     }
     __syncthreads();
-    // ---- 1x128 quantization of each row's h-group; codes go through LDS for coalesced stores
+    // ---- 1x128 quantization of each row's h-group; codes staged in LDS for coalesced stores
+    uint8_t* codes = st0.a;  // BM x 128 bytes, free after the main loop
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -200,19 +235,19 @@ __global__ __launch_bounds__(kThreads) void gemm_tiled_kernel(
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int col = 64 * wn + 16 * j + lr;
-          sA[row * 128 + col] = s == 0.0f ? 0 : static_cast<uint8_t>(enc1_e4m3(qdiv(h[i][j][r], s)));
+          codes[row * 128 + col] = s == 0.0f ? 0 : static_cast<uint8_t>(enc1_e4m3(qdiv(h[i][j][r], s)));
           if (h_tap != nullptr && m0 + row < M) h_tap[(m0 + row) * I + by * 128 + col] = h[i][j][r];
         }
       }
     __syncthreads();
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int row = lrow + 32 * u;
+    for (int c = t; c < BM * 8; c += NW * 64) {
+      const int row = c >> 3, ch = c & 7;
       if (m0 + row < M)
-        *reinterpret_cast<uint4*>(hq + (m0 + row) * I + by * 128 + lch * 16) =
-            *reinterpret_cast<const uint4*>(sA + row * 128 + lch * 16);
+        *reinterpret_cast<uint4*>(hq + (m0 + row) * I + by * 128 + ch * 16) =
+            *reinterpret_cast<const uint4*>(codes + row * 128 + ch * 16);
     }
-    if (t < BM && m0 + t < M) hs[by * M + m0 + t] = __builtin_fmaxf(sRed[0][t], sRed[1][t]) / kE4M3Max;
+    for (int row = t; row < BM; row += NW * 64)
+      if (m0 + row < M) hs[by * M + m0 + row] = __builtin_fmaxf(sRed[0][row], sRed[1][row]) / kE4M3Max;
   } else {
     // ---- bf16 output, nearest-even from the fp32 accumulator
 #pragma unroll
@@ -233,24 +268,51 @@ __global__ __launch_bounds__(kThreads) void gemm_tiled_kernel(
   }
 }
 
+template __global__ void gemm_tiled_kernel<true, 256>(const uint8_t*, const float*, const uint8_t*, const float*,
+                                                     uint8_t*, float*, float*, uint16_t*, float*, int64_t, int64_t,
+                                                     int64_t, int64_t);
+template __global__ void gemm_tiled_kernel<true, 128>(const uint8_t*, const float*, const uint8_t*, const float*,
+                                                     uint8_t*, float*, float*, uint16_t*, float*, int64_t, int64_t,
+                                                     int64_t, int64_t);
+template __global__ void gemm_tiled_kernel<false, 256>(const uint8_t*, const float*, const uint8_t*, const float*,
+                                                      uint8_t*, float*, float*, uint16_t*, float*, int64_t, int64_t,
+                                                      int64_t, int64_t);
+template __global__ void gemm_tiled_kernel<false, 128>(const uint8_t*, const float*, const uint8_t*, const float*,
+                                                      uint8_t*, float*, float*, uint16_t*, float*, int64_t, int64_t,
+                                                      int64_t, int64_t);
+
+namespace {
+
+template <bool kGateUp, int BM>
+hipError_t launch_tiled(hipStream_t st, const uint8_t* aq, const float* as, const uint8_t* bq, const float* bs,
+                        uint8_t* hq, float* hs, float* h_tap, uint16_t* out, float* out_tap, int64_t M, int64_t K,
+                        int64_t N, int64_t I) {
+  const unsigned ny = kGateUp ? static_cast<unsigned>(I / 128) : static_cast<unsigned>((N + BNR - 1) / BNR);
+  dim3 grid(static_cast<unsigned>((M + BM - 1) / BM), ny);
+  hipLaunchKernelGGL((gemm_tiled_kernel<kGateUp, BM>), grid, dim3(BM / 32 * 64), 0, st, aq, as, bq, bs, hq, hs,
+                     h_tap, out, out_tap, M, K, N, I);
+  return hipGetLastError();
+}
+
+// Row-tile height: 256 when there are enough row tiles to fill the chip with
+// one workgroup per CU, else 128.
+bool use_bm256(int64_t M, int64_t col_tiles) { return ((M + 255) / 256) * col_tiles >= 512; }
+
 }  // namespace
 
 hipError_t launch_gateup_tiled(hipStream_t st, const uint8_t* xq, const float* xs, const uint8_t* wq,
                                const float* ws, uint8_t* hq, float* hs, float* h_tap, int64_t M, int64_t H,
                                int64_t I) {
-  dim3 grid(static_cast<unsigned>((M + BM - 1) / BM), static_cast<unsigned>(I / 128));
-  hipLaunchKernelGGL(gemm_tiled_kernel<true>, grid, dim3(kThreads), 0, st, xq, xs, wq, ws, hq, hs, h_tap,
-                     static_cast<uint16_t*>(nullptr), static_cast<float*>(nullptr), M, H, 2 * I, I);
-  return hipGetLastError();
+  if (use_bm256(M, I / 128))
+    return launch_tiled<true, 256>(st, xq, xs, wq, ws, hq, hs, h_tap, nullptr, nullptr, M, H, 2 * I, I);
+  return launch_tiled<true, 128>(st, xq, xs, wq, ws, hq, hs, h_tap, nullptr, nullptr, M, H, 2 * I, I);
 }
 
 hipError_t launch_down_tiled(hipStream_t st, const uint8_t* hq, const float* hs, const uint8_t* wq, const float* ws,
                              uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I) {
-  dim3 grid(static_cast<unsigned>((M + BM - 1) / BM), static_cast<unsigned>((H + BNR - 1) / BNR));
-  hipLaunchKernelGGL(gemm_tiled_kernel<false>, grid, dim3(kThreads), 0, st, hq, hs, wq, ws,
-                     static_cast<uint8_t*>(nullptr), static_cast<float*>(nullptr), static_cast<float*>(nullptr),
-                     out, out_tap, M, I, H, I);
-  return hipGetLastError();
+  if (use_bm256(M, (H + BNR - 1) / BNR))
+    return launch_tiled<false, 256>(st, hq, hs, wq, ws, nullptr, nullptr, nullptr, out, out_tap, M, I, H, I);
+  return launch_tiled<false, 128>(st, hq, hs, wq, ws, nullptr, nullptr, nullptr, out, out_tap, M, I, H, I);
 }
 
 }  // namespace lacache
