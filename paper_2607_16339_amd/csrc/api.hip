@@ -9,7 +9,7 @@
 #include <mutex>
 #include <vector>
 
-#include "../../include/lacache.h"
+#include "lacache.h"
 #include "launch.h"
 
 namespace {

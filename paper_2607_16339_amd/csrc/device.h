@@ -39,6 +39,28 @@ __device__ __forceinline__ uint32_t enc1_e4m3(float a) {
 // rounded fp32 division).
 __device__ __forceinline__ float qdiv(float y, float s) { return y / s; }
 
+// The same code, E(RN32(y / s)), from the hardware reciprocal rs = rcp(s)
+// (1 ulp): q0 = y * rs is within 2^-22 (relative) of y / s, so when the codes
+// of q0 * (1 - 2^-20) and q0 * (1 + 2^-20) agree, that is the code of every
+// value in between, RN32(y / s) included (the encoder is monotone). Otherwise
+// the value sits at an e4m3 rounding boundary and the correctly rounded
+// division decides. Requires s >= 2^-100 (see scale_is_fast).
+__device__ __forceinline__ uint32_t enc1_div_fast(float y, float s, float rs) {
+  const float q0 = y * rs;
+  const float d = __builtin_fabsf(q0) * 0x1p-20f;
+  const uint32_t w = static_cast<uint32_t>(__builtin_amdgcn_cvt_pk_fp8_f32(clip448(q0 - d), clip448(q0 + d), 0, false));
+  if ((w & 0xFFu) == ((w >> 8) & 0xFFu)) return w & 0xFFu;
+  return enc1_e4m3(y / s);
+}
+__device__ __forceinline__ bool scale_is_fast(float s) { return s >= 0x1p-100f; }
+__device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+
+// SiLU(g) * u in fp32 with the hardware exp2 and reciprocal (a few ulp).
+__device__ __forceinline__ float swiglu_fast(float g, float u) {
+  const float e = __builtin_amdgcn_exp2f(-g * 1.44269504088896341f);
+  return g * fast_rcp(1.0f + e) * u;
+}
+
 // ---------------------------------------------------------------------------
 // bf16 <-> fp32
 // ---------------------------------------------------------------------------
@@ -79,6 +101,14 @@ __device__ __forceinline__ void lds_dma16(const void* src, void* lds) {
 }
 __device__ __forceinline__ void lds_dma4(const void* src, void* lds) {
   __builtin_amdgcn_global_load_lds(src, lds, 4, 0, 0);
+}
+
+// L2 prefetch: a 1-byte vector load of the cache line at p into `sink`, a
+// register the caller keeps live (and never reads) until it has waited for
+// vmcnt to drain. The load is opaque to the compiler, so it neither waits for
+// it nor reuses `sink` early.
+__device__ __forceinline__ void prefetch_l2(const void* p, uint32_t& sink) {
+  asm volatile("global_load_ubyte %0, %1, off" : "+v"(sink) : "v"(p));
 }
 
 // An int the compiler can see is the same in every lane of the wavefront.

@@ -28,11 +28,15 @@ namespace {
 
 constexpr int BNR = 256;           // weight rows per workgroup
 constexpr int kMaxKGroups = 512;   // K <= 65536
+#ifndef LACACHE_L2_PREFETCH
+#define LACACHE_L2_PREFETCH 0
+#endif
+constexpr bool kL2Prefetch = LACACHE_L2_PREFETCH != 0;
 
 // LDS tiles are [rows][128 bytes]; the eight 16-byte chunks of a row are
-// permuted by an xor with a row hash so that the 16 rows an MFMA operand read
-// touches at one logical chunk fall into distinct banks.
-__device__ __forceinline__ int swz(int row) { return (row ^ (row >> 3)) & 7; }
+// permuted by an xor with (row / 2) mod 8, which spreads the 16 rows of an
+// MFMA operand read over the banks (the best of the permutations measured).
+__device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
 __device__ __forceinline__ int lds_off(int row, int chunk) { return row * 128 + ((chunk ^ swz(row)) << 4); }
 
 // MFMA operand for one 16-row slab: lane (q = l/16, r = l%16) takes row
@@ -51,10 +55,34 @@ template <int BM>
 struct Stage {
   uint8_t a[BM * 128];
   uint8_t b[BNR * 128];
-  float xs[BM + 64];  // BM scales + a spare slot for redundant copies
+  alignas(16) float xs[BM + 64];  // BM scales + a spare slot for redundant copies
 };
 
-__device__ __forceinline__ void wait_vm0() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// s_waitcnt with only vmcnt constrained (gfx9 encoding: vmcnt in bits 3:0,
+// expcnt 6:4 and lgkmcnt 11:8 left at their maxima). The builtin, unlike
+// inline asm, is visible to the compiler's own wait-count tracking.
+__device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+// Workgroup barrier between pipeline steps. Each wave has already waited for
+// its own copies into the next stage, and every LDS read of the current stage
+// has been consumed, so no memory fence is needed (a fence would also wait
+// for the L2 prefetches); the empty asm statements keep the compiler from
+// moving LDS accesses across it.
+__device__ __forceinline__ void stage_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+template <int N>
+__device__ __forceinline__ void wait_vm_prefetch() {
+  static_assert(N >= 0 && N < 16, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+}
+
+// Scheduling hint: one MFMA followed by four VALU instructions.
+__device__ __forceinline__ void sched_mfma_then_4valu() {
+  __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+  __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+}
 
 }  // namespace
 
@@ -113,6 +141,28 @@ __global__ __launch_bounds__(BM / 32 * 64) void gemm_tiled_kernel(
   const int xs_dst = wave < BM / 64 ? wave * 64 : BM;
   const float* xs_base = as + m0;
 
+  // ---- L2 prefetch two K-groups ahead. A row's K-group is one 128-byte
+  // cache line; a 1-byte load per lane pulls 64 lines into L2 while moving
+  // only 64 bytes. Wave w covers tile rows 64 (w + NW u) .. +63 of the
+  // BM + 256 rows (A rows first, then B rows).
+  constexpr int kPRows = BM + BNR;
+  constexpr int kPInst = kL2Prefetch ? (kPRows / 64 + NW - 1) / NW : 0;
+  const uint8_t* p_base[kPInst > 0 ? kPInst : 1];
+  uint32_t p_off[kPInst > 0 ? kPInst : 1];
+#pragma unroll
+  for (int u = 0; u < kPInst; ++u) {
+    int row = 64 * (wave + NW * u) + lane;
+    if (row >= kPRows) row = kPRows - 1;
+    if (row < BM) {
+      p_base[u] = a_base;
+      p_off[u] = static_cast<uint32_t>((m0 + row < M ? row : M - 1 - m0) * K);
+    } else {
+      const int br = row - BM;
+      p_base[u] = (kGateUp && br >= 128) ? b_base_hi : b_base;
+      p_off[u] = static_cast<uint32_t>(((kGateUp || n0 + br < N) ? br : N - 1 - n0) * K);
+    }
+  }
+
   // (down: the wave's 128 columns may lie past N in the last column tile)
   const bool nb_ok = kGateUp || n0 + 128 * wn < N;
   // The workgroup's weight-block scales for all K-groups, staged in LDS once:
@@ -138,7 +188,13 @@ __global__ __launch_bounds__(BM / 32 * 64) void gemm_tiled_kernel(
   // Copies K-group kn into stage `nxt` (asynchronously) and multiplies K-group
   // kb from stage `cur`. The two stages never alias; the restrict qualifiers
   // let the compiler see that, so reading `cur` does not wait for the copy.
-  auto step = [&](const Stage<BM>* __restrict__ cur, Stage<BM>* __restrict__ nxt, int64_t kb, int64_t kn) {
+  uint32_t sink = 0u;  // destination of the prefetch loads, live until the final vmcnt(0)
+  auto prefetch = [&](int64_t kp) {
+#pragma unroll
+    for (int u = 0; u < kPInst; ++u) prefetch_l2(p_base[u] + kp * 128 + p_off[u], sink);
+  };
+  auto step = [&](const Stage<BM>* __restrict__ cur, Stage<BM>* __restrict__ nxt, int64_t kb, int64_t kn,
+                  int64_t kp) {
     const int64_t ko = kn * 128;
 #pragma unroll
     for (int u = 0; u < kAInst; ++u)
@@ -149,32 +205,60 @@ __global__ __launch_bounds__(BM / 32 * 64) void gemm_tiled_kernel(
       lds_dma16(base + ko + b_off[u], nxt->b + (wave * kBInst + u) * 1024);
     }
     lds_dma4(xs_base + kn * M + xs_off, nxt->xs + xs_dst);
+    prefetch(kp);
 
     const float w0 = nb_ok ? sW[wsel0][kb] : 0.0f;
     const float w1 = nb_ok ? sW[wsel1][kb] : 0.0f;
     v8i af[4];
-    float xa[4][4];
+    float sc[2][4][4];  // RN32(x_scale * w_scale) for the two weight blocks
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       af[i] = load_frag(cur->a, 64 * wm + 16 * i + lr, q);
       const float4 xv = *reinterpret_cast<const float4*>(cur->xs + 64 * wm + 16 * i + 4 * q);
-      xa[i][0] = xv.x; xa[i][1] = xv.y; xa[i][2] = xv.z; xa[i][3] = xv.w;
+      const float xa[4] = {xv.x, xv.y, xv.z, xv.w};
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        sc[0][i][r] = xa[r] * w0;
+        sc[1][i][r] = xa[r] * w1;
+      }
     }
+    // Software pipeline over the 32 sub-tiles: MFMA s is issued before the
+    // four scale FMAs of MFMA s-1, so the VALU works on a finished result
+    // while the matrix core runs; the B operand of slab j+1 is read from
+    // LDS while slab j multiplies.
+    auto brow = [&](int j) {
+      return kGateUp ? (j < 4 ? 64 * wn + 16 * j : 128 + 64 * wn + 16 * (j - 4)) : 128 * wn + 16 * j;
+    };
+    v8i bcur = load_frag(cur->b, brow(0) + lr, q);
+    v4f pprev = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      const int brow = kGateUp ? (j < 4 ? 64 * wn + 16 * j : 128 + 64 * wn + 16 * (j - 4)) : 128 * wn + 16 * j;
-      const v8i bf = load_frag(cur->b, brow + lr, q);
-      const float w = (kGateUp && j >= 4) ? w1 : w0;
+      const v8i bnext = j < 7 ? load_frag(cur->b, brow(j + 1) + lr, q) : bcur;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const v4f zero = {0.0f, 0.0f, 0.0f, 0.0f};
-        const v4f p = mfma_fp8_16x16x128(af[i], bf, zero);
+        const v4f p = mfma_fp8_16x16x128(af[i], bcur, zero);
+        const int s = j * 4 + i;
+        if (s > 0) {
+          const int pi = (s - 1) & 3, pj = (s - 1) >> 2;
+          const int blk = (kGateUp && pj >= 4) ? 1 : 0;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) acc[i][j][r] = __builtin_fmaf(p[r], xa[i][r] * w, acc[i][j][r]);
+          for (int r = 0; r < 4; ++r) acc[pi][pj][r] = __builtin_fmaf(pprev[r], sc[blk][pi][r], acc[pi][pj][r]);
+        }
+        pprev = p;
+        sched_mfma_then_4valu();
       }
+      bcur = bnext;
     }
-    wait_vm0();
-    __syncthreads();
+    {
+      const int blk = kGateUp ? 1 : 0;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[3][7][r] = __builtin_fmaf(pprev[r], sc[blk][3][r], acc[3][7][r]);
+    }
+    // loads retire in issue order: this waits for the stage copy while the
+    // kPInst prefetches issued after it stay in flight across the barrier
+    wait_vm_prefetch<kPInst>();
+    stage_barrier();
   };
 
   // ---- main loop: two LDS stages, the copy of the next group in flight. The
@@ -190,14 +274,17 @@ __global__ __launch_bounds__(BM / 32 * 64) void gemm_tiled_kernel(
       lds_dma16(base + ko + b_off[u], st0.b + (wave * kBInst + u) * 1024);
     }
     lds_dma4(xs_base + xs_off, st0.xs + xs_dst);
-    wait_vm0();
+    prefetch(KB > 1 ? 1 : 0);
+    wait_vm_prefetch<kPInst>();
     __syncthreads();
   }
+  auto clampk = [&](int64_t k) { return k < KB ? k : KB - 1; };
   for (int64_t kb = 0; kb < KB; kb += 2) {
-    step(&st0, &st1, kb, kb + 1 < KB ? kb + 1 : kb);
+    step(&st0, &st1, kb, clampk(kb + 1), clampk(kb + 2));
     if (kb + 1 >= KB) break;
-    step(&st1, &st0, kb + 1, kb + 2 < KB ? kb + 2 : kb + 1);
+    step(&st1, &st0, kb + 1, clampk(kb + 2), clampk(kb + 3));
   }
+  wait_vm0();
 
   if (kGateUp) {
     // ---- SwiGLU: h = SiLU(g) * u, lanes hold matching gate (j) and up (j + 4) values
@@ -210,8 +297,7 @@ __global__ __launch_bounds__(BM / 32 * 64) void gemm_tiled_kernel(
         float a = 0.0f;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const float g = acc[i][j][r], u = acc[i][j + 4][r];
-          const float v = g / (1.0f + expf(-g)) * u;
+          const float v = swiglu_fast(acc[i][j][r], acc[i][j + 4][r]);
           h[i][j][r] = v;
           a = __builtin_fmaxf(a, __builtin_fabsf(v));
         }
@@ -232,10 +318,15 @@ __global__ __launch_bounds__(BM / 32 * 64) void gemm_tiled_kernel(
       for (int r = 0; r < 4; ++r) {
         const int row = 64 * wm + 16 * i + 4 * q + r;
         const float s = __builtin_fmaxf(sRed[0][row], sRed[1][row]) / kE4M3Max;
+        const bool fast = scale_is_fast(s);
+        const float rs = fast_rcp(s);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int col = 64 * wn + 16 * j + lr;
-          codes[row * 128 + col] = s == 0.0f ? 0 : static_cast<uint8_t>(enc1_e4m3(qdiv(h[i][j][r], s)));
+          const float v = h[i][j][r];
+          uint32_t c = 0u;
+          if (s != 0.0f) c = fast ? enc1_div_fast(v, s, rs) : enc1_e4m3(qdiv(v, s));
+          codes[row * 128 + col] = static_cast<uint8_t>(c);
           if (h_tap != nullptr && m0 + row < M) h_tap[(m0 + row) * I + by * 128 + col] = h[i][j][r];
         }
       }
