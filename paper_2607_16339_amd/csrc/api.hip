@@ -81,22 +81,29 @@ int hip_status(hipError_t e) { return e == hipSuccess ? LACACHE_OK : LACACHE_ERR
 
 // Kernel path for the GEMM stages.
 enum class Path { kSkinny, kTiled };
-int choose_path(int64_t M, Path* p) {
+int choose_path(int64_t M, int64_t H, int64_t I, Path* p) {
   const int pol = g_policy.load();
+  const bool skinny_ok = skinny_supported(M, H, I) || M == 0;
   if (pol == 1) {
-    if (M > kSkinnyMaxM) return LACACHE_ERR_UNSUPPORTED;
+    if (!skinny_ok) return LACACHE_ERR_UNSUPPORTED;
     *p = Path::kSkinny;
   } else if (pol == 2) {
     *p = Path::kTiled;
   } else {
-    *p = M <= kSkinnyMaxM ? Path::kSkinny : Path::kTiled;
+    *p = (M <= kSkinnyMaxM && skinny_ok) ? Path::kSkinny : Path::kTiled;
   }
   return LACACHE_OK;
 }
 
+// Scratch of the skinny kernels: one fp32 buffer that serves the gate/up h
+// and, afterwards, the down partial sums.
+size_t skinny_scratch_bytes(int64_t M, int64_t H, int64_t I) {
+  const size_t a = skinny_gateup_ws_bytes(M, I), b = skinny_down_ws_bytes(M, H, I);
+  return a > b ? a : b;
+}
+
 // ---------------------------------------------------------------------------
-// Library-owned workspace: one grow-only device buffer per device, zero-filled
-// when (re)allocated.
+// Library-owned workspace: one grow-only device buffer per device.
 // ---------------------------------------------------------------------------
 struct DeviceWs {
   void* ptr = nullptr;
@@ -105,21 +112,8 @@ struct DeviceWs {
 std::mutex g_ws_mu;
 std::vector<DeviceWs> g_ws;
 
-__global__ void zero_fill_kernel(uint32_t* p, size_t n) {
-  const size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i < n) p[i] = 0u;
-}
-
-hipError_t zero_fill(hipStream_t st, void* p, size_t bytes) {
-  const size_t n = bytes / 4;
-  if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(zero_fill_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, st,
-                     static_cast<uint32_t*>(p), n);
-  return hipGetLastError();
-}
-
 // Returns a workspace of at least `bytes` on the current device.
-int get_workspace(hipStream_t st, size_t bytes, void** out) {
+int get_workspace(size_t bytes, void** out) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return LACACHE_ERR_HIP;
   std::lock_guard<std::mutex> lk(g_ws_mu);
@@ -137,10 +131,6 @@ int get_workspace(hipStream_t st, size_t bytes, void** out) {
     }
     void* p = nullptr;
     if (hipMalloc(&p, bytes) != hipSuccess) return LACACHE_ERR_ALLOC;
-    if (zero_fill(st, p, bytes) != hipSuccess) {
-      (void)hipFree(p);
-      return LACACHE_ERR_HIP;
-    }
     w.ptr = p;
     w.bytes = bytes;
   }
@@ -149,14 +139,10 @@ int get_workspace(hipStream_t st, size_t bytes, void** out) {
 }
 
 // Workspace layout (every region 256-byte aligned):
-//   [skinny counters: kSkinnyCounterBytes, always present, always at offset 0]
-//   [skinny h buffer: M x I fp32, only when M <= kSkinnyMaxM]
+//   [skinny scratch: fp32 h or down partials, only when M <= kSkinnyMaxM]
 //   [xq: M x H][xs: H/128 x M fp32][hq: M x I][hs: I/128 x M fp32]
-// The counters sit at the same place for every shape, so the library-owned
-// workspace keeps them zero between calls (zero-filled on allocation, re-armed
-// by the kernel); a caller-owned workspace is cleared by the norm kernel.
 struct FfnWs {
-  void* skinny;  // counters followed by the h buffer
+  void* skinny;  // skinny-path scratch
   uint8_t* xq;
   float* xs;
   uint8_t* hq;
@@ -168,7 +154,7 @@ FfnWs ffn_layout(void* base, int64_t M, int64_t H, int64_t I) {
   char* b = static_cast<char*>(base);
   size_t off = 0;
   w.skinny = b;
-  off += M <= kSkinnyMaxM ? skinny_gateup_ws_bytes(M, I) : kSkinnyCounterBytes;
+  off += M <= kSkinnyMaxM ? skinny_scratch_bytes(M, H, I) : 0;
   w.xq = reinterpret_cast<uint8_t*>(b + off);
   off += align256(static_cast<size_t>(M * H));
   w.xs = reinterpret_cast<float*>(b + off);
@@ -189,8 +175,8 @@ int run_gateup(hipStream_t st, Path path, const uint8_t* xq, const float* xs, co
 }
 
 int run_down(hipStream_t st, Path path, const uint8_t* hq, const float* hs, const uint8_t* wq, const float* ws,
-             uint16_t* out, float* tap, int64_t M, int64_t H, int64_t I) {
-  if (path == Path::kSkinny) return hip_status(launch_down_skinny(st, hq, hs, wq, ws, out, tap, M, H, I));
+             uint16_t* out, float* tap, int64_t M, int64_t H, int64_t I, void* skinny_ws) {
+  if (path == Path::kSkinny) return hip_status(launch_down_skinny(st, hq, hs, wq, ws, out, tap, M, H, I, skinny_ws));
   return hip_status(launch_down_tiled(st, hq, hs, wq, ws, out, tap, M, H, I));
 }
 
@@ -213,13 +199,9 @@ int validate_ffn(const uint16_t* x, const uint16_t* norm_w, const uint8_t* wgu_q
 int ffn_core(hipStream_t st, const uint16_t* x, const uint16_t* norm_w, const uint8_t* wgu_q, const float* wgu_s,
              const uint8_t* wd_q, const float* wd_s, uint16_t* out, int64_t M, int64_t H, int64_t I, Path path,
              const FfnWs& w) {
-  // The norm kernel clears the skinny gate/up counters on its way (a
-  // caller-owned workspace may hold anything).
-  uint32_t* clear = path == Path::kSkinny ? static_cast<uint32_t*>(w.skinny) : nullptr;
-  if (launch_rmsnorm_quant(st, x, norm_w, w.xq, w.xs, M, H, clear, static_cast<int>(I / kGroup)) != hipSuccess)
-    return LACACHE_ERR_HIP;
+  if (launch_rmsnorm_quant(st, x, norm_w, w.xq, w.xs, M, H) != hipSuccess) return LACACHE_ERR_HIP;
   RETURN_IF(run_gateup(st, path, w.xq, w.xs, wgu_q, wgu_s, w.hq, w.hs, nullptr, M, H, I, w.skinny));
-  return run_down(st, path, w.hq, w.hs, wd_q, wd_s, out, nullptr, M, H, I);
+  return run_down(st, path, w.hq, w.hs, wd_q, wd_s, out, nullptr, M, H, I, w.skinny);
 }
 
 }  // namespace
@@ -257,7 +239,7 @@ int lacache_gateup_swiglu_quant(void* stream, const uint8_t* xq, const float* xs
   RETURN_IF(check_dim(H, kMaxH));
   RETURN_IF(check_dim(I, kMaxI));
   Path path;
-  RETURN_IF(choose_path(M, &path));
+  RETURN_IF(choose_path(M, H, I, &path));
   if (M == 0) return LACACHE_OK;
   if (!ptrs_ok({xq, xs, wgu_q, wgu_s, hq, hs}) || !opt_ptr_ok(h_tap)) return LACACHE_ERR_INVALID_ARG;
   if (!disjoint({rng(hq, M * I), rng(hs, (I / 128) * M * 4), rng(h_tap, h_tap ? M * I * 4 : 0)},
@@ -266,11 +248,7 @@ int lacache_gateup_swiglu_quant(void* stream, const uint8_t* xq, const float* xs
     return LACACHE_ERR_INVALID_ARG;
   hipStream_t st = static_cast<hipStream_t>(stream);
   void* skinny = nullptr;
-  if (path == Path::kSkinny) {
-    // counters at offset 0 of the library workspace: zero since allocation,
-    // re-armed by every skinny gate/up kernel
-    RETURN_IF(get_workspace(st, skinny_gateup_ws_bytes(M, I), &skinny));
-  }
+  if (path == Path::kSkinny) RETURN_IF(get_workspace(skinny_scratch_bytes(M, H, I), &skinny));
   return run_gateup(st, path, xq, xs, wgu_q, wgu_s, hq, hs, h_tap, M, H, I, skinny);
 }
 
@@ -281,13 +259,16 @@ int lacache_down_proj(void* stream, const uint8_t* hq, const float* hs, const ui
   RETURN_IF(check_dim(H, kMaxH));
   RETURN_IF(check_dim(I, kMaxI));
   Path path;
-  RETURN_IF(choose_path(M, &path));
+  RETURN_IF(choose_path(M, H, I, &path));
   if (M == 0) return LACACHE_OK;
   if (!ptrs_ok({hq, hs, wd_q, wd_s, out}) || !opt_ptr_ok(out_tap)) return LACACHE_ERR_INVALID_ARG;
   if (!disjoint({rng(out, M * H * 2), rng(out_tap, out_tap ? M * H * 4 : 0)},
                 {rng(hq, M * I), rng(hs, (I / 128) * M * 4), rng(wd_q, H * I), rng(wd_s, (H / 128) * (I / 128) * 4)}))
     return LACACHE_ERR_INVALID_ARG;
-  return run_down(static_cast<hipStream_t>(stream), path, hq, hs, wd_q, wd_s, out, out_tap, M, H, I);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  void* skinny = nullptr;
+  if (path == Path::kSkinny) RETURN_IF(get_workspace(skinny_scratch_bytes(M, H, I), &skinny));
+  return run_down(st, path, hq, hs, wd_q, wd_s, out, out_tap, M, H, I, skinny);
 }
 
 size_t lacache_ffn_workspace_bytes(int64_t M, int64_t H, int64_t I, int group) {
@@ -302,11 +283,11 @@ int lacache_ffn_fp8(void* stream, const uint16_t* x, const uint16_t* norm_w, con
                     int64_t I, int group) {
   RETURN_IF(validate_ffn(x, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, M, H, I, group));
   Path path;
-  RETURN_IF(choose_path(M, &path));
+  RETURN_IF(choose_path(M, H, I, &path));
   if (M == 0) return LACACHE_OK;
   hipStream_t st = static_cast<hipStream_t>(stream);
   void* base = nullptr;
-  RETURN_IF(get_workspace(st, ffn_layout(nullptr, M, H, I).total, &base));
+  RETURN_IF(get_workspace(ffn_layout(nullptr, M, H, I).total, &base));
   return ffn_core(st, x, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, M, H, I, path, ffn_layout(base, M, H, I));
 }
 
@@ -315,7 +296,7 @@ int lacache_ffn_fp8_ws(void* stream, const uint16_t* x, const uint16_t* norm_w, 
                        int64_t H, int64_t I, int group, void* workspace, size_t ws_bytes) {
   RETURN_IF(validate_ffn(x, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, M, H, I, group));
   Path path;
-  RETURN_IF(choose_path(M, &path));
+  RETURN_IF(choose_path(M, H, I, &path));
   if (M == 0) return LACACHE_OK;
   const FfnWs lay = ffn_layout(workspace, M, H, I);
   if (workspace == nullptr || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0 || ws_bytes < lay.total)

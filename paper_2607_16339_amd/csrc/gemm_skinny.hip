@@ -1,278 +1,451 @@
-// Skinny-M (M <= 64) FP8 GEMMs for block-only calls: bound by streaming the
-// fp8 weights from HBM once, so they are spread over many workgroups that
-// each own a thin slice of weight rows and the whole K.
+// Skinny-M (M <= 64) FP8 GEMMs for block-only calls (Sec. 3.4 linears at a
+// decode block's 32 tokens). At this size the FFN is bound by streaming the
+// fp8 weights from HBM once, so the kernels are built around that stream:
 //
-//   gate/up: workgroup c owns h-columns [16c, 16c+16): gate rows 16c.. and up
-//            rows I+16c.. of Wgu. Its wavefronts split K by interleaved
-//            K-groups, each K-group is one 16x16x128 FP8 MFMA per 16-row slab
-//            of x, scaled by RN32(x_scale * w_scale) into fp32. The partial
-//            sums meet in LDS (fixed order), SwiGLU gives h in fp32, and h is
-//            parked in a small fp32 workspace. The 8 workgroups of one
-//            128-wide h-group count themselves in; the last to arrive
-//            quantizes the group (row amax, scale, e4m3 codes) and re-arms
-//            the counter.
-//   down:    workgroup c owns output columns [16c, 16c+16) of W_down, same
-//            K split and LDS reduction, bf16 store.
+//   * a workgroup owns NW x NS slabs of 16 weight rows and a range of
+//     K-groups, and walks the range in blocks of two K-groups (256 bytes of
+//     each row);
+//   * every block of weights and of the M activation rows goes global -> LDS
+//     with direct-to-LDS copies into a ring of D slots, D - 1 blocks ahead of
+//     the multiply, so D - 1 blocks per CU are always in flight;
+//   * the copies are issued with inline asm and waited for with explicit
+//     vmcnt counts (loads retire in issue order), so the compiler never adds
+//     a wait that would drain the ring;
+//   * in LDS, row r's 16-byte chunk c sits at chunk c ^ (r mod 16), so the
+//     16 rows of an MFMA operand read hit 16 different bank groups, while each
+//     copy instruction still reads 256 contiguous bytes of a row;
+//   * each K-group of each 16 x 16 output tile is one 16x16x128 FP8 MFMA,
+//     added to the fp32 accumulator times RN32(x_scale * w_scale).
+//
+// gate/up: NW = 3 waves, each owning the gate rows 16p.. and the matching up
+//          rows I + 16p.. (NS = 2), all of K; SwiGLU in registers, h stored
+//          as fp32. A second kernel quantizes h per 1x128 group (a group's
+//          columns come from several workgroups, and stream order is the
+//          cheapest way to make all of them visible).
+// down:    NW = 4 waves x 16 output columns, K split over KS workgroups that
+//          store fp32 partials; a second kernel adds them in split order and
+//          rounds to bf16.
 #include "device.h"
 #include "launch.h"
+
+#pragma clang diagnostic ignored "-Winline-asm"
 
 namespace lacache {
 namespace {
 
-constexpr int kCols = 16;                    // weight rows (output columns) per workgroup slice
-constexpr int kSlicesPerGroup = kGroup / kCols;
+constexpr int kRowBytes = 256;  // one block: two K-groups of a row
+constexpr int kMaxNkb = 64;     // K-groups per workgroup (scales staged in LDS)
+constexpr int kGuWaves = 3;     // gate/up: (gate, up) slab pairs per workgroup
+constexpr int kDnWaves = 4;     // down: 16-column slabs per workgroup
+constexpr int kDnCols = kDnWaves * 16;
+#ifndef LACACHE_SKINNY_ROT
+#define LACACHE_SKINNY_ROT 1
+#endif
+// Workgroups start their walk over K at different blocks (and wrap), so that
+// at any moment the chip's copies spread over all memory channels instead of
+// all reading the same K offset of rows that are a multiple of 4 KB apart.
+constexpr bool kRotateK = LACACHE_SKINNY_ROT != 0;
 
-__device__ __forceinline__ v8i load_frag_global(const uint8_t* p) {
-  // lane q reads bytes [16q, 16q+16) and [64+16q, 64+16q+16) of the row's K-group
-  const uint4 lo = *reinterpret_cast<const uint4*>(p);
-  const uint4 hi = *reinterpret_cast<const uint4*>(p + 64);
+__device__ __forceinline__ uint32_t lds_u32(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) char*)(p)));
+}
+
+// 16 bytes per lane global -> LDS (lane l lands at lds + 16 l). Inline asm so
+// the compiler neither waits for it nor reorders memory accesses across it.
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+}
+
+// s_waitcnt vmcnt(n), n < 64, other counters untouched.
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
+}
+
+// s_waitcnt vmcnt(n) lgkmcnt(0): this wave's copies up to n-from-last have
+// landed and its LDS reads have returned (so the slot they read may be
+// overwritten once every wave has passed the next barrier).
+template <int N>
+__device__ __forceinline__ void wait_vm_lds() {
+  static_assert(N >= 0 && N < 64, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt(0x0070 | (N & 15) | ((N >> 4) << 14));
+}
+
+__device__ __forceinline__ void bar() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// MFMA operand from a ring slot laid out [row][256 B] with the chunk xor:
+// lane (q, lr) takes row base + lr, logical chunks kk*8 + q and kk*8 + 4 + q.
+__device__ __forceinline__ v8i ring_frag(const uint8_t* slab, int lr, int q, int kk) {
+  const uint8_t* row = slab + lr * kRowBytes;
+  const uint4 lo = *reinterpret_cast<const uint4*>(row + (((kk * 8 + q) ^ lr) << 4));
+  const uint4 hi = *reinterpret_cast<const uint4*>(row + (((kk * 8 + 4 + q) ^ lr) << 4));
   v8i f;
   f[0] = static_cast<int>(lo.x); f[1] = static_cast<int>(lo.y); f[2] = static_cast<int>(lo.z); f[3] = static_cast<int>(lo.w);
   f[4] = static_cast<int>(hi.x); f[5] = static_cast<int>(hi.y); f[6] = static_cast<int>(hi.z); f[7] = static_cast<int>(hi.w);
   return f;
 }
 
-template <int MT, int NB>
-struct SkinnyOperands {
-  v8i a[MT];
-  v8i b[NB];
-  float xs[MT][4];
-  float ws[NB];
+template <bool kGateUp, int MT, int D>
+struct Cfg {
+  static constexpr int NW = kGateUp ? kGuWaves : kDnWaves;
+  static constexpr int NS = kGateUp ? 2 : 1;
+  static constexpr int RA = MT * 16;                     // activation rows in a slot (padded)
+  static constexpr int kA = RA * kRowBytes;              // activation bytes per slot
+  static constexpr int kW = NW * NS * 16 * kRowBytes;    // weight bytes per slot
+  static constexpr int kSlot = kA + kW;
+  static constexpr int AI = RA / 4;                      // 1 KB copies of activations per block
+  static constexpr int AIW = (AI + NW - 1) / NW;         // ... per wave (the last may repeat one)
+  static constexpr int WI = NS * 4;                      // 1 KB copies of weights per wave per block
+  static constexpr int PER = AIW + WI;                   // copies per wave per block
 };
 
-// Loads one K-group's operands: activation slabs (rows 16i + lr, zero past M),
-// weight slices and the scales.
-template <int MT, int NB>
-__device__ __forceinline__ void skinny_load(SkinnyOperands<MT, NB>& o, const uint8_t* __restrict__ aq,
-                                            const float* __restrict__ as, const uint8_t* const* wrow,
-                                            const float* __restrict__ bs, const int64_t* nb, int64_t kb,
-                                            int64_t KB, int64_t M, int64_t K, int q, int lr) {
-  const v8i z = {0, 0, 0, 0, 0, 0, 0, 0};
-#pragma unroll
-  for (int i = 0; i < MT; ++i) {
-    const int64_t row = 16 * i + lr;
-    o.a[i] = row < M ? load_frag_global(aq + row * K + kb * 128 + 16 * q) : z;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int64_t sr = 16 * i + 4 * q + r;
-      o.xs[i][r] = sr < M ? as[kb * M + sr] : 0.0f;
-    }
-  }
-#pragma unroll
-  for (int n = 0; n < NB; ++n) {
-    o.b[n] = load_frag_global(wrow[n] + kb * 128 + 16 * q);
-    o.ws[n] = bs[nb[n] * KB + kb];
-  }
-}
+template <bool kGateUp, int MT, int D>
+__global__ __launch_bounds__((kGateUp ? kGuWaves : kDnWaves) * 64) void skinny_kernel(
+    const uint8_t* __restrict__ aq, const float* __restrict__ as,  // activations [M x K], scales [K/128 x M]
+    const uint8_t* __restrict__ wq, const float* __restrict__ ws,  // weights [N x K], scales [N/128 x K/128]
+    float* __restrict__ h_tap, float* __restrict__ wsbuf, int64_t M, int64_t K, int64_t N, int64_t I, int KS) {
+  using C = Cfg<kGateUp, MT, D>;
+  constexpr int NW = C::NW, NS = C::NS, RA = C::RA;
+  __shared__ __align__(16) uint8_t ring[D * C::kSlot];
+  __shared__ __align__(16) float sXs[kMaxNkb * RA];
+  __shared__ float sWs[NW * NS * kMaxNkb];
 
-template <int MT, int NB>
-__device__ __forceinline__ void skinny_mma(float (&acc)[MT][NB][4], const SkinnyOperands<MT, NB>& o) {
-#pragma unroll
-  for (int n = 0; n < NB; ++n)
-#pragma unroll
-    for (int i = 0; i < MT; ++i) {
-      const v4f zero = {0.0f, 0.0f, 0.0f, 0.0f};
-      const v4f p = mfma_fp8_16x16x128(o.a[i], o.b[n], zero);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) acc[i][n][r] = __builtin_fmaf(p[r], o.xs[i][r] * o.ws[n], acc[i][n][r]);
-    }
-}
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = wave_uniform(t >> 6);
+  const int q = lane >> 4, lr = lane & 15;
+  const int64_t KB = K / 128;
 
-// K loop of one wavefront (K-groups wave, wave + NW, ...) with one K-group of
-// operands in flight while the previous one is multiplied.
-template <int MT, int NB, int NW>
-__device__ __forceinline__ void skinny_kloop(float (&acc)[MT][NB][4], const uint8_t* __restrict__ aq,
-                                             const float* __restrict__ as, const uint8_t* const* wrow,
-                                             const float* __restrict__ bs, const int64_t* nb, int64_t KB,
-                                             int64_t M, int64_t K, int wave, int q, int lr) {
+  // ---- work of this workgroup and wavefront
+  int64_t kb0, kb1, slab_row[NS];
+  bool active;
+  int64_t pair = 0, cg = 0, sp = 0;
+  if (kGateUp) {
+    pair = static_cast<int64_t>(blockIdx.x) * NW + wave;  // h-columns 16 pair ..
+    active = pair < I / 16;
+    const int64_t p = active ? pair : 0;
+    slab_row[0] = 16 * p;           // gate rows
+    slab_row[NS - 1] = I + 16 * p;  // up rows
+    kb0 = 0;
+    kb1 = KB;
+  } else {
+    cg = blockIdx.x / KS;  // 64-column group
+    sp = blockIdx.x % KS;  // K split
+    const int64_t sub = cg * NW + wave;
+    active = 16 * sub < N;
+    slab_row[0] = 16 * (active ? sub : 0);
+    kb0 = sp * KB / KS;
+    kb1 = (sp + 1) * KB / KS;
+  }
+  const int nkb = static_cast<int>(kb1 - kb0);
+  const int NB = (nkb + 1) / 2;
+  // block visited at step b (steps past the end repeat the last visited block)
+  const int rot = kRotateK ? static_cast<int>((blockIdx.x >> 3) % static_cast<unsigned>(NB)) : 0;
+  auto block_at = [&](int b) {
+    int bb = (b < NB ? b : NB - 1) + rot;
+    return bb >= NB ? bb - NB : bb;
+  };
+
+  // ---- copy plan. Copy instruction u of a 16-row slab covers rows 4u..4u+3;
+  // lane l fills slot chunk l%16 of row 4u + l/16 with logical chunk
+  // (l%16) ^ row, i.e. K-group half (chunk / 8) and 16-byte piece chunk % 8.
+  const int crow = lane >> 4;  // row within the copy's 4 rows
+  const int pch = lane & 15;   // physical chunk in LDS
+  // activations: wave copies instructions a = wave + NW j (clamped: repeats are identical writes)
+  int64_t a_off[C::AIW];
+  int a_dst[C::AIW];
+  int a_half[C::AIW];
+#pragma unroll
+  for (int j = 0; j < C::AIW; ++j) {
+    int a = wave + NW * j;
+    if (a > C::AI - 1) a = C::AI - 1;
+    const int row = 4 * a + crow;                        // slot row
+    const int lch = pch ^ (row & 15);
+    const int64_t gr = row < M ? row : M - 1;
+    a_off[j] = gr * K + (lch & 7) * 16;
+    a_half[j] = lch >> 3;
+    a_dst[j] = a * 1024;
+  }
+  int64_t w_off[C::WI];
+  int w_half[C::WI];
+  int w_dst[C::WI];
+#pragma unroll
+  for (int n = 0; n < NS; ++n)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int row = 4 * u + crow;
+      const int lch = pch ^ row;
+      w_off[n * 4 + u] = (slab_row[n] + row) * K + (lch & 7) * 16;
+      w_half[n * 4 + u] = lch >> 3;
+      w_dst[n * 4 + u] = C::kA + ((wave * NS + n) * 16 * kRowBytes) + u * 1024;
+    }
+
+  // Issues the copies of step b (the repeats past the end rewrite the last
+  // block's own data into an idle slot).
+  auto issue = [&](int b, int slot) {
+    const int bb = block_at(b);
+    const uint32_t base = lds_u32(ring + slot * C::kSlot);
+#pragma unroll
+    for (int j = 0; j < C::AIW; ++j) {
+      int64_t kg = kb0 + 2 * bb + a_half[j];
+      if (kg >= kb1) kg = kb1 - 1;
+      dma16(aq + a_off[j] + kg * 128, wave_uniform(static_cast<int>(base) + a_dst[j]));
+    }
+#pragma unroll
+    for (int i = 0; i < C::WI; ++i) {
+      int64_t kg = kb0 + 2 * bb + w_half[i];
+      if (kg >= kb1) kg = kb1 - 1;
+      dma16(wq + w_off[i] + kg * 128, wave_uniform(static_cast<int>(base) + w_dst[i]));
+    }
+  };
+
+  float acc[MT][NS][4];
 #pragma unroll
   for (int i = 0; i < MT; ++i)
 #pragma unroll
-    for (int n = 0; n < NB; ++n)
+    for (int n = 0; n < NS; ++n)
 #pragma unroll
       for (int r = 0; r < 4; ++r) acc[i][n][r] = 0.0f;
-  if (wave >= KB) return;
-  SkinnyOperands<MT, NB> cur, nxt;
-  skinny_load<MT, NB>(cur, aq, as, wrow, bs, nb, wave, KB, M, K, q, lr);
-  for (int64_t kb = wave; kb < KB; kb += NW) {
-    const bool more = kb + NW < KB;
-    if (more) skinny_load<MT, NB>(nxt, aq, as, wrow, bs, nb, kb + NW, KB, M, K, q, lr);
-    skinny_mma<MT, NB>(acc, cur);
-    if (more) cur = nxt;
-  }
-}
 
-// Fixed-order sum of the NW wavefronts' accumulators through LDS; wavefront 0
-// ends with the totals.
-template <int MT, int NB, int NW>
-__device__ __forceinline__ void skinny_reduce(float (&acc)[MT][NB][4], float* red, int wave, int lane) {
-  constexpr int E = MT * NB * 4;
-  if (wave != 0) {
+  // ---- the stream: D - 1 blocks ahead
 #pragma unroll
-    for (int i = 0; i < MT; ++i)
+  for (int b = 0; b < D - 1; ++b) issue(b, b);
+
+  // ---- scales for the whole K range, staged in LDS. Loaded after the first
+  // copies are on their way and all issued before any is stored, so the
+  // staging costs one memory latency, overlapped with the copies'.
+  {
+    constexpr int XPT = (kMaxNkb * RA + NW * 64 - 1) / (NW * 64);
+    constexpr int WPT = (NW * NS * kMaxNkb + NW * 64 - 1) / (NW * 64);
+    float xv[XPT], wv[WPT];
 #pragma unroll
-      for (int n = 0; n < NB; ++n)
+    for (int j = 0; j < XPT; ++j) {
+      const int i = t + j * NW * 64;
+      const int kb = i / RA, m = i % RA;
+      xv[j] = (i < nkb * RA && m < M) ? as[(kb0 + kb) * M + m] : 0.0f;
+    }
 #pragma unroll
-        for (int r = 0; r < 4; ++r) red[((wave - 1) * E + (i * NB + n) * 4 + r) * 64 + lane] = acc[i][n][r];
+    for (int j = 0; j < WPT; ++j) {
+      const int i = t + j * NW * 64;
+      const int w = i / (NS * nkb), n = (i / nkb) % NS, kb = i % nkb;
+      int64_t r;
+      bool ok = i < NW * NS * nkb;
+      if (kGateUp) {
+        const int64_t p = static_cast<int64_t>(blockIdx.x) * NW + w;
+        ok = ok && p < I / 16;
+        r = n == 0 ? 16 * p : I + 16 * p;
+      } else {
+        const int64_t sub = cg * NW + w;
+        ok = ok && 16 * sub < N;
+        r = 16 * sub;
+      }
+      wv[j] = ok ? ws[(r / 128) * KB + kb0 + kb] : 0.0f;
+    }
+#pragma unroll
+    for (int j = 0; j < XPT; ++j) {
+      const int i = t + j * NW * 64;
+      if (i < nkb * RA) sXs[i] = xv[j];
+    }
+#pragma unroll
+    for (int j = 0; j < WPT; ++j) {
+      const int i = t + j * NW * 64;
+      if (i < NW * NS * nkb) sWs[i] = wv[j];
+    }
   }
   __syncthreads();
-  if (wave == 0) {
+
+  for (int b = 0; b < NB; ++b) {
+    wait_vm_lds<(D - 2) * C::PER>();  // block b has landed (later blocks may still fly)
+    bar();                            // ... for every wave; and slot (b-1) % D is free
+    issue(b + D - 1, (b + D - 1) % D);
+    const uint8_t* slot = ring + (b % D) * C::kSlot;
+    const int bk = block_at(b);
 #pragma unroll
-    for (int w = 1; w < NW; ++w)
+    for (int kk = 0; kk < 2; ++kk) {
+      const int kb = 2 * bk + kk;
+      if (kb >= nkb) break;
+      v8i af[MT];
+      float xa[MT][4];
 #pragma unroll
-      for (int i = 0; i < MT; ++i)
+      for (int i = 0; i < MT; ++i) {
+        af[i] = ring_frag(slot + i * 16 * kRowBytes, lr, q, kk);
+        const float4 xv = *reinterpret_cast<const float4*>(sXs + kb * RA + 16 * i + 4 * q);
+        xa[i][0] = xv.x; xa[i][1] = xv.y; xa[i][2] = xv.z; xa[i][3] = xv.w;
+      }
 #pragma unroll
-        for (int n = 0; n < NB; ++n)
+      for (int n = 0; n < NS; ++n) {
+        const v8i bf = ring_frag(slot + C::kA + (wave * NS + n) * 16 * kRowBytes, lr, q, kk);
+        const float w = sWs[(wave * NS + n) * nkb + kb];
 #pragma unroll
-          for (int r = 0; r < 4; ++r) acc[i][n][r] += red[((w - 1) * E + (i * NB + n) * 4 + r) * 64 + lane];
+        for (int i = 0; i < MT; ++i) {
+          const v4f zero = {0.0f, 0.0f, 0.0f, 0.0f};
+          const v4f p = mfma_fp8_16x16x128(af[i], bf, zero);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) acc[i][n][r] = __builtin_fmaf(p[r], xa[i][r] * w, acc[i][n][r]);
+        }
+      }
+    }
   }
-}
+  wait_vm<0>();  // drain the trailing repeat copies
 
-template <int MT, int NW>
-__global__ __launch_bounds__(NW * 64) void gateup_skinny_kernel(
-    const uint8_t* __restrict__ xq, const float* __restrict__ xs, const uint8_t* __restrict__ wq,
-    const float* __restrict__ ws, uint8_t* __restrict__ hq, float* __restrict__ hs, float* __restrict__ h_tap,
-    float* __restrict__ hbuf, unsigned* __restrict__ counters, int64_t M, int64_t H, int64_t I) {
-  __shared__ float red[(NW - 1) * MT * 2 * 4 * 64];
-  __shared__ int last;
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int q = lane >> 4, lr = lane & 15;
-  const int64_t c = blockIdx.x;
-  const int64_t hg = c / kSlicesPerGroup;
-  const int64_t KB = H / 128;
-  const uint8_t* wrow[2] = {wq + (c * kCols + lr) * H, wq + (I + c * kCols + lr) * H};
-  const int64_t nb[2] = {hg, I / 128 + hg};
-
-  float acc[MT][2][4];
-  skinny_kloop<MT, 2, NW>(acc, xq, xs, wrow, ws, nb, KB, M, H, wave, q, lr);
-  skinny_reduce<MT, 2, NW>(acc, red, wave, lane);
-
-  if (wave == 0) {
+  if (!active) return;
+  if (kGateUp) {
+    // ---- SwiGLU, h -> fp32 [M x I]
 #pragma unroll
     for (int i = 0; i < MT; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int64_t row = 16 * i + 4 * q + r;
-        const float g = acc[i][0][r], u = acc[i][1][r];
-        const float h = g / (1.0f + expf(-g)) * u;
         if (row < M) {
-          hbuf[row * I + c * kCols + lr] = h;
-          if (h_tap != nullptr) h_tap[row * I + c * kCols + lr] = h;
+          const float h = swiglu_fast(acc[i][0][r], acc[i][NS - 1][r]);
+          wsbuf[row * I + 16 * pair + lr] = h;
+          if (h_tap != nullptr) h_tap[row * I + 16 * pair + lr] = h;
         }
       }
-    __threadfence();  // release this slice's h before counting in
-    if (lane == 0) last = (atomicAdd(counters + hg, 1u) == kSlicesPerGroup - 1);
+  } else {
+    // ---- fp32 partial of this K split -> [KS x M x N]
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t row = 16 * i + 4 * q + r;
+        if (row < M) wsbuf[(sp * M + row) * N + slab_row[0] + lr] = acc[i][0][r];
+      }
   }
-  __syncthreads();
-  if (!last) return;  // uniform across the workgroup
-  __threadfence();    // acquire the other slices' h
+}
 
-  // Last arrival: quantize the 128-wide h-group of every row. Four threads per
-  // row, 32 consecutive values each.
-  const int64_t row = t >> 2;
-  const int part = t & 3;
-  for (int64_t r0 = 0; r0 < M; r0 += (NW * 64) / 4) {
-    const int64_t rr = r0 + row;
-    const bool ok = rr < M;
-    float v[32];
-    const float4* src = reinterpret_cast<const float4*>(hbuf + rr * I + hg * 128 + part * 32);
+// h [M x I] fp32 -> 1x128 e4m3 groups (Eq. 7): codes [M x I], scales
+// [I/128 x M]. 16 lanes per group, 8 values per lane.
+__global__ __launch_bounds__(256) void skinny_hquant_kernel(const float* __restrict__ h, uint8_t* __restrict__ hq,
+                                                            float* __restrict__ hs, int64_t M, int64_t I) {
+  const int64_t gi = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) >> 4;  // group index, row-major
+  const int part = threadIdx.x & 15;
+  const int64_t G = I / 128;
+  const bool ok = gi < M * G;
+  const int64_t row = ok ? gi / G : 0, g = ok ? gi % G : 0;
+  float v[8];
+  const float4* src = reinterpret_cast<const float4*>(h + row * I + g * 128 + part * 8);
+  const float4 a = src[0], b = src[1];
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+  float m = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) m = __builtin_fmaxf(m, __builtin_fabsf(v[e]));
+  m = max_xor<16>(m);
+  const float s = m / kE4M3Max;
+  const bool fast = scale_is_fast(s);
+  const float rs = fast_rcp(s);
+  uint32_t w[2] = {0u, 0u};
+  if (s != 0.0f) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const float4 f = ok ? src[e] : make_float4(0.f, 0.f, 0.f, 0.f);
-      v[4 * e] = f.x; v[4 * e + 1] = f.y; v[4 * e + 2] = f.z; v[4 * e + 3] = f.w;
-    }
-    float a = 0.0f;
-#pragma unroll
-    for (int e = 0; e < 32; ++e) a = __builtin_fmaxf(a, __builtin_fabsf(v[e]));
-    a = max_xor<4>(a);
-    const float s = a / kE4M3Max;
-    uint32_t w[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-      w[e] = s == 0.0f ? 0u
-                       : enc4_e4m3(qdiv(v[4 * e], s), qdiv(v[4 * e + 1], s), qdiv(v[4 * e + 2], s),
-                                   qdiv(v[4 * e + 3], s));
-    if (ok) {
-      uint4* dst = reinterpret_cast<uint4*>(hq + rr * I + hg * 128 + part * 32);
-      dst[0] = make_uint4(w[0], w[1], w[2], w[3]);
-      dst[1] = make_uint4(w[4], w[5], w[6], w[7]);
-      if (part == 0) hs[hg * M + rr] = s;
+      const uint32_t c = fast ? enc1_div_fast(v[e], s, rs) : enc1_e4m3(qdiv(v[e], s));
+      w[e >> 2] |= c << (8 * (e & 3));
     }
   }
-  if (t == 0) counters[hg] = 0u;  // re-arm for the next call on this stream
+  if (!ok) return;
+  *reinterpret_cast<uint2*>(hq + row * I + g * 128 + part * 8) = make_uint2(w[0], w[1]);
+  if (part == 0) hs[g * M + row] = s;
 }
 
-template <int MT, int NW>
-__global__ __launch_bounds__(NW * 64) void down_skinny_kernel(
-    const uint8_t* __restrict__ hq, const float* __restrict__ hs, const uint8_t* __restrict__ wq,
-    const float* __restrict__ ws, uint16_t* __restrict__ out, float* __restrict__ out_tap, int64_t M, int64_t H,
-    int64_t I) {
-  __shared__ float red[(NW - 1) * MT * 1 * 4 * 64];
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int q = lane >> 4, lr = lane & 15;
-  const int64_t c = blockIdx.x;
+// out = RNE_bf16(sum of the KS partials, in split order); 4 columns per thread.
+__global__ __launch_bounds__(256) void skinny_reduce_kernel(const float* __restrict__ part, uint16_t* __restrict__ out,
+                                                            float* __restrict__ out_tap, int64_t MN, int KS) {
+  const int64_t e = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 4;
+  if (e >= MN) return;
+  float4 acc = *reinterpret_cast<const float4*>(part + e);
+  for (int s = 1; s < KS; ++s) {
+    const float4 p = *reinterpret_cast<const float4*>(part + s * MN + e);
+    acc.x += p.x; acc.y += p.y; acc.z += p.z; acc.w += p.w;
+  }
+  *reinterpret_cast<uint2*>(out + e) = make_uint2(pack_bf16x2(acc.x, acc.y), pack_bf16x2(acc.z, acc.w));
+  if (out_tap != nullptr) *reinterpret_cast<float4*>(out_tap + e) = acc;
+}
+
+// Ring depth per (path, M-tiles): the deepest ring that fits the LDS.
+template <bool kGateUp, int MT>
+constexpr int ring_depth() {
+  return kGateUp ? (MT <= 2 ? 4 : 3) : (MT <= 2 ? 5 : 4);
+}
+
+int down_splits(int64_t H, int64_t I) {
   const int64_t KB = I / 128;
-  const uint8_t* wrow[1] = {wq + (c * kCols + lr) * I};
-  const int64_t nb[1] = {(c * kCols) / 128};
-
-  float acc[MT][1][4];
-  skinny_kloop<MT, 1, NW>(acc, hq, hs, wrow, ws, nb, KB, M, I, wave, q, lr);
-  skinny_reduce<MT, 1, NW>(acc, red, wave, lane);
-  if (wave == 0) {
-#pragma unroll
-    for (int i = 0; i < MT; ++i)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int64_t row = 16 * i + 4 * q + r;
-        if (row < M) {
-          out[row * H + c * kCols + lr] = static_cast<uint16_t>(f32_to_bf16(acc[i][0][r]));
-          if (out_tap != nullptr) out_tap[row * H + c * kCols + lr] = acc[i][0][r];
-        }
-      }
-  }
+  const int64_t groups = (H + kDnCols - 1) / kDnCols;
+  int64_t ks = (256 + groups - 1) / groups;           // about one workgroup per CU
+  const int64_t need = (KB + kMaxNkb - 1) / kMaxNkb;  // K-groups per split fit the LDS scales
+  if (ks < need) ks = need;
+  if (ks > KB) ks = KB;
+  return static_cast<int>(ks);
 }
 
-constexpr int kGateUpWaves = 4;
-constexpr int kDownWaves = 8;
+template <bool kGateUp, int MT>
+hipError_t launch_skinny(hipStream_t st, const uint8_t* aq, const float* as, const uint8_t* wq, const float* ws,
+                         float* h_tap, float* wsbuf, int64_t M, int64_t K, int64_t N, int64_t I, int KS,
+                         unsigned grid) {
+  constexpr int D = ring_depth<kGateUp, MT>();
+  hipLaunchKernelGGL((skinny_kernel<kGateUp, MT, D>), dim3(grid), dim3(Cfg<kGateUp, MT, D>::NW * 64), 0, st, aq,
+                     as, wq, ws, h_tap, wsbuf, M, K, N, I, KS);
+  return hipGetLastError();
+}
 
 }  // namespace
 
-size_t skinny_gateup_ws_bytes(int64_t M, int64_t I) {
-  const size_t h = static_cast<size_t>(M) * static_cast<size_t>(I) * sizeof(float);
-  return kSkinnyCounterBytes + ((h + 255) / 256) * 256;
+bool skinny_supported(int64_t M, int64_t H, int64_t I) {
+  (void)I;
+  return M >= 1 && M <= kSkinnyMaxM && H / 128 <= kMaxNkb;
 }
 
-// Workspace layout: [counters: kSkinnyCounterBytes][hbuf: M x I fp32]. The
-// counters (I/128 words) must be zero when the kernel starts; the kernel
-// leaves them zero again.
+size_t skinny_gateup_ws_bytes(int64_t M, int64_t I) {
+  const size_t h = static_cast<size_t>(M) * static_cast<size_t>(I) * sizeof(float);
+  return ((h + 255) / 256) * 256;
+}
+
+size_t skinny_down_ws_bytes(int64_t M, int64_t H, int64_t I) {
+  const size_t p = static_cast<size_t>(down_splits(H, I)) * static_cast<size_t>(M) * static_cast<size_t>(H) * 4;
+  return ((p + 255) / 256) * 256;
+}
+
+// ws_buf: an fp32 buffer of skinny_*_ws_bytes() (h, or the down partials).
 hipError_t launch_gateup_skinny(hipStream_t st, const uint8_t* xq, const float* xs, const uint8_t* wq,
                                 const float* ws, uint8_t* hq, float* hs, float* h_tap, int64_t M, int64_t H,
                                 int64_t I, void* ws_buf) {
-  unsigned* counters = static_cast<unsigned*>(ws_buf);
-  float* hbuf = reinterpret_cast<float*>(static_cast<char*>(ws_buf) + kSkinnyCounterBytes);
-  dim3 grid(static_cast<unsigned>(I / kCols)), block(kGateUpWaves * 64);
+  float* hbuf = static_cast<float*>(ws_buf);
+  const unsigned grid = static_cast<unsigned>((I / 16 + kGuWaves - 1) / kGuWaves);
   const int mt = static_cast<int>((M + 15) / 16);
-#define LAUNCH_GU(MT_) \
-  hipLaunchKernelGGL((gateup_skinny_kernel<MT_, kGateUpWaves>), grid, block, 0, st, xq, xs, wq, ws, hq, hs, h_tap, hbuf, counters, M, H, I)
-  if (mt <= 1) LAUNCH_GU(1);
-  else if (mt == 2) LAUNCH_GU(2);
-  else if (mt == 3) LAUNCH_GU(3);
-  else LAUNCH_GU(4);
-#undef LAUNCH_GU
+  hipError_t e;
+#define GU(MT_) launch_skinny<true, MT_>(st, xq, xs, wq, ws, h_tap, hbuf, M, H, 2 * I, I, 1, grid)
+  if (mt <= 1) e = GU(1);
+  else if (mt == 2) e = GU(2);
+  else if (mt == 3) e = GU(3);
+  else e = GU(4);
+#undef GU
+  if (e != hipSuccess) return e;
+  const int64_t groups = M * (I / 128);
+  hipLaunchKernelGGL(skinny_hquant_kernel, dim3(static_cast<unsigned>((groups + 15) / 16)), dim3(256), 0, st, hbuf, hq,
+                     hs, M, I);
   return hipGetLastError();
 }
 
 hipError_t launch_down_skinny(hipStream_t st, const uint8_t* hq, const float* hs, const uint8_t* wq, const float* ws,
-                              uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I) {
-  dim3 grid(static_cast<unsigned>(H / kCols)), block(kDownWaves * 64);
+                              uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I, void* ws_buf) {
+  float* part = static_cast<float*>(ws_buf);
+  const int KS = down_splits(H, I);
+  const unsigned grid = static_cast<unsigned>(((H + kDnCols - 1) / kDnCols) * KS);
   const int mt = static_cast<int>((M + 15) / 16);
-#define LAUNCH_DN(MT_) \
-  hipLaunchKernelGGL((down_skinny_kernel<MT_, kDownWaves>), grid, block, 0, st, hq, hs, wq, ws, out, out_tap, M, H, I)
-  if (mt <= 1) LAUNCH_DN(1);
-  else if (mt == 2) LAUNCH_DN(2);
-  else if (mt == 3) LAUNCH_DN(3);
-  else LAUNCH_DN(4);
-#undef LAUNCH_DN
+  hipError_t e;
+#define DN(MT_) launch_skinny<false, MT_>(st, hq, hs, wq, ws, nullptr, part, M, I, H, I, KS, grid)
+  if (mt <= 1) e = DN(1);
+  else if (mt == 2) e = DN(2);
+  else if (mt == 3) e = DN(3);
+  else e = DN(4);
+#undef DN
+  if (e != hipSuccess) return e;
+  const int64_t mn = M * H;
+  hipLaunchKernelGGL(skinny_reduce_kernel, dim3(static_cast<unsigned>((mn / 4 + 255) / 256)), dim3(256), 0, st, part,
+                     out, out_tap, mn, KS);
   return hipGetLastError();
 }
 

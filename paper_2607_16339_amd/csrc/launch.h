@@ -9,10 +9,8 @@
 namespace lacache {
 
 hipError_t launch_quant_weights(hipStream_t st, const uint16_t* w, uint8_t* wq, float* ws, int64_t N, int64_t K);
-// `clear` (optional): clear_n 32-bit words zeroed by the kernel before the
-// next kernel in the stream starts (the skinny gate/up counters).
 hipError_t launch_rmsnorm_quant(hipStream_t st, const uint16_t* x, const uint16_t* nw, uint8_t* xq, float* xs,
-                                int64_t M, int64_t H, uint32_t* clear = nullptr, int clear_n = 0);
+                                int64_t M, int64_t H);
 hipError_t launch_add_bf16(hipStream_t st, uint16_t* x, const uint16_t* y, int64_t n);
 hipError_t launch_encode_e4m3(hipStream_t st, const float* v, uint8_t* codes, int64_t n);
 
@@ -23,17 +21,17 @@ hipError_t launch_gateup_tiled(hipStream_t st, const uint8_t* xq, const float* x
 hipError_t launch_down_tiled(hipStream_t st, const uint8_t* hq, const float* hs, const uint8_t* wq, const float* ws,
                              uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I);
 
-// Skinny weight-streaming GEMMs (M <= kSkinnyMaxM). The gate/up kernel needs
-// a workspace of skinny_gateup_ws_bytes(M, I) bytes that starts with a
-// counter block of kSkinnyCounterBytes (room for I/128 <= 512 words), which
-// must be zero when the kernel starts (the kernel leaves it zero again).
+// Skinny weight-streaming GEMMs (M <= kSkinnyMaxM, H <= 8192). Each needs an
+// fp32 scratch buffer of skinny_*_ws_bytes() (no initial contents); the two
+// stages may share one (they run one after the other on the stream).
 constexpr int64_t kSkinnyMaxM = 64;
-constexpr size_t kSkinnyCounterBytes = 2048;
+bool skinny_supported(int64_t M, int64_t H, int64_t I);
 size_t skinny_gateup_ws_bytes(int64_t M, int64_t I);
+size_t skinny_down_ws_bytes(int64_t M, int64_t H, int64_t I);
 hipError_t launch_gateup_skinny(hipStream_t st, const uint8_t* xq, const float* xs, const uint8_t* wq,
                                 const float* ws, uint8_t* hq, float* hs, float* h_tap, int64_t M, int64_t H,
                                 int64_t I, void* ws_buf);
 hipError_t launch_down_skinny(hipStream_t st, const uint8_t* hq, const float* hs, const uint8_t* wq, const float* ws,
-                              uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I);
+                              uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I, void* ws_buf);
 
 }  // namespace lacache

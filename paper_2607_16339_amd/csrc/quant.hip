@@ -71,11 +71,7 @@ template <int T>
 __global__ __launch_bounds__(256) void rmsnorm_quant_kernel(const uint16_t* __restrict__ x,
                                                             const uint16_t* __restrict__ nw,
                                                             uint8_t* __restrict__ xq, float* __restrict__ xs,
-                                                            int64_t M, int H, uint32_t* __restrict__ clear,
-                                                            int clear_n) {
-  // Optional: zero a small counter block for the kernel that runs next.
-  if (clear != nullptr && blockIdx.x == 0)
-    for (int i = threadIdx.x; i < clear_n; i += 256) clear[i] = 0u;
+                                                            int64_t M, int H) {
   const int lane = threadIdx.x & 63;
   const int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
   if (row >= M) return;  // uniform per wavefront; no workgroup barrier below
@@ -133,16 +129,16 @@ __global__ __launch_bounds__(256) void rmsnorm_quant_kernel(const uint16_t* __re
 }
 
 hipError_t launch_rmsnorm_quant(hipStream_t st, const uint16_t* x, const uint16_t* nw, uint8_t* xq, float* xs,
-                                int64_t M, int64_t H, uint32_t* clear, int clear_n) {
+                                int64_t M, int64_t H) {
   const int T = static_cast<int>((H + 511) / 512);
   dim3 grid(static_cast<unsigned>((M + 3) / 4)), block(256);
   const int h = static_cast<int>(H);
-  if (T <= 1) hipLaunchKernelGGL(rmsnorm_quant_kernel<1>, grid, block, 0, st, x, nw, xq, xs, M, h, clear, clear_n);
-  else if (T <= 2) hipLaunchKernelGGL(rmsnorm_quant_kernel<2>, grid, block, 0, st, x, nw, xq, xs, M, h, clear, clear_n);
-  else if (T <= 4) hipLaunchKernelGGL(rmsnorm_quant_kernel<4>, grid, block, 0, st, x, nw, xq, xs, M, h, clear, clear_n);
-  else if (T <= 8) hipLaunchKernelGGL(rmsnorm_quant_kernel<8>, grid, block, 0, st, x, nw, xq, xs, M, h, clear, clear_n);
-  else if (T <= 16) hipLaunchKernelGGL(rmsnorm_quant_kernel<16>, grid, block, 0, st, x, nw, xq, xs, M, h, clear, clear_n);
-  else hipLaunchKernelGGL(rmsnorm_quant_kernel<32>, grid, block, 0, st, x, nw, xq, xs, M, h, clear, clear_n);
+  if (T <= 1) hipLaunchKernelGGL(rmsnorm_quant_kernel<1>, grid, block, 0, st, x, nw, xq, xs, M, h);
+  else if (T <= 2) hipLaunchKernelGGL(rmsnorm_quant_kernel<2>, grid, block, 0, st, x, nw, xq, xs, M, h);
+  else if (T <= 4) hipLaunchKernelGGL(rmsnorm_quant_kernel<4>, grid, block, 0, st, x, nw, xq, xs, M, h);
+  else if (T <= 8) hipLaunchKernelGGL(rmsnorm_quant_kernel<8>, grid, block, 0, st, x, nw, xq, xs, M, h);
+  else if (T <= 16) hipLaunchKernelGGL(rmsnorm_quant_kernel<16>, grid, block, 0, st, x, nw, xq, xs, M, h);
+  else hipLaunchKernelGGL(rmsnorm_quant_kernel<32>, grid, block, 0, st, x, nw, xq, xs, M, h);
   return hipGetLastError();
 }
 
