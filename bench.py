@@ -32,7 +32,9 @@ PEAK_FP8_TFLOPS = 5033.0  # dense FP8 MFMA: 256 CU x 2.4 GHz x 8192 FLOP/clk
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pmc_traffic.json")
 KERNEL_SOURCES = {
     "gateup_skinny": ["gemm_skinny.hip", "device.h"],
+    "hquant_skinny": ["gemm_skinny.hip", "device.h"],
     "down_skinny": ["gemm_skinny.hip", "device.h"],
+    "reduce_skinny": ["gemm_skinny.hip", "device.h"],
     "gateup_tiled": ["gemm_tiled.hip", "device.h"],
     "down_tiled": ["gemm_tiled.hip", "device.h"],
 }
@@ -48,6 +50,11 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--profile-only", action="store_true",
                    help="run warmup + timed steps only (for rocprofv3), print the line without the CPU leg")
+    p.add_argument("--calibrate-copy", action="store_true",
+                   help="also run a plain device copy of 256 MiB three times (the HBM counter calibration)")
+    p.add_argument("--traffic-from", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "WORKLOAD"),
+                   help="turn two rocprofv3 --pmc counter CSVs (FETCH_SIZE, WRITE_SIZE) of a --calibrate-copy "
+                        "run into per-launch HBM bytes in profiles/pmc_traffic.json, then exit")
     return p.parse_args()
 
 
@@ -70,8 +77,82 @@ def stage_bytes(M, H, I):
     }
 
 
+COPY_BYTES = 256 << 20
+
+
+def kernel_key(name):
+    """Short kernel key of a rocprofv3 kernel name."""
+    if "skinny_kernel<true" in name:
+        return "gateup_skinny"
+    if "skinny_kernel<false" in name:
+        return "down_skinny"
+    if "skinny_hquant" in name:
+        return "hquant_skinny"
+    if "skinny_reduce" in name:
+        return "reduce_skinny"
+    if "gemm_tiled_kernel<true" in name:
+        return "gateup_tiled"
+    if "gemm_tiled_kernel<false" in name:
+        return "down_tiled"
+    if "rmsnorm_quant" in name:
+        return "rmsnorm_quant"
+    if "copyBuffer" in name:
+        return "copy"
+    return None
+
+
+def traffic_from(fetch_csv, write_csv, workload):
+    """Per-dispatch FETCH_SIZE / WRITE_SIZE (KiB) averaged per kernel, scaled by
+    the ratio of the known bytes of a plain 256 MiB device copy to what the
+    same counter reads for that copy."""
+    import csv
+    import collections
+
+    def per_kernel(path, counter):
+        per = collections.defaultdict(float)
+        names = {}
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            d = r["Dispatch_Id"]
+            per[d] += float(r["Counter_Value"])
+            names[d] = r["Kernel_Name"]
+        out = collections.defaultdict(list)
+        for d, v in per.items():
+            k = kernel_key(names[d])
+            if k:
+                out[k].append(v * 1024.0)  # KiB -> bytes
+        # the runtime's own small copies share the copy kernel: keep the 256 MiB ones
+        big = max(out["copy"])
+        out["copy"] = [v for v in out["copy"] if v > big / 2]
+        return {k: sum(v) / len(v) for k, v in out.items()}
+
+    fetch = per_kernel(fetch_csv, "FETCH_SIZE")
+    write = per_kernel(write_csv, "WRITE_SIZE")
+    f_scale = COPY_BYTES / fetch["copy"]
+    w_scale = COPY_BYTES / write["copy"]
+    try:
+        with open(TRAFFIC_FILE) as f:
+            table = json.load(f)
+    except (OSError, ValueError):
+        table = {}
+    for k in KERNEL_SOURCES:
+        if k in fetch and k in write:
+            table[k + ":" + workload] = {
+                "fetch_bytes": round(fetch[k] * f_scale), "write_bytes": round(write[k] * w_scale),
+                "hbm_bytes_per_launch": round(fetch[k] * f_scale + write[k] * w_scale),
+                "copy_scale": {"fetch": round(f_scale, 4), "write": round(w_scale, 4)},
+                "source_sha": source_sha(k)}
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(table, f, indent=1, sort_keys=True)
+    print(json.dumps({k: v for k, v in table.items() if k.endswith(":" + workload)}, indent=1))
+
+
 def main():
     args = parse()
+    if args.traffic_from:
+        traffic_from(*args.traffic_from)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (the FFN shards by rows with no "
@@ -117,15 +198,25 @@ def main():
         step(i)
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     t_wall = time.perf_counter()
-    e0.record(stream)
+    ev[0].record(stream)
     for i in range(args.steps):
         step(i)
-    e1.record(stream)
+        ev[i + 1].record(stream)
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
-    ms = e0.elapsed_time(e1) / args.steps
+    ms = ev[0].elapsed_time(ev[-1]) / args.steps
+    per_step = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)])
+    pct = {"p10": float(np.percentile(per_step, 10)), "p50": float(np.percentile(per_step, 50)),
+           "p90": float(np.percentile(per_step, 90))}
+    if args.calibrate_copy:
+        src = torch.empty(COPY_BYTES, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     flop = 6.0 * M * H * I
     tflops = flop / (ms * 1e-3) / 1e12
@@ -158,6 +249,9 @@ def main():
     k_ms = {k: float(np.mean([a.elapsed_time(b) for a, b in v])) for k, v in kt.items()}
     dom = "gateup"
     kname = dom + ("_skinny" if skinny else "_tiled")
+    # the skinny gate/up stage is the weight-streaming kernel followed by the
+    # small h-quantization kernel; both are inside the timed stage
+    kparts = ["gateup_skinny", "hquant_skinny"] if skinny else ["gateup_tiled"]
     if skinny:
         achieved = sb[dom] / (k_ms[dom] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
@@ -166,14 +260,16 @@ def main():
         achieved = 4.0 * M * H * I / (k_ms[dom] * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_FP8_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_FP8_TFLOPS, 4)}
-    roof["kernel"] = kname
+    roof["kernel"] = " + ".join(kparts)
     roof["kernel_ms"] = round(k_ms[dom], 5)
+    roof["algorithmic_bytes" if skinny else "algorithmic_flop"] = sb[dom] if skinny else 4 * M * H * I
     roof["traffic"] = None
     try:
         with open(TRAFFIC_FILE) as f:
-            tr = json.load(f).get(kname + ":" + args.workload)
-        if tr and tr.get("source_sha") == source_sha(kname):
-            roof["traffic"] = tr["hbm_bytes_per_launch"]
+            table = json.load(f)
+        parts = [table.get(k + ":" + args.workload) for k in kparts]
+        if all(t and t.get("source_sha") == source_sha(k) for t, k in zip(parts, kparts)):
+            roof["traffic"] = sum(t["hbm_bytes_per_launch"] for t in parts)
     except (OSError, ValueError):
         pass
 
@@ -185,12 +281,35 @@ def main():
                    "path": "skinny" if skinny else "tiled"},
         "tokens_per_s": round(tok_s, 1), "hbm_GBps_min_bytes": round(gbps, 1),
         "frac_hbm_peak": round(gbps / PEAK_HBM_GBPS, 4), "frac_fp8_peak": round(tflops / PEAK_FP8_TFLOPS, 4),
+        "ms_per_step_pct": {k: round(v, 5) for k, v in pct.items()},
         "stage_ms": {k: round(v, 5) for k, v in k_ms.items()}, "wall_s_timed": round(t_wall, 4),
         "roofline": roof,
     }
+    if not args.profile_only:
+        line["vs_bf16_ffn"] = error_vs_bf16(w, sets[0], out, dev)
     if not args.no_cpu_baseline and not args.profile_only:
         line["cpu_baseline"] = cpu_baseline(w, sets, out, dev)
     print(json.dumps(line), flush=True)
+
+
+def error_vs_bf16(w, s, out, dev, rows=8):
+    """Context figure: the FP8 FFN's output against an unquantized FFN (bf16
+    operands, fp64 arithmetic) on the first rows of weight set 1."""
+    import numpy as np
+    import torch
+    import oracle.ffn as O
+    import synth
+
+    import paper_2607_16339_amd as lc
+    lc.lacache_ffn_fp8(s["x"], s["norm_w"], s["wgu_q"], s["wgu_s"], s["wd_q"], s["wd_s"], out)
+    got = out[:rows].float().cpu().numpy().astype(np.float64)
+    b = synth.make_weights(w, 1)
+    xb = synth.make_x(w, layer=1, step=0)[:rows]
+    ref = O.ffn_bf16_reference(xb, b["norm_w"], b["w_gate"], b["w_up"], b["w_down"])
+    err = np.abs(got - ref)
+    return {"rows": rows, "max_abs_err": float(err.max()), "ref_max_abs": float(np.abs(ref).max()),
+            "max_err_rel_to_max": float(err.max() / np.abs(ref).max()),
+            "rms_err_rel_to_rms": float(np.sqrt((err ** 2).mean() / (ref ** 2).mean()))}
 
 
 def cpu_baseline(w, sets, out, dev):

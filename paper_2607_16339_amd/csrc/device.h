@@ -53,6 +53,26 @@ __device__ __forceinline__ uint32_t enc1_div_fast(float y, float s, float rs) {
   return enc1_e4m3(y / s);
 }
 __device__ __forceinline__ bool scale_is_fast(float s) { return s >= 0x1p-100f; }
+
+// Eight values at once, branch-free: the codes of q0 * (1 -+ 2^-20) for
+// each value (q0 = y * rs), as in enc1_div_fast. Returns true when all eight
+// pairs agree; the codes in lo/hi are then E(RN32(y / s)). Otherwise the
+// caller redoes the eight with the correctly rounded division.
+__device__ __forceinline__ bool enc8_div_fast(const float (&y)[8], float rs, uint32_t& lo, uint32_t& hi) {
+  float m[8], p[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float q0 = y[e] * rs;
+    const float d = __builtin_fabsf(q0) * 0x1p-20f;
+    m[e] = q0 - d;
+    p[e] = q0 + d;
+  }
+  lo = enc4_e4m3(m[0], m[1], m[2], m[3]);
+  hi = enc4_e4m3(m[4], m[5], m[6], m[7]);
+  const uint32_t lo2 = enc4_e4m3(p[0], p[1], p[2], p[3]);
+  const uint32_t hi2 = enc4_e4m3(p[4], p[5], p[6], p[7]);
+  return ((lo ^ lo2) | (hi ^ hi2)) == 0u;
+}
 __device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
 
 // SiLU(g) * u in fp32 with the hardware exp2 and reciprocal (a few ulp).

@@ -336,18 +336,13 @@ __global__ __launch_bounds__(256) void skinny_hquant_kernel(const float* __restr
   for (int e = 0; e < 8; ++e) m = __builtin_fmaxf(m, __builtin_fabsf(v[e]));
   m = max_xor<16>(m);
   const float s = m / kE4M3Max;
-  const bool fast = scale_is_fast(s);
-  const float rs = fast_rcp(s);
-  uint32_t w[2] = {0u, 0u};
-  if (s != 0.0f) {
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const uint32_t c = fast ? enc1_div_fast(v[e], s, rs) : enc1_e4m3(qdiv(v[e], s));
-      w[e >> 2] |= c << (8 * (e & 3));
-    }
+  uint32_t lo = 0u, hi = 0u;
+  if (s != 0.0f && !(scale_is_fast(s) && enc8_div_fast(v, fast_rcp(s), lo, hi))) {
+    lo = enc4_e4m3(qdiv(v[0], s), qdiv(v[1], s), qdiv(v[2], s), qdiv(v[3], s));
+    hi = enc4_e4m3(qdiv(v[4], s), qdiv(v[5], s), qdiv(v[6], s), qdiv(v[7], s));
   }
   if (!ok) return;
-  *reinterpret_cast<uint2*>(hq + row * I + g * 128 + part * 8) = make_uint2(w[0], w[1]);
+  *reinterpret_cast<uint2*>(hq + row * I + g * 128 + part * 8) = make_uint2(lo, hi);
   if (part == 0) hs[g * M + row] = s;
 }
 

@@ -103,8 +103,10 @@ __global__ __launch_bounds__(BM / 32 * 64) void gemm_tiled_kernel(
   const int wave = wave_uniform(t >> 6);
   const int wm = wave >> 1, wn = wave & 1;
   const int q = lane >> 4, lr = lane & 15;
-  const int64_t m0 = static_cast<int64_t>(blockIdx.x) * BM;
-  const int64_t by = blockIdx.y;  // gate/up: h-group; down: 256-column tile
+  int64_t tile_r, tile_c;
+  xcd_grouped_tile(blockIdx.x, (M + BM - 1) / BM, gridDim.x / ((M + BM - 1) / BM), tile_r, tile_c);
+  const int64_t m0 = tile_r * BM;
+  const int64_t by = tile_c;  // gate/up: h-group; down: 256-column tile
   const int64_t KB = K / 128;
   const int64_t n0 = kGateUp ? 0 : by * BNR;
 
@@ -378,8 +380,8 @@ template <bool kGateUp, int BM>
 hipError_t launch_tiled(hipStream_t st, const uint8_t* aq, const float* as, const uint8_t* bq, const float* bs,
                         uint8_t* hq, float* hs, float* h_tap, uint16_t* out, float* out_tap, int64_t M, int64_t K,
                         int64_t N, int64_t I) {
-  const unsigned ny = kGateUp ? static_cast<unsigned>(I / 128) : static_cast<unsigned>((N + BNR - 1) / BNR);
-  dim3 grid(static_cast<unsigned>((M + BM - 1) / BM), ny);
+  const int64_t ny = kGateUp ? I / 128 : (N + BNR - 1) / BNR;
+  const dim3 grid(static_cast<unsigned>(((M + BM - 1) / BM) * ny));
   hipLaunchKernelGGL((gemm_tiled_kernel<kGateUp, BM>), grid, dim3(BM / 32 * 64), 0, st, aq, as, bq, bs, hq, hs,
                      h_tap, out, out_tap, M, K, N, I);
   return hipGetLastError();

@@ -14,6 +14,28 @@ hipError_t launch_rmsnorm_quant(hipStream_t st, const uint16_t* x, const uint16_
 hipError_t launch_add_bf16(hipStream_t st, uint16_t* x, const uint16_t* y, int64_t n);
 hipError_t launch_encode_e4m3(hipStream_t st, const float* v, uint8_t* codes, int64_t n);
 
+// Tile (row r, column c) of workgroup `bid` in an R x C grid of output tiles.
+// Workgroups are handed out round-robin over the 8 XCDs, each with its own
+// L2, so XCD x runs workgroups x, x + 8, ... Each XCD gets a contiguous range
+// of tiles in grouped order (kTileGroupRows row tiles by all columns, row
+// tile fastest): the workgroups an XCD runs at the same time cover a few
+// weight tiles and a few activation tiles, which its L2 then serves to all of
+// them. A bijection of [0, R*C) for any R, C.
+constexpr int64_t kXcds = 8;
+constexpr int64_t kTileGroupRows = 8;
+__host__ __device__ inline void xcd_grouped_tile(int64_t bid, int64_t R, int64_t C, int64_t& r, int64_t& c) {
+  const int64_t T = R * C;
+  const int64_t x = bid % kXcds, slot = bid / kXcds;
+  const int64_t per = T / kXcds, rem = T % kXcds;
+  const int64_t t = (x < rem ? x * (per + 1) : rem * (per + 1) + (x - rem) * per) + slot;
+  const int64_t g = t / (kTileGroupRows * C);
+  const int64_t first = g * kTileGroupRows;
+  const int64_t rows = R - first < kTileGroupRows ? R - first : kTileGroupRows;
+  const int64_t w = t - g * kTileGroupRows * C;
+  r = first + w % rows;
+  c = w / rows;
+}
+
 // Tiled MFMA GEMMs (any M).
 hipError_t launch_gateup_tiled(hipStream_t st, const uint8_t* xq, const float* xs, const uint8_t* wq,
                                const float* ws, uint8_t* hq, float* hs, float* h_tap, int64_t M, int64_t H,

@@ -61,29 +61,42 @@ hipError_t launch_quant_weights(hipStream_t st, const uint16_t* w, uint8_t* wq, 
 }
 
 // ---------------------------------------------------------------------------
-// Fused RMSNorm + 1x128 quantization. One wavefront per row; lane l holds
-// chunks c = 64 t + l (8 bf16 each) for t < T, so a 128-wide group is the
-// 16 lanes 16g'..16g'+15 of one pass. The fp64 sum of squares follows the
-// fixed order: per-lane partials in increasing element index, then a xor
-// butterfly over offsets 32..1 (every lane ends with the same bits).
+// Fused RMSNorm + 1x128 quantization. A row belongs to 1 << wpr_log2
+// wavefronts; lane l of each holds chunks c = 64 t + l (8 bf16 each) for
+// t < T, so a 128-wide group is the 16 lanes 16g'..16g'+15 of one pass. The
+// fp64 sum of squares follows the fixed order: per-lane partials in
+// increasing element index, then a xor butterfly over offsets 32..1 (every
+// lane ends with the same bits); each wavefront of the row computes it, and
+// quantizes the passes t with t mod (1 << wpr_log2) equal to its index in the
+// row (several wavefronts per row shorten the path of a small-M call).
 // ---------------------------------------------------------------------------
 template <int T>
 __global__ __launch_bounds__(256) void rmsnorm_quant_kernel(const uint16_t* __restrict__ x,
                                                             const uint16_t* __restrict__ nw,
                                                             uint8_t* __restrict__ xq, float* __restrict__ xs,
-                                                            int64_t M, int H) {
+                                                            int64_t M, int H, int wpr_log2) {
   const int lane = threadIdx.x & 63;
-  const int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  const int wave = threadIdx.x >> 6;
+  const int part = wave & ((1 << wpr_log2) - 1);
+  const int64_t row = (static_cast<int64_t>(blockIdx.x) * (blockDim.x >> 6) + wave) >> wpr_log2;
   if (row >= M) return;  // uniform per wavefront; no workgroup barrier below
   const int nchunk = H >> 3;
   const uint4* xr = reinterpret_cast<const uint4*>(x + row * H);
   const uint4* wr = reinterpret_cast<const uint4*>(nw);
-  uint4 xv[T];
+  // every load of the row and of the norm weight is issued before any is
+  // used (clamped indices keep them unconditional), so the wavefront waits
+  // for memory once
+  uint4 xv[T], wv[T];
 #pragma unroll
   for (int t = 0; t < T; ++t) {
     const int c = t * 64 + lane;
-    xv[t] = c < nchunk ? xr[c] : make_uint4(0u, 0u, 0u, 0u);
+    const int cc = c < nchunk ? c : nchunk - 1;
+    xv[t] = xr[cc];
+    wv[t] = wr[cc];
   }
+#pragma unroll
+  for (int t = 0; t < T; ++t)
+    if (t * 64 + lane >= nchunk) xv[t] = make_uint4(0u, 0u, 0u, 0u);
   double p = 0.0;
 #pragma unroll
   for (int t = 0; t < T; ++t) {
@@ -100,11 +113,11 @@ __global__ __launch_bounds__(256) void rmsnorm_quant_kernel(const uint16_t* __re
   const float r = static_cast<float>(1.0 / __builtin_sqrt(p / static_cast<double>(H) + 1e-5));
 #pragma unroll
   for (int t = 0; t < T; ++t) {
+    if ((t & ((1 << wpr_log2) - 1)) != part) continue;  // uniform
     const int c = t * 64 + lane;
     const bool valid = c < nchunk;  // whole 16-lane groups share validity (H % 128 == 0)
-    const uint4 wv = valid ? wr[c] : make_uint4(0u, 0u, 0u, 0u);
     const uint32_t q[4] = {xv[t].x, xv[t].y, xv[t].z, xv[t].w};
-    const uint32_t g[4] = {wv.x, wv.y, wv.z, wv.w};
+    const uint32_t g[4] = {wv[t].x, wv[t].y, wv[t].z, wv[t].w};
     float y[8];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -117,7 +130,7 @@ __global__ __launch_bounds__(256) void rmsnorm_quant_kernel(const uint16_t* __re
     amax = max_xor<16>(amax);
     const float s = amax / kE4M3Max;
     uint32_t lo = 0u, hi = 0u;
-    if (s != 0.0f) {
+    if (s != 0.0f && !(scale_is_fast(s) && enc8_div_fast(y, fast_rcp(s), lo, hi))) {
       lo = enc4_e4m3(qdiv(y[0], s), qdiv(y[1], s), qdiv(y[2], s), qdiv(y[3], s));
       hi = enc4_e4m3(qdiv(y[4], s), qdiv(y[5], s), qdiv(y[6], s), qdiv(y[7], s));
     }
@@ -131,14 +144,22 @@ __global__ __launch_bounds__(256) void rmsnorm_quant_kernel(const uint16_t* __re
 hipError_t launch_rmsnorm_quant(hipStream_t st, const uint16_t* x, const uint16_t* nw, uint8_t* xq, float* xs,
                                 int64_t M, int64_t H) {
   const int T = static_cast<int>((H + 511) / 512);
-  dim3 grid(static_cast<unsigned>((M + 3) / 4)), block(256);
+  // small M: up to 4 wavefronts per row (one row per workgroup); large M: one
+  // wavefront per row, 4 rows per workgroup
+  int wl = 0;
+  if (M <= 1024) wl = T >= 4 ? 2 : (T >= 2 ? 1 : 0);
+  const int64_t waves = M << wl;
+  const int per_block = M <= 1024 ? (1 << wl) : 4;
+  dim3 grid(static_cast<unsigned>((waves + per_block - 1) / per_block)), block(64 * per_block);
   const int h = static_cast<int>(H);
-  if (T <= 1) hipLaunchKernelGGL(rmsnorm_quant_kernel<1>, grid, block, 0, st, x, nw, xq, xs, M, h);
-  else if (T <= 2) hipLaunchKernelGGL(rmsnorm_quant_kernel<2>, grid, block, 0, st, x, nw, xq, xs, M, h);
-  else if (T <= 4) hipLaunchKernelGGL(rmsnorm_quant_kernel<4>, grid, block, 0, st, x, nw, xq, xs, M, h);
-  else if (T <= 8) hipLaunchKernelGGL(rmsnorm_quant_kernel<8>, grid, block, 0, st, x, nw, xq, xs, M, h);
-  else if (T <= 16) hipLaunchKernelGGL(rmsnorm_quant_kernel<16>, grid, block, 0, st, x, nw, xq, xs, M, h);
-  else hipLaunchKernelGGL(rmsnorm_quant_kernel<32>, grid, block, 0, st, x, nw, xq, xs, M, h);
+#define NQ(T_) hipLaunchKernelGGL(rmsnorm_quant_kernel<T_>, grid, block, 0, st, x, nw, xq, xs, M, h, wl)
+  if (T <= 1) NQ(1);
+  else if (T <= 2) NQ(2);
+  else if (T <= 4) NQ(4);
+  else if (T <= 8) NQ(8);
+  else if (T <= 16) NQ(16);
+  else NQ(32);
+#undef NQ
   return hipGetLastError();
 }
 
