@@ -9,7 +9,7 @@ mixed-precision FFN computes (Sec. 3.4, Eqs. 7-8, and the fusion points named at
 the end of Sec. 3.4 and in the Fig. 2 caption), written in NumPy with fp64
 arithmetic wherever the paper does not fix a precision. It shares no code with
 the HIP path. Each function names the passage it follows; the readings taken
-where the paper is silent are listed in the design doc of the repository.
+where the paper is silent are stated in each function.
 
 Modules
 -------

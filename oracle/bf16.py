@@ -1,7 +1,7 @@
 """bfloat16 helpers for the oracle (test infrastructure only).
 
-The paper keeps every module outside the FP8 linears in its "original fp16
-settings" (Sec. 3.4); the 16-bit type of this build is bfloat16, stored as raw
+The paper keeps every module outside the FP8 linears at its original 16-bit
+precision (Sec. 3.4); the 16-bit type here is bfloat16, stored as raw
 uint16 bit patterns (the upper half of an IEEE fp32).
 """
 

@@ -8,7 +8,7 @@ gate-up linear and into the SwiGLU before the ffout linear (end of Sec. 3.4;
 Fig. 2 caption). Everything else keeps 16-bit precision (bf16 here).
 
 Arithmetic is fp64 unless a step states fp32. Readings taken where the paper
-is silent (listed again in the design doc):
+is silent:
   * FP8 = OCP e4m3fn, Q_max = 448, saturating RNE (see ``oracle.e4m3``).
   * scale_g is an fp32 value, RN32(amax / 448); codes are E(RN32(y / s)) with a
     correctly rounded fp32 division. An all-zero group (or one whose scale
