@@ -7,11 +7,17 @@ FP8 down GEMM to bf16. Inputs are seeded synthetic activations and weights
 Weights rotate over several independently drawn layers, more bytes than the
 256 MB Infinity Cache holds, so every step streams its weights from HBM.
 
+Timing: W warm-up steps, then the K steps are captured once in a HIP graph
+(as a serving loop runs its decode steps; every step is the whole call) and
+one replay of the graph is the timed region, between HIP events and device
+synchronizations; --eager times the plain host loop instead (its figures are
+reported either way).
+
 Prints one JSON line. The default workload is the 32-token decode block
 (M=32); --workload selects another. Besides the whole-step throughput the
-line carries the dominant kernel's roofline figures (timed live with HIP
-events around that kernel alone) and the CPU oracle's throughput on a bounded
-sample of the same workload.
+line carries the dominant stage's roofline figures (timed live with HIP
+events around graph-captured back-to-back calls of that stage alone) and the
+CPU oracle's throughput on a bounded sample of the same workload.
 
   python bench.py [--gpus 1] [--steps 50] [--warmup 10] [--workload block32_h4096_i12288]
 """
@@ -48,6 +54,8 @@ def parse():
     p.add_argument("--workload", default="block32_h4096_i12288")
     p.add_argument("--weight-sets", type=int, default=4)
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--eager", action="store_true",
+                   help="time the eager host loop instead of the HIP-graph replay of the K steps")
     p.add_argument("--profile-only", action="store_true",
                    help="run warmup + timed steps only (for rocprofv3), print the line without the CPU leg")
     p.add_argument("--calibrate-copy", action="store_true",
@@ -194,22 +202,58 @@ def main():
         s = sets[i % S]
         lc.lacache_ffn_fp8(s["x"], s["norm_w"], s["wgu_q"], s["wgu_s"], s["wd_q"], s["wd_s"], out)
 
+    stream = torch.cuda.current_stream()
+    # eager: one host call per step, per-step events
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
-    stream = torch.cuda.current_stream()
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    t_wall = time.perf_counter()
     ev[0].record(stream)
     for i in range(args.steps):
         step(i)
         ev[i + 1].record(stream)
     torch.cuda.synchronize()
-    t_wall = time.perf_counter() - t_wall
-    ms = ev[0].elapsed_time(ev[-1]) / args.steps
+    ms_eager = ev[0].elapsed_time(ev[-1]) / args.steps
     per_step = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)])
     pct = {"p10": float(np.percentile(per_step, 10)), "p50": float(np.percentile(per_step, 50)),
            "p90": float(np.percentile(per_step, 90))}
+
+    # graph: the K steps captured once in a HIP graph (as a serving loop runs
+    # its decode steps), every step the whole call on its own weight set
+    ms_graph = None
+    replays = []
+    if not args.eager:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for i in range(args.steps):
+                step(i)
+        for _ in range(max(1, args.warmup // args.steps)):
+            g.replay()
+        torch.cuda.synchronize()
+        got = out.clone()
+        step(args.steps - 1)
+        torch.cuda.synchronize()
+        if not torch.equal(got, out):
+            raise RuntimeError("graph replay of the FFN step differs from the eager call")
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t_wall = time.perf_counter()
+        e0.record(stream)
+        g.replay()  # the timed region: exactly K steps
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t_wall = time.perf_counter() - t_wall
+        ms_graph = e0.elapsed_time(e1) / args.steps
+        for _ in range(5):
+            e0.record(stream)
+            g.replay()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            replays.append(e0.elapsed_time(e1) / args.steps)
+        del g
+    else:
+        t_wall = float(per_step.sum()) * 1e-3
+    ms = ms_graph if ms_graph is not None else ms_eager
     if args.calibrate_copy:
         src = torch.empty(COPY_BYTES, dtype=torch.uint8, device=dev).fill_(1)
         dst = torch.empty_like(src)
@@ -224,29 +268,52 @@ def main():
     bytes_min = 3 * H * I + 4 * (3 * I // 128) * (H // 128) + 2 * H + 4 * M * H
     gbps = bytes_min / (ms * 1e-3) / 1e9
 
-    # ---- dominant kernel, timed alone: the stage calls launch the same kernels
+    # ---- each stage timed alone: the stage entry points launch the same
+    # kernels as the fused call. R back-to-back calls (rotating over the
+    # weight sets) are captured in a HIP graph, so that the host's per-call
+    # cost does not leave the GPU idle between them; the graph is replayed
+    # between HIP events on the stream it runs on.
     skinny = M <= 64
     xq = torch.empty((M, H), dtype=torch.uint8, device=dev)
     xs = torch.empty((H // 128, M), dtype=torch.float32, device=dev)
     hq = torch.empty((M, I), dtype=torch.uint8, device=dev)
     hs = torch.empty((I // 128, M), dtype=torch.float32, device=dev)
     sb = stage_bytes(M, H, I)
-    kt = {"gateup": [], "down": []}
-    reps = max(args.steps, 20)
-    for i in range(args.warmup + reps):
-        s = sets[i % S]
-        lc.lacache_rmsnorm_quant(s["x"], s["norm_w"], xq, xs)
-        a0, a1, b1 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
-        a0.record(stream)
-        lc.lacache_gateup_swiglu_quant(xq, xs, s["wgu_q"], s["wgu_s"], hq, hs)
-        a1.record(stream)
-        lc.lacache_down_proj(hq, hs, s["wd_q"], s["wd_s"], out)
-        b1.record(stream)
-        if i >= args.warmup:
-            kt["gateup"].append((a0, a1))
-            kt["down"].append((a1, b1))
-    torch.cuda.synchronize()
-    k_ms = {k: float(np.mean([a.elapsed_time(b) for a, b in v])) for k, v in kt.items()}
+    stage_fn = {
+        "norm": lambda s: lc.lacache_rmsnorm_quant(s["x"], s["norm_w"], xq, xs),
+        "gateup": lambda s: lc.lacache_gateup_swiglu_quant(xq, xs, s["wgu_q"], s["wgu_s"], hq, hs),
+        "down": lambda s: lc.lacache_down_proj(hq, hs, s["wd_q"], s["wd_s"], out),
+    }
+    reps = max(min(args.steps, 64), 8)
+    k_ms = {}
+    for name in ("norm", "gateup", "down"):
+        fn = stage_fn[name]
+        for i in range(S):  # inputs of every stage valid, workspace allocated
+            for n2 in ("norm", "gateup", "down"):
+                stage_fn[n2](sets[i])
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for i in range(reps):
+                fn(sets[i % S])
+        g.replay()
+        torch.cuda.synchronize()
+        # the replay must reproduce the eager result of its last call
+        probe = {"norm": xq, "gateup": hq, "down": out}[name]
+        got = probe.clone()
+        fn(sets[(reps - 1) % S])
+        torch.cuda.synchronize()
+        if not torch.equal(got, probe):
+            raise RuntimeError("graph replay of the %s stage differs from the eager call" % name)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        nrep = 3
+        e0.record(torch.cuda.current_stream())
+        for _ in range(nrep):
+            g.replay()
+        e1.record(torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        k_ms[name] = e0.elapsed_time(e1) / (nrep * reps)
+        del g
     dom = "gateup"
     kname = dom + ("_skinny" if skinny else "_tiled")
     # the skinny gate/up stage is the weight-streaming kernel followed by the
@@ -281,8 +348,12 @@ def main():
                    "path": "skinny" if skinny else "tiled"},
         "tokens_per_s": round(tok_s, 1), "hbm_GBps_min_bytes": round(gbps, 1),
         "frac_hbm_peak": round(gbps / PEAK_HBM_GBPS, 4), "frac_fp8_peak": round(tflops / PEAK_FP8_TFLOPS, 4),
-        "ms_per_step_pct": {k: round(v, 5) for k, v in pct.items()},
-        "stage_ms": {k: round(v, 5) for k, v in k_ms.items()}, "wall_s_timed": round(t_wall, 4),
+        "step_timing": "HIP graph replay of the K steps" if ms_graph is not None else "eager host loop",
+        "ms_per_step_eager": round(ms_eager, 5),
+        "ms_per_step_eager_pct": {k: round(v, 5) for k, v in pct.items()},
+        "ms_per_step_graph_replays": [round(v, 5) for v in replays],
+        "stage_ms": {k: round(v, 5) for k, v in k_ms.items()}, "stage_timing": "HIP graph of back-to-back stage calls",
+        "wall_s_timed": round(t_wall, 4),
         "roofline": roof,
     }
     if not args.profile_only:

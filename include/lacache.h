@@ -34,8 +34,8 @@
  *   non-NULL (except the optional *_tap outputs) and 16-byte aligned.
  *   Outputs must not overlap inputs.
  * - The caller owns every buffer it passes. The library owns only its
- *   workspace: the intermediates of lacache_ffn_fp8 and the fp32 scratch of
- *   the skinny (M <= 64) stage calls (see lacache_ffn_fp8).
+ *   workspace: the intermediates of lacache_ffn_fp8 and the fp32 h of the
+ *   skinny (M <= 64) gate/up stage call (see lacache_ffn_fp8).
  * - Results are deterministic: the same inputs give the same output bytes
  *   (no floating-point atomics).
  * - A failed HIP launch or allocation returns LACACHE_ERR_HIP or
@@ -110,9 +110,8 @@ int lacache_gateup_swiglu_quant(void* stream, const uint8_t* xq, const float* xs
  *   out     [M x H] bf16, rounded to nearest-even from fp32         (output)
  *   out_tap [M x H] fp32 or NULL: if non-NULL, also receives the fp32 value
  *           that was rounded (test hook)
- * On the skinny path the K range is split over several workgroups whose fp32
- * partial sums pass through the library workspace and are added in a fixed
- * order.
+ * On the skinny path (M <= 64) the K range is split over the four wavefronts
+ * of a workgroup, whose fp32 partial sums are added in a fixed order.
  */
 int lacache_down_proj(void* stream, const uint8_t* hq, const float* hs, const uint8_t* wd_q, const float* wd_s,
                       uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I, int group);
@@ -149,8 +148,8 @@ int lacache_encode_e4m3(void* stream, const float* v, uint8_t* codes, int64_t n)
 
 /*
  * Kernel-path policy for the GEMM stages, process-wide:
- *   0 = automatic (the skinny weight-streaming kernels for M <= 64 and
- *       H <= 8192, the tiled MFMA kernels otherwise), 1 = always skinny
+ *   0 = automatic (the skinny weight-streaming kernels for M <= 64,
+ *       H <= 8192 and I <= 16384, the tiled MFMA kernels otherwise), 1 = always skinny
  *       (other shapes return LACACHE_ERR_UNSUPPORTED), 2 = always tiled.
  * Returns the previous policy, or LACACHE_ERR_INVALID_ARG for other values.
  */

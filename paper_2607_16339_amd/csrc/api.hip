@@ -95,12 +95,8 @@ int choose_path(int64_t M, int64_t H, int64_t I, Path* p) {
   return LACACHE_OK;
 }
 
-// Scratch of the skinny kernels: one fp32 buffer that serves the gate/up h
-// and, afterwards, the down partial sums.
-size_t skinny_scratch_bytes(int64_t M, int64_t H, int64_t I) {
-  const size_t a = skinny_gateup_ws_bytes(M, I), b = skinny_down_ws_bytes(M, H, I);
-  return a > b ? a : b;
-}
+// Scratch of the skinny gate/up stage: the fp32 h.
+size_t skinny_scratch_bytes(int64_t M, int64_t I) { return skinny_gateup_ws_bytes(M, I); }
 
 // ---------------------------------------------------------------------------
 // Library-owned workspace: one grow-only device buffer per device.
@@ -139,7 +135,7 @@ int get_workspace(size_t bytes, void** out) {
 }
 
 // Workspace layout (every region 256-byte aligned):
-//   [skinny scratch: fp32 h or down partials, only when M <= kSkinnyMaxM]
+//   [skinny scratch: fp32 h (M x I), only when M <= kSkinnyMaxM]
 //   [xq: M x H][xs: H/128 x M fp32][hq: M x I][hs: I/128 x M fp32]
 struct FfnWs {
   void* skinny;  // skinny-path scratch
@@ -154,7 +150,7 @@ FfnWs ffn_layout(void* base, int64_t M, int64_t H, int64_t I) {
   char* b = static_cast<char*>(base);
   size_t off = 0;
   w.skinny = b;
-  off += M <= kSkinnyMaxM ? skinny_scratch_bytes(M, H, I) : 0;
+  off += M <= kSkinnyMaxM ? skinny_scratch_bytes(M, I) : 0;
   w.xq = reinterpret_cast<uint8_t*>(b + off);
   off += align256(static_cast<size_t>(M * H));
   w.xs = reinterpret_cast<float*>(b + off);
@@ -175,8 +171,8 @@ int run_gateup(hipStream_t st, Path path, const uint8_t* xq, const float* xs, co
 }
 
 int run_down(hipStream_t st, Path path, const uint8_t* hq, const float* hs, const uint8_t* wq, const float* ws,
-             uint16_t* out, float* tap, int64_t M, int64_t H, int64_t I, void* skinny_ws) {
-  if (path == Path::kSkinny) return hip_status(launch_down_skinny(st, hq, hs, wq, ws, out, tap, M, H, I, skinny_ws));
+             uint16_t* out, float* tap, int64_t M, int64_t H, int64_t I) {
+  if (path == Path::kSkinny) return hip_status(launch_down_skinny(st, hq, hs, wq, ws, out, tap, M, H, I));
   return hip_status(launch_down_tiled(st, hq, hs, wq, ws, out, tap, M, H, I));
 }
 
@@ -201,7 +197,7 @@ int ffn_core(hipStream_t st, const uint16_t* x, const uint16_t* norm_w, const ui
              const FfnWs& w) {
   if (launch_rmsnorm_quant(st, x, norm_w, w.xq, w.xs, M, H) != hipSuccess) return LACACHE_ERR_HIP;
   RETURN_IF(run_gateup(st, path, w.xq, w.xs, wgu_q, wgu_s, w.hq, w.hs, nullptr, M, H, I, w.skinny));
-  return run_down(st, path, w.hq, w.hs, wd_q, wd_s, out, nullptr, M, H, I, w.skinny);
+  return run_down(st, path, w.hq, w.hs, wd_q, wd_s, out, nullptr, M, H, I);
 }
 
 }  // namespace
@@ -248,7 +244,7 @@ int lacache_gateup_swiglu_quant(void* stream, const uint8_t* xq, const float* xs
     return LACACHE_ERR_INVALID_ARG;
   hipStream_t st = static_cast<hipStream_t>(stream);
   void* skinny = nullptr;
-  if (path == Path::kSkinny) RETURN_IF(get_workspace(skinny_scratch_bytes(M, H, I), &skinny));
+  if (path == Path::kSkinny) RETURN_IF(get_workspace(skinny_scratch_bytes(M, I), &skinny));
   return run_gateup(st, path, xq, xs, wgu_q, wgu_s, hq, hs, h_tap, M, H, I, skinny);
 }
 
@@ -265,10 +261,7 @@ int lacache_down_proj(void* stream, const uint8_t* hq, const float* hs, const ui
   if (!disjoint({rng(out, M * H * 2), rng(out_tap, out_tap ? M * H * 4 : 0)},
                 {rng(hq, M * I), rng(hs, (I / 128) * M * 4), rng(wd_q, H * I), rng(wd_s, (H / 128) * (I / 128) * 4)}))
     return LACACHE_ERR_INVALID_ARG;
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  void* skinny = nullptr;
-  if (path == Path::kSkinny) RETURN_IF(get_workspace(skinny_scratch_bytes(M, H, I), &skinny));
-  return run_down(st, path, hq, hs, wd_q, wd_s, out, out_tap, M, H, I, skinny);
+  return run_down(static_cast<hipStream_t>(stream), path, hq, hs, wd_q, wd_s, out, out_tap, M, H, I);
 }
 
 size_t lacache_ffn_workspace_bytes(int64_t M, int64_t H, int64_t I, int group) {

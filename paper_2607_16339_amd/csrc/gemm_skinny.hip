@@ -2,9 +2,8 @@
 // decode block's 32 tokens). At this size the FFN is bound by streaming the
 // fp8 weights from HBM once, so the kernels are built around that stream:
 //
-//   * a workgroup owns NW x NS slabs of 16 weight rows and a range of
-//     K-groups, and walks the range in blocks of two K-groups (256 bytes of
-//     each row);
+//   * a workgroup owns slabs of 16 weight rows and walks K in blocks of
+//     K-groups;
 //   * every block of weights and of the M activation rows goes global -> LDS
 //     with direct-to-LDS copies into a ring of D slots, D - 1 blocks ahead of
 //     the multiply, so D - 1 blocks per CU are always in flight;
@@ -17,14 +16,16 @@
 //   * each K-group of each 16 x 16 output tile is one 16x16x128 FP8 MFMA,
 //     added to the fp32 accumulator times RN32(x_scale * w_scale).
 //
-// gate/up: NW = 3 waves, each owning the gate rows 16p.. and the matching up
-//          rows I + 16p.. (NS = 2), all of K; SwiGLU in registers, h stored
-//          as fp32. A second kernel quantizes h per 1x128 group (a group's
-//          columns come from several workgroups, and stream order is the
-//          cheapest way to make all of them visible).
-// down:    NW = 4 waves x 16 output columns, K split over KS workgroups that
-//          store fp32 partials; a second kernel adds them in split order and
-//          rounds to bf16.
+// gate/up: 3 waves, each owning the gate rows 16p.. and the matching up rows
+//          I + 16p.., all of K, in blocks of two K-groups (256 bytes of each
+//          row) shared by the waves; SwiGLU in registers, h stored as fp32.
+//          A second kernel quantizes h per 1x128 group (a group's columns
+//          come from several workgroups, and stream order is the cheapest
+//          way to make all of them visible: device-scope fences inside the
+//          kernel cost more than the stream).
+// down:    16 output columns per workgroup, its 4 waves take a quarter of K
+//          each, one K-group per block, in private rings; the partials are
+//          added in LDS in wave order.
 #include "device.h"
 #include "launch.h"
 
@@ -36,8 +37,6 @@ namespace {
 constexpr int kRowBytes = 256;  // one block: two K-groups of a row
 constexpr int kMaxNkb = 64;     // K-groups per workgroup (scales staged in LDS)
 constexpr int kGuWaves = 3;     // gate/up: (gate, up) slab pairs per workgroup
-constexpr int kDnWaves = 4;     // down: 16-column slabs per workgroup
-constexpr int kDnCols = kDnWaves * 16;
 #ifndef LACACHE_SKINNY_ROT
 #define LACACHE_SKINNY_ROT 1
 #endif
@@ -90,10 +89,10 @@ __device__ __forceinline__ v8i ring_frag(const uint8_t* slab, int lr, int q, int
   return f;
 }
 
-template <bool kGateUp, int MT, int D>
+template <int MT>
 struct Cfg {
-  static constexpr int NW = kGateUp ? kGuWaves : kDnWaves;
-  static constexpr int NS = kGateUp ? 2 : 1;
+  static constexpr int NW = kGuWaves;
+  static constexpr int NS = 2;                           // gate and up slab
   static constexpr int RA = MT * 16;                     // activation rows in a slot (padded)
   static constexpr int kA = RA * kRowBytes;              // activation bytes per slot
   static constexpr int kW = NW * NS * 16 * kRowBytes;    // weight bytes per slot
@@ -104,12 +103,12 @@ struct Cfg {
   static constexpr int PER = AIW + WI;                   // copies per wave per block
 };
 
-template <bool kGateUp, int MT, int D>
-__global__ __launch_bounds__((kGateUp ? kGuWaves : kDnWaves) * 64) void skinny_kernel(
+template <int MT, int D>
+__global__ __launch_bounds__(kGuWaves * 64) void skinny_gateup_kernel(
     const uint8_t* __restrict__ aq, const float* __restrict__ as,  // activations [M x K], scales [K/128 x M]
-    const uint8_t* __restrict__ wq, const float* __restrict__ ws,  // weights [N x K], scales [N/128 x K/128]
-    float* __restrict__ h_tap, float* __restrict__ wsbuf, int64_t M, int64_t K, int64_t N, int64_t I, int KS) {
-  using C = Cfg<kGateUp, MT, D>;
+    const uint8_t* __restrict__ wq, const float* __restrict__ ws,  // weights [2I x K], scales [2I/128 x K/128]
+    float* __restrict__ h_tap, float* __restrict__ hbuf, int64_t M, int64_t K, int64_t I) {
+  using C = Cfg<MT>;
   constexpr int NW = C::NW, NS = C::NS, RA = C::RA;
   __shared__ __align__(16) uint8_t ring[D * C::kSlot];
   __shared__ __align__(16) float sXs[kMaxNkb * RA];
@@ -120,27 +119,12 @@ __global__ __launch_bounds__((kGateUp ? kGuWaves : kDnWaves) * 64) void skinny_k
   const int q = lane >> 4, lr = lane & 15;
   const int64_t KB = K / 128;
 
-  // ---- work of this workgroup and wavefront
-  int64_t kb0, kb1, slab_row[NS];
-  bool active;
-  int64_t pair = 0, cg = 0, sp = 0;
-  if (kGateUp) {
-    pair = static_cast<int64_t>(blockIdx.x) * NW + wave;  // h-columns 16 pair ..
-    active = pair < I / 16;
-    const int64_t p = active ? pair : 0;
-    slab_row[0] = 16 * p;           // gate rows
-    slab_row[NS - 1] = I + 16 * p;  // up rows
-    kb0 = 0;
-    kb1 = KB;
-  } else {
-    cg = blockIdx.x / KS;  // 64-column group
-    sp = blockIdx.x % KS;  // K split
-    const int64_t sub = cg * NW + wave;
-    active = 16 * sub < N;
-    slab_row[0] = 16 * (active ? sub : 0);
-    kb0 = sp * KB / KS;
-    kb1 = (sp + 1) * KB / KS;
-  }
+  // ---- work of this wavefront: h columns 16 pair .. 16 pair + 15
+  const int64_t pair = static_cast<int64_t>(blockIdx.x) * NW + wave;
+  const bool active = pair < I / 16;
+  const int64_t p0 = active ? pair : 0;
+  const int64_t slab_row[NS] = {16 * p0, I + 16 * p0};  // gate rows, up rows
+  const int64_t kb0 = 0, kb1 = KB;
   const int nkb = static_cast<int>(kb1 - kb0);
   const int NB = (nkb + 1) / 2;
   // block visited at step b (steps past the end repeat the last visited block)
@@ -232,17 +216,9 @@ __global__ __launch_bounds__((kGateUp ? kGuWaves : kDnWaves) * 64) void skinny_k
     for (int j = 0; j < WPT; ++j) {
       const int i = t + j * NW * 64;
       const int w = i / (NS * nkb), n = (i / nkb) % NS, kb = i % nkb;
-      int64_t r;
-      bool ok = i < NW * NS * nkb;
-      if (kGateUp) {
-        const int64_t p = static_cast<int64_t>(blockIdx.x) * NW + w;
-        ok = ok && p < I / 16;
-        r = n == 0 ? 16 * p : I + 16 * p;
-      } else {
-        const int64_t sub = cg * NW + w;
-        ok = ok && 16 * sub < N;
-        r = 16 * sub;
-      }
+      const int64_t p = static_cast<int64_t>(blockIdx.x) * NW + w;
+      const bool ok = i < NW * NS * nkb && p < I / 16;
+      const int64_t r = n == 0 ? 16 * p : I + 16 * p;
       wv[j] = ok ? ws[(r / 128) * KB + kb0 + kb] : 0.0f;
     }
 #pragma unroll
@@ -293,28 +269,160 @@ __global__ __launch_bounds__((kGateUp ? kGuWaves : kDnWaves) * 64) void skinny_k
   wait_vm<0>();  // drain the trailing repeat copies
 
   if (!active) return;
-  if (kGateUp) {
-    // ---- SwiGLU, h -> fp32 [M x I]
+  // ---- SwiGLU, h -> fp32 [M x I]
 #pragma unroll
-    for (int i = 0; i < MT; ++i)
+  for (int i = 0; i < MT; ++i)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int64_t row = 16 * i + 4 * q + r;
-        if (row < M) {
-          const float h = swiglu_fast(acc[i][0][r], acc[i][NS - 1][r]);
-          wsbuf[row * I + 16 * pair + lr] = h;
-          if (h_tap != nullptr) h_tap[row * I + 16 * pair + lr] = h;
-        }
+    for (int r = 0; r < 4; ++r) {
+      const int64_t row = 16 * i + 4 * q + r;
+      if (row < M) {
+        const float h = swiglu_fast(acc[i][0][r], acc[i][1][r]);
+        hbuf[row * I + 16 * pair + lr] = h;
+        if (h_tap != nullptr) h_tap[row * I + 16 * pair + lr] = h;
       }
-  } else {
-    // ---- fp32 partial of this K split -> [KS x M x N]
+    }
+}
+
+// ---------------------------------------------------------------------------
+// down, K split inside the workgroup: 16 output columns per workgroup, its 4
+// wavefronts take a quarter of K each. A wavefront streams its own K range
+// (the 16 weight rows and the M activation rows, one K-group per slot) into
+// a private LDS ring, so the streaming needs no workgroup barrier; the four
+// fp32 partials meet in LDS at the end and are added in wavefront order.
+// ---------------------------------------------------------------------------
+constexpr int kDnSplit = 4;       // wavefronts (K quarters) per workgroup
+constexpr int kDnMaxNkbW = 32;    // K-groups per wavefront (scales staged in LDS)
+
+template <int MT>
+struct DnCfg {
+  static constexpr int RA = MT * 16;        // activation rows in a slot (padded)
+  static constexpr int kA = RA * 128;       // activation bytes per slot
+  static constexpr int kSlot = kA + 16 * 128;
+  static constexpr int AI = RA / 8;         // 1 KB copies of activations per slot
+  static constexpr int PER = AI + 2;        // copies per slot (activations + 2 of weights)
+  static constexpr int D = MT == 1 ? 8 : (MT == 2 ? 5 : (MT == 3 ? 4 : 3));  // ring depth that fits the LDS
+};
+
+// MFMA operand from a slot laid out [row][128 B], physical chunk = logical
+// chunk ^ (row & 7): lane (q, lr) takes row lr, logical chunks q and 4 + q.
+__device__ __forceinline__ v8i slot_frag(const uint8_t* rows, int lr, int q) {
+  const uint8_t* row = rows + lr * 128;
+  const uint4 lo = *reinterpret_cast<const uint4*>(row + ((q ^ (lr & 7)) << 4));
+  const uint4 hi = *reinterpret_cast<const uint4*>(row + (((4 + q) ^ (lr & 7)) << 4));
+  v8i f;
+  f[0] = static_cast<int>(lo.x); f[1] = static_cast<int>(lo.y); f[2] = static_cast<int>(lo.z); f[3] = static_cast<int>(lo.w);
+  f[4] = static_cast<int>(hi.x); f[5] = static_cast<int>(hi.y); f[6] = static_cast<int>(hi.z); f[7] = static_cast<int>(hi.w);
+  return f;
+}
+
+template <int MT>
+__global__ __launch_bounds__(kDnSplit * 64) void skinny_down_kernel(
+    const uint8_t* __restrict__ aq, const float* __restrict__ as,  // h codes [M x K], scales [K/128 x M]
+    const uint8_t* __restrict__ wq, const float* __restrict__ ws,  // W_down codes [N x K], scales [N/128 x K/128]
+    uint16_t* __restrict__ out, float* __restrict__ out_tap, int64_t M, int64_t K, int64_t N) {
+  using C = DnCfg<MT>;
+  constexpr int D = C::D, RA = C::RA;
+  __shared__ __align__(16) uint8_t ring[kDnSplit][D * C::kSlot];
+  __shared__ __align__(16) float sXs[kDnSplit][kDnMaxNkbW * RA];
+  __shared__ float sWs[kDnSplit][kDnMaxNkbW];
+
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = wave_uniform(t >> 6);
+  const int q = lane >> 4, lr = lane & 15;
+  const int64_t KB = K / 128;
+  const int64_t n0 = static_cast<int64_t>(blockIdx.x) * 16;
+  const int64_t kb0 = wave * KB / kDnSplit, kb1 = (wave + 1) * KB / kDnSplit;
+  const int nkb = static_cast<int>(kb1 - kb0);  // 0 when K has fewer groups than wavefronts
+  uint8_t* my = ring[wave];
+
+  // copy plan: instruction u fills slot rows 8u..8u+7; lane l fills row
+  // 8u + l/8, physical chunk l%8, i.e. logical chunk (l%8) ^ (row & 7)
+  const int crow = lane >> 3, pch = lane & 7;
+  int64_t a_off[C::AI];
 #pragma unroll
-    for (int i = 0; i < MT; ++i)
+  for (int u = 0; u < C::AI; ++u) {
+    const int row = 8 * u + crow;
+    const int64_t gr = row < M ? row : M - 1;
+    a_off[u] = gr * K + ((pch ^ (row & 7)) << 4);
+  }
+  int64_t w_off[2];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int64_t row = 16 * i + 4 * q + r;
-        if (row < M) wsbuf[(sp * M + row) * N + slab_row[0] + lr] = acc[i][0][r];
-      }
+  for (int u = 0; u < 2; ++u) {
+    const int row = 8 * u + crow;
+    w_off[u] = (n0 + row) * K + ((pch ^ (row & 7)) << 4);
+  }
+  auto issue = [&](int b, int slot) {
+    const int64_t kg = kb0 + (b < nkb ? b : nkb - 1);  // past the end: the last K-group again
+    const uint32_t base = lds_u32(my + slot * C::kSlot);
+#pragma unroll
+    for (int u = 0; u < C::AI; ++u) dma16(aq + a_off[u] + kg * 128, wave_uniform(static_cast<int>(base) + u * 1024));
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+      dma16(wq + w_off[u] + kg * 128, wave_uniform(static_cast<int>(base) + C::kA + u * 1024));
+  };
+  if (nkb > 0) {
+#pragma unroll
+    for (int b = 0; b < D - 1; ++b) issue(b, b);
+  }
+
+  // ---- this wavefront's scales, staged in LDS (loaded after the first copies)
+  {
+    constexpr int XPT = kDnMaxNkbW * RA / 64;
+    float xv[XPT];
+#pragma unroll
+    for (int j = 0; j < XPT; ++j) {
+      const int i = lane + 64 * j, kb = i / RA, m = i % RA;
+      xv[j] = (i < nkb * RA && m < M) ? as[(kb0 + kb) * M + m] : 0.0f;
+    }
+    const float wv = lane < nkb ? ws[(n0 / 128) * KB + kb0 + lane] : 0.0f;
+#pragma unroll
+    for (int j = 0; j < XPT; ++j) {
+      const int i = lane + 64 * j;
+      if (i < nkb * RA) sXs[wave][i] = xv[j];
+    }
+    if (lane < nkb) sWs[wave][lane] = wv;
+  }
+
+  float acc[MT][4];
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) acc[i][r] = 0.0f;
+  for (int b = 0; b < nkb; ++b) {
+    wait_vm_lds<(D - 2) * C::PER>();  // K-group b has landed; slot (b-1) % D is read
+    issue(b + D - 1, (b + D - 1) % D);
+    const uint8_t* slot = my + (b % D) * C::kSlot;
+    const v8i bf = slot_frag(slot + C::kA, lr, q);
+    const float w = sWs[wave][b];
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      const v8i af = slot_frag(slot + i * 16 * 128, lr, q);
+      const float4 x4 = *reinterpret_cast<const float4*>(&sXs[wave][b * RA + 16 * i + 4 * q]);
+      const v4f zero = {0.0f, 0.0f, 0.0f, 0.0f};
+      const v4f p = mfma_fp8_16x16x128(af, bf, zero);
+      acc[i][0] = __builtin_fmaf(p[0], x4.x * w, acc[i][0]);
+      acc[i][1] = __builtin_fmaf(p[1], x4.y * w, acc[i][1]);
+      acc[i][2] = __builtin_fmaf(p[2], x4.z * w, acc[i][2]);
+      acc[i][3] = __builtin_fmaf(p[3], x4.w * w, acc[i][3]);
+    }
+  }
+  wait_vm<0>();  // the trailing repeat copies
+  __syncthreads();  // every ring is idle: reuse the space for the partials
+
+  // ---- partials [wave][RA][16] -> sum in wavefront order -> bf16
+  float* red = reinterpret_cast<float*>(&ring[0][0]);
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) red[(wave * RA + 16 * i + 4 * q + r) * 16 + lr] = acc[i][r];
+  __syncthreads();
+  for (int e = t; e < M * 16; e += kDnSplit * 64) {
+    const int row = e >> 4, col = e & 15;
+    float sum = red[row * 16 + col];
+#pragma unroll
+    for (int w = 1; w < kDnSplit; ++w) sum += red[(w * RA + row) * 16 + col];
+    out[row * N + n0 + col] = static_cast<uint16_t>(f32_to_bf16(sum));
+    if (out_tap != nullptr) out_tap[row * N + n0 + col] = sum;
   }
 }
 
@@ -346,51 +454,25 @@ __global__ __launch_bounds__(256) void skinny_hquant_kernel(const float* __restr
   if (part == 0) hs[g * M + row] = s;
 }
 
-// out = RNE_bf16(sum of the KS partials, in split order); 4 columns per thread.
-__global__ __launch_bounds__(256) void skinny_reduce_kernel(const float* __restrict__ part, uint16_t* __restrict__ out,
-                                                            float* __restrict__ out_tap, int64_t MN, int KS) {
-  const int64_t e = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 4;
-  if (e >= MN) return;
-  float4 acc = *reinterpret_cast<const float4*>(part + e);
-  for (int s = 1; s < KS; ++s) {
-    const float4 p = *reinterpret_cast<const float4*>(part + s * MN + e);
-    acc.x += p.x; acc.y += p.y; acc.z += p.z; acc.w += p.w;
-  }
-  *reinterpret_cast<uint2*>(out + e) = make_uint2(pack_bf16x2(acc.x, acc.y), pack_bf16x2(acc.z, acc.w));
-  if (out_tap != nullptr) *reinterpret_cast<float4*>(out_tap + e) = acc;
+// Ring depth per M-tile count: the deepest ring that fits the LDS.
+template <int MT>
+constexpr int gateup_ring_depth() {
+  return MT <= 2 ? 4 : 3;
 }
 
-// Ring depth per (path, M-tiles): the deepest ring that fits the LDS.
-template <bool kGateUp, int MT>
-constexpr int ring_depth() {
-  return kGateUp ? (MT <= 2 ? 4 : 3) : (MT <= 2 ? 5 : 4);
-}
-
-int down_splits(int64_t H, int64_t I) {
-  const int64_t KB = I / 128;
-  const int64_t groups = (H + kDnCols - 1) / kDnCols;
-  int64_t ks = (256 + groups - 1) / groups;           // about one workgroup per CU
-  const int64_t need = (KB + kMaxNkb - 1) / kMaxNkb;  // K-groups per split fit the LDS scales
-  if (ks < need) ks = need;
-  if (ks > KB) ks = KB;
-  return static_cast<int>(ks);
-}
-
-template <bool kGateUp, int MT>
-hipError_t launch_skinny(hipStream_t st, const uint8_t* aq, const float* as, const uint8_t* wq, const float* ws,
-                         float* h_tap, float* wsbuf, int64_t M, int64_t K, int64_t N, int64_t I, int KS,
-                         unsigned grid) {
-  constexpr int D = ring_depth<kGateUp, MT>();
-  hipLaunchKernelGGL((skinny_kernel<kGateUp, MT, D>), dim3(grid), dim3(Cfg<kGateUp, MT, D>::NW * 64), 0, st, aq,
-                     as, wq, ws, h_tap, wsbuf, M, K, N, I, KS);
+template <int MT>
+hipError_t launch_gateup(hipStream_t st, const uint8_t* aq, const float* as, const uint8_t* wq, const float* ws,
+                         float* h_tap, float* hbuf, int64_t M, int64_t K, int64_t I, unsigned grid) {
+  constexpr int D = gateup_ring_depth<MT>();
+  hipLaunchKernelGGL((skinny_gateup_kernel<MT, D>), dim3(grid), dim3(kGuWaves * 64), 0, st, aq, as, wq, ws, h_tap,
+                     hbuf, M, K, I);
   return hipGetLastError();
 }
 
 }  // namespace
 
 bool skinny_supported(int64_t M, int64_t H, int64_t I) {
-  (void)I;
-  return M >= 1 && M <= kSkinnyMaxM && H / 128 <= kMaxNkb;
+  return M >= 1 && M <= kSkinnyMaxM && H / 128 <= kMaxNkb && I / 128 <= kDnSplit * kDnMaxNkbW;
 }
 
 size_t skinny_gateup_ws_bytes(int64_t M, int64_t I) {
@@ -398,12 +480,7 @@ size_t skinny_gateup_ws_bytes(int64_t M, int64_t I) {
   return ((h + 255) / 256) * 256;
 }
 
-size_t skinny_down_ws_bytes(int64_t M, int64_t H, int64_t I) {
-  const size_t p = static_cast<size_t>(down_splits(H, I)) * static_cast<size_t>(M) * static_cast<size_t>(H) * 4;
-  return ((p + 255) / 256) * 256;
-}
-
-// ws_buf: an fp32 buffer of skinny_*_ws_bytes() (h, or the down partials).
+// ws_buf: an fp32 buffer of skinny_gateup_ws_bytes() for h.
 hipError_t launch_gateup_skinny(hipStream_t st, const uint8_t* xq, const float* xs, const uint8_t* wq,
                                 const float* ws, uint8_t* hq, float* hs, float* h_tap, int64_t M, int64_t H,
                                 int64_t I, void* ws_buf) {
@@ -411,7 +488,7 @@ hipError_t launch_gateup_skinny(hipStream_t st, const uint8_t* xq, const float* 
   const unsigned grid = static_cast<unsigned>((I / 16 + kGuWaves - 1) / kGuWaves);
   const int mt = static_cast<int>((M + 15) / 16);
   hipError_t e;
-#define GU(MT_) launch_skinny<true, MT_>(st, xq, xs, wq, ws, h_tap, hbuf, M, H, 2 * I, I, 1, grid)
+#define GU(MT_) launch_gateup<MT_>(st, xq, xs, wq, ws, h_tap, hbuf, M, H, I, grid)
   if (mt <= 1) e = GU(1);
   else if (mt == 2) e = GU(2);
   else if (mt == 3) e = GU(3);
@@ -425,22 +502,15 @@ hipError_t launch_gateup_skinny(hipStream_t st, const uint8_t* xq, const float* 
 }
 
 hipError_t launch_down_skinny(hipStream_t st, const uint8_t* hq, const float* hs, const uint8_t* wq, const float* ws,
-                              uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I, void* ws_buf) {
-  float* part = static_cast<float*>(ws_buf);
-  const int KS = down_splits(H, I);
-  const unsigned grid = static_cast<unsigned>(((H + kDnCols - 1) / kDnCols) * KS);
+                              uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I) {
+  const dim3 grid(static_cast<unsigned>(H / 16)), block(kDnSplit * 64);
   const int mt = static_cast<int>((M + 15) / 16);
-  hipError_t e;
-#define DN(MT_) launch_skinny<false, MT_>(st, hq, hs, wq, ws, nullptr, part, M, I, H, I, KS, grid)
-  if (mt <= 1) e = DN(1);
-  else if (mt == 2) e = DN(2);
-  else if (mt == 3) e = DN(3);
-  else e = DN(4);
+#define DN(MT_) hipLaunchKernelGGL(skinny_down_kernel<MT_>, grid, block, 0, st, hq, hs, wq, ws, out, out_tap, M, I, H)
+  if (mt <= 1) DN(1);
+  else if (mt == 2) DN(2);
+  else if (mt == 3) DN(3);
+  else DN(4);
 #undef DN
-  if (e != hipSuccess) return e;
-  const int64_t mn = M * H;
-  hipLaunchKernelGGL(skinny_reduce_kernel, dim3(static_cast<unsigned>((mn / 4 + 255) / 256)), dim3(256), 0, st, part,
-                     out, out_tap, mn, KS);
   return hipGetLastError();
 }
 

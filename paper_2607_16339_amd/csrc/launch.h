@@ -43,17 +43,16 @@ hipError_t launch_gateup_tiled(hipStream_t st, const uint8_t* xq, const float* x
 hipError_t launch_down_tiled(hipStream_t st, const uint8_t* hq, const float* hs, const uint8_t* wq, const float* ws,
                              uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I);
 
-// Skinny weight-streaming GEMMs (M <= kSkinnyMaxM, H <= 8192). Each needs an
-// fp32 scratch buffer of skinny_*_ws_bytes() (no initial contents); the two
-// stages may share one (they run one after the other on the stream).
+// Skinny weight-streaming GEMMs (M <= kSkinnyMaxM, H <= 8192, I <= 16384).
+// The gate/up stage needs an fp32 scratch buffer of skinny_gateup_ws_bytes()
+// (no initial contents) for h; the down stage needs none.
 constexpr int64_t kSkinnyMaxM = 64;
 bool skinny_supported(int64_t M, int64_t H, int64_t I);
 size_t skinny_gateup_ws_bytes(int64_t M, int64_t I);
-size_t skinny_down_ws_bytes(int64_t M, int64_t H, int64_t I);
 hipError_t launch_gateup_skinny(hipStream_t st, const uint8_t* xq, const float* xs, const uint8_t* wq,
                                 const float* ws, uint8_t* hq, float* hs, float* h_tap, int64_t M, int64_t H,
                                 int64_t I, void* ws_buf);
 hipError_t launch_down_skinny(hipStream_t st, const uint8_t* hq, const float* hs, const uint8_t* wq, const float* ws,
-                              uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I, void* ws_buf);
+                              uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I);
 
 }  // namespace lacache

@@ -105,8 +105,9 @@ def test_path_policy(L):
         # skinny kernels only take M <= 64
         assert L.lacache_gateup_swiglu_quant(None, p[0], p[1], p[2], p[3], p[4], p[5], None, 65, 256, 768, 128) == UNSUP
         assert L.lacache_down_proj(None, p[0], p[1], p[2], p[3], p[4], None, 65, 256, 768, 128) == UNSUP
-        # ... and H <= 8192 (the activation scales of a K range are staged in LDS)
+        # ... and H <= 8192, I <= 16384 (the scales of a K range are staged in LDS)
         assert L.lacache_gateup_swiglu_quant(None, p[0], p[1], p[2], p[3], p[4], p[5], None, 8, 8320, 768, 128) == UNSUP
+        assert L.lacache_down_proj(None, p[0], p[1], p[2], p[3], p[4], None, 8, 256, 16512, 128) == UNSUP
         assert L.lacache_set_path_policy(2) == 1
     finally:
         L.lacache_set_path_policy(prev)
@@ -116,9 +117,8 @@ def test_workspace_bytes_and_status_strings(L):
     def a256(b):
         return (b + 255) // 256 * 256
     M, H, I = 32, 4096, 12288
-    # one fp32 scratch buffer: the gate/up h (M x I) or the down partials
-    # (K splits x M x H; 4 splits of the 96 K-groups at H = 4096)
-    skinny = a256(max(M * I * 4, 4 * M * H * 4))
+    # one fp32 scratch buffer for the gate/up h (M x I)
+    skinny = a256(M * I * 4)
     want = skinny + a256(M * H) + a256(H // 128 * M * 4) + a256(M * I) + a256(I // 128 * M * 4)
     assert L.lacache_ffn_workspace_bytes(M, H, I, 128) == want
     M = 512

@@ -32,6 +32,7 @@ TINY = synth.WORKLOADS["tiny_m64_h256_i768"]
 BLOCK32 = synth.WORKLOADS["block32_h4096_i12288"]
 SAR512 = synth.WORKLOADS["sar512_h4096_i12288"]
 BATCH8K = synth.WORKLOADS["batch8x1024_h4096_i12288"]
+STACK = synth.WORKLOADS["stack31_m512_h4096_i12288"]
 
 
 def _say(msg):
@@ -270,6 +271,37 @@ def test_batch8192_sampled(big_layer):
     rows = lambda M: np.concatenate([[0, M - 1], np.sort(np.random.default_rng(4).choice(M, 6, replace=False))])
     frac, e = _full_size_case(big_layer, BATCH8K, 0, rows, 0)
     _say("batch8192: hq mismatch %.2e, error %.2e" % (frac, e))
+
+
+@pytest.mark.parametrize("step", [0, 31])
+def test_stack_layers_with_residual_adds(step):
+    """Three consecutive layers of the 31-layer stack (own weights per layer)
+    at the first and the last denoising step: each layer runs on the bf16
+    state the previous layer and residual add produced. Every layer's stages
+    are checked on sampled rows as in the single-layer cases, the fused call
+    must equal the stages, and the residual add is bit-exact."""
+    M, H, I = STACK.M, STACK.H, STACK.I
+    rows = np.sort(np.random.default_rng(6 + step).choice(M, 8, replace=False))
+    x = dev_bf16(synth.make_x(STACK, layer=1, step=step))
+    for li in (1, 2, 3):
+        _say("stack step %d layer %d" % (step, li))
+        layer = Layer(STACK, layer=li)
+        xb = host_bf16(x)
+        t = run_stages(x, layer, M, H, I)
+        wgu_q, wgu_s, wd_q, wd_s = layer.host_weights()
+        xq, xs = host(t["xq"])[rows], host(t["xs"])[:, rows]
+        hq, hs = host(t["hq"])[rows], host(t["hs"])[:, rows]
+        check_norm_exact(xb[rows], layer.bits["norm_w"], xq, xs)
+        check_requant_exact(host(t["h_tap"])[rows], hq, hs)
+        check_gateup_explained(xq, xs, wgu_q, wgu_s, I, hq, hs)
+        check_down_same_operands(hq, hs, wd_q, wd_s, host(t["out_tap"])[rows], host_bf16(t["out"])[rows])
+        y = lc.ffn_fp8(x, layer.norm_w, layer.wgu_q, layer.wgu_s, layer.wd_q, layer.wd_s)
+        torch.cuda.synchronize()
+        assert np.array_equal(host_bf16(y), host_bf16(t["out"]))
+        lc.lacache_add_bf16(x, y)
+        torch.cuda.synchronize()
+        assert np.array_equal(host_bf16(x), O.residual_add(xb, host_bf16(y)))
+        del layer, t, y
 
 
 # ---------------------------------------------------------------------------
