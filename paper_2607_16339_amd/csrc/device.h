@@ -135,6 +135,49 @@ __device__ __forceinline__ void prefetch_l2(const void* p, uint32_t& sink) {
 __device__ __forceinline__ int wave_uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
 // ---------------------------------------------------------------------------
+// Direct-to-LDS streaming with explicit waits. The copies are inline asm, so
+// the compiler neither waits for them nor moves memory accesses across them;
+// the kernels wait with explicit vmcnt counts (loads retire in issue order).
+// ---------------------------------------------------------------------------
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+// LDS byte address of a pointer into __shared__ memory.
+__device__ __forceinline__ uint32_t lds_u32(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) char*)(p)));
+}
+// 16 bytes per lane global -> LDS: lane l lands at lds + 16 l (lds wave-uniform).
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+}
+// 4 bytes per lane global -> LDS: lane l lands at lds + 4 l.
+__device__ __forceinline__ void dma4(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// s_waitcnt vmcnt(n), n < 64, other counters untouched (gfx9 encoding: vmcnt
+// in bits 3:0 and 15:14, expcnt 6:4 and lgkmcnt 11:8 at their maxima).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
+}
+// s_waitcnt vmcnt(n) lgkmcnt(0): this wave's copies up to the n most recent
+// have landed, and its LDS reads have returned.
+template <int N>
+__device__ __forceinline__ void wait_vm_lds() {
+  static_assert(N >= 0 && N < 64, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt(0x0070 | (N & 15) | ((N >> 4) << 14));
+}
+// Workgroup barrier without a memory fence (a fence would drain the copies in
+// flight); the empty asm statements keep LDS accesses from moving across it.
+__device__ __forceinline__ void bar() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// ---------------------------------------------------------------------------
 // Wavefront reductions (max is exact, so order does not matter)
 // ---------------------------------------------------------------------------
 template <int kWidth>

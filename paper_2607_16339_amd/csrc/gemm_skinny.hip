@@ -29,8 +29,6 @@
 #include "device.h"
 #include "launch.h"
 
-#pragma clang diagnostic ignored "-Winline-asm"
-
 namespace lacache {
 namespace {
 
@@ -44,38 +42,6 @@ constexpr int kGuWaves = 3;     // gate/up: (gate, up) slab pairs per workgroup
 // at any moment the chip's copies spread over all memory channels instead of
 // all reading the same K offset of rows that are a multiple of 4 KB apart.
 constexpr bool kRotateK = LACACHE_SKINNY_ROT != 0;
-
-__device__ __forceinline__ uint32_t lds_u32(const void* p) {
-  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) char*)(p)));
-}
-
-// 16 bytes per lane global -> LDS (lane l lands at lds + 16 l). Inline asm so
-// the compiler neither waits for it nor reorders memory accesses across it.
-__device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
-}
-
-// s_waitcnt vmcnt(n), n < 64, other counters untouched.
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-  static_assert(N >= 0 && N < 64, "vmcnt field");
-  __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
-}
-
-// s_waitcnt vmcnt(n) lgkmcnt(0): this wave's copies up to n-from-last have
-// landed and its LDS reads have returned (so the slot they read may be
-// overwritten once every wave has passed the next barrier).
-template <int N>
-__device__ __forceinline__ void wait_vm_lds() {
-  static_assert(N >= 0 && N < 64, "vmcnt field");
-  __builtin_amdgcn_s_waitcnt(0x0070 | (N & 15) | ((N >> 4) << 14));
-}
-
-__device__ __forceinline__ void bar() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
 
 // MFMA operand from a ring slot laid out [row][256 B] with the chunk xor:
 // lane (q, lr) takes row base + lr, logical chunks kk*8 + q and kk*8 + 4 + q.

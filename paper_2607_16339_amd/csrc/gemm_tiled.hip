@@ -3,23 +3,27 @@
 //   down:    h[M x I] . Wd[H x I]^T -> bf16
 //
 // A workgroup of BM/32 wavefronts computes a BM-row x 256-weight-row tile.
-// Each wavefront owns 64 rows x 128 weight rows (4 x 8 sub-tiles of 16x16).
-// K is walked one 128-wide group at a time:
+// Wavefront (wm, wn) owns rows 64 wm.. x weight rows 128 wn.. (4 x 8
+// sub-tiles of 16x16), i.e. one 128-row weight block. K is walked one
+// 128-wide group at a time:
 //   * the group's fp8 tiles (A: BM x 128 B, B: 256 x 128 B) and the BM
-//     activation scales go global -> LDS with direct-to-LDS loads into one of
-//     two LDS stages, issued one group ahead, so no registers hold staging
+//     activation scales go global -> LDS with direct-to-LDS copies into one
+//     of two LDS stages, issued one group ahead, so no registers hold staging
 //     data and the copy of group kb+1 overlaps the MFMAs of group kb;
 //   * every 16x16 sub-tile gets one 16x16x128 FP8 MFMA (exactly one K-group)
 //     and its fp32 result is added to the accumulator times
-//     RN32(x_scale[row] * w_scale[block]): four VALU FMAs per MFMA, which the
-//     VALU issues while the matrix core works.
+//     RN32(x_scale[row] * w_scale[block]): four VALU FMAs per MFMA, issued two
+//     MFMAs later so that they find the result finished, while the matrix
+//     core works on the next ones; the B operand of the next 16-row slab is
+//     read from LDS while the current one multiplies.
 // One workgroup barrier per K-group.
 //
-// For gate/up the tile's 256 weight rows are the 128 gate rows and the 128
-// matching up rows of one h-group, so each lane holds gate and up values of
-// the same (row, column) and a row's whole 128-wide h-group lives in one
-// workgroup: SwiGLU, the row amax and the e4m3 encoding happen in registers
-// and LDS before anything is written; h never reaches memory.
+// For gate/up the tile's 256 weight rows are the 128 gate rows (wn = 0) and
+// the 128 matching up rows (wn = 1) of one h-group: after the K loop the up
+// wavefronts hand their values to the gate wavefronts through LDS, so a row's
+// whole 128-wide h-group lives in one wavefront: SwiGLU, the row amax and the
+// e4m3 encoding happen in registers before anything is written; h never
+// reaches memory.
 #include "device.h"
 #include "launch.h"
 
@@ -28,10 +32,6 @@ namespace {
 
 constexpr int BNR = 256;           // weight rows per workgroup
 constexpr int kMaxKGroups = 512;   // K <= 65536
-#ifndef LACACHE_L2_PREFETCH
-#define LACACHE_L2_PREFETCH 0
-#endif
-constexpr bool kL2Prefetch = LACACHE_L2_PREFETCH != 0;
 
 // LDS tiles are [rows][128 bytes]; the eight 16-byte chunks of a row are
 // permuted by an xor with (row / 2) mod 8, which spreads the 16 rows of an
@@ -57,32 +57,6 @@ struct Stage {
   uint8_t b[BNR * 128];
   alignas(16) float xs[BM + 64];  // BM scales + a spare slot for redundant copies
 };
-
-// s_waitcnt with only vmcnt constrained (gfx9 encoding: vmcnt in bits 3:0,
-// expcnt 6:4 and lgkmcnt 11:8 left at their maxima). The builtin, unlike
-// inline asm, is visible to the compiler's own wait-count tracking.
-__device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
-// Workgroup barrier between pipeline steps. Each wave has already waited for
-// its own copies into the next stage, and every LDS read of the current stage
-// has been consumed, so no memory fence is needed (a fence would also wait
-// for the L2 prefetches); the empty asm statements keep the compiler from
-// moving LDS accesses across it.
-__device__ __forceinline__ void stage_barrier() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
-template <int N>
-__device__ __forceinline__ void wait_vm_prefetch() {
-  static_assert(N >= 0 && N < 16, "vmcnt field");
-  __builtin_amdgcn_s_waitcnt(0x0F70 | N);
-}
-
-// Scheduling hint: one MFMA followed by four VALU instructions.
-__device__ __forceinline__ void sched_mfma_then_4valu() {
-  __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-  __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
-}
 
 }  // namespace
 
@@ -143,28 +117,6 @@ __global__ __launch_bounds__(BM / 32 * 64) void gemm_tiled_kernel(
   const int xs_dst = wave < BM / 64 ? wave * 64 : BM;
   const float* xs_base = as + m0;
 
-  // ---- L2 prefetch two K-groups ahead. A row's K-group is one 128-byte
-  // cache line; a 1-byte load per lane pulls 64 lines into L2 while moving
-  // only 64 bytes. Wave w covers tile rows 64 (w + NW u) .. +63 of the
-  // BM + 256 rows (A rows first, then B rows).
-  constexpr int kPRows = BM + BNR;
-  constexpr int kPInst = kL2Prefetch ? (kPRows / 64 + NW - 1) / NW : 0;
-  const uint8_t* p_base[kPInst > 0 ? kPInst : 1];
-  uint32_t p_off[kPInst > 0 ? kPInst : 1];
-#pragma unroll
-  for (int u = 0; u < kPInst; ++u) {
-    int row = 64 * (wave + NW * u) + lane;
-    if (row >= kPRows) row = kPRows - 1;
-    if (row < BM) {
-      p_base[u] = a_base;
-      p_off[u] = static_cast<uint32_t>((m0 + row < M ? row : M - 1 - m0) * K);
-    } else {
-      const int br = row - BM;
-      p_base[u] = (kGateUp && br >= 128) ? b_base_hi : b_base;
-      p_off[u] = static_cast<uint32_t>(((kGateUp || n0 + br < N) ? br : N - 1 - n0) * K);
-    }
-  }
-
   // (down: the wave's 128 columns may lie past N in the last column tile)
   const bool nb_ok = kGateUp || n0 + 128 * wn < N;
   // The workgroup's weight-block scales for all K-groups, staged in LDS once:
@@ -177,7 +129,6 @@ __global__ __launch_bounds__(BM / 32 * 64) void gemm_tiled_kernel(
       sW[i < KB ? 0 : 1][i < KB ? i : i - KB] = bs[row * KB + (i < KB ? i : i - KB)];
     }
   }
-  const int wsel0 = kGateUp ? 0 : wn, wsel1 = kGateUp ? 1 : wn;
 
   float acc[4][8][4];
 #pragma unroll
@@ -187,106 +138,88 @@ __global__ __launch_bounds__(BM / 32 * 64) void gemm_tiled_kernel(
 #pragma unroll
       for (int r = 0; r < 4; ++r) acc[i][j][r] = 0.0f;
 
-  // Copies K-group kn into stage `nxt` (asynchronously) and multiplies K-group
-  // kb from stage `cur`. The two stages never alias; the restrict qualifiers
-  // let the compiler see that, so reading `cur` does not wait for the copy.
-  uint32_t sink = 0u;  // destination of the prefetch loads, live until the final vmcnt(0)
-  auto prefetch = [&](int64_t kp) {
-#pragma unroll
-    for (int u = 0; u < kPInst; ++u) prefetch_l2(p_base[u] + kp * 128 + p_off[u], sink);
-  };
-  auto step = [&](const Stage<BM>* __restrict__ cur, Stage<BM>* __restrict__ nxt, int64_t kb, int64_t kn,
-                  int64_t kp) {
+  // Copies of K-group kn into stage dst (asynchronous).
+  auto issue = [&](int64_t kn, Stage<BM>* dst) {
     const int64_t ko = kn * 128;
+    const int la = static_cast<int>(lds_u32(dst->a)), lb = static_cast<int>(lds_u32(dst->b));
 #pragma unroll
-    for (int u = 0; u < kAInst; ++u)
-      lds_dma16(a_base + ko + a_off[u], nxt->a + (wave * kAInst + u) * 1024);
+    for (int u = 0; u < kAInst; ++u) dma16(a_base + ko + a_off[u], wave_uniform(la + (wave * kAInst + u) * 1024));
 #pragma unroll
     for (int u = 0; u < kBInst; ++u) {
       const uint8_t* base = (kGateUp && (wave * kBInst + u) * 8 >= 128) ? b_base_hi : b_base;
-      lds_dma16(base + ko + b_off[u], nxt->b + (wave * kBInst + u) * 1024);
+      dma16(base + ko + b_off[u], wave_uniform(lb + (wave * kBInst + u) * 1024));
     }
-    lds_dma4(xs_base + kn * M + xs_off, nxt->xs + xs_dst);
-    prefetch(kp);
+    dma4(xs_base + kn * M + xs_off, wave_uniform(static_cast<int>(lds_u32(dst->xs)) + xs_dst * 4));
+  };
 
-    const float w0 = nb_ok ? sW[wsel0][kb] : 0.0f;
-    const float w1 = nb_ok ? sW[wsel1][kb] : 0.0f;
+  // Multiplies K-group kb from stage cur.
+  auto compute = [&](const Stage<BM>* cur, int64_t kb) {
+    // gate/up: slabs 0-3 are gate rows, 4-7 the matching up rows (two weight
+    // blocks); down: one block
+    const float w0 = nb_ok ? sW[kGateUp ? 0 : wn][kb] : 0.0f;
+    const float w1 = nb_ok ? sW[kGateUp ? 1 : wn][kb] : 0.0f;
     v8i af[4];
-    float sc[2][4][4];  // RN32(x_scale * w_scale) for the two weight blocks
+    float sc[kGateUp ? 2 : 1][4][4];  // RN32(x_scale * w_scale)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       af[i] = load_frag(cur->a, 64 * wm + 16 * i + lr, q);
       const float4 xv = *reinterpret_cast<const float4*>(cur->xs + 64 * wm + 16 * i + 4 * q);
-      const float xa[4] = {xv.x, xv.y, xv.z, xv.w};
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        sc[0][i][r] = xa[r] * w0;
-        sc[1][i][r] = xa[r] * w1;
+      sc[0][i][0] = xv.x * w0;
+      sc[0][i][1] = xv.y * w0;
+      sc[0][i][2] = xv.z * w0;
+      sc[0][i][3] = xv.w * w0;
+      if (kGateUp) {
+        sc[kGateUp ? 1 : 0][i][0] = xv.x * w1;
+        sc[kGateUp ? 1 : 0][i][1] = xv.y * w1;
+        sc[kGateUp ? 1 : 0][i][2] = xv.z * w1;
+        sc[kGateUp ? 1 : 0][i][3] = xv.w * w1;
       }
     }
-    // Software pipeline over the 32 sub-tiles: MFMA s is issued before the
-    // four scale FMAs of MFMA s-1, so the VALU works on a finished result
-    // while the matrix core runs; the B operand of slab j+1 is read from
-    // LDS while slab j multiplies.
     auto brow = [&](int j) {
       return kGateUp ? (j < 4 ? 64 * wn + 16 * j : 128 + 64 * wn + 16 * (j - 4)) : 128 * wn + 16 * j;
     };
-    v8i bcur = load_frag(cur->b, brow(0) + lr, q);
-    v4f pprev = {0.0f, 0.0f, 0.0f, 0.0f};
+    // Software pipeline over the 32 sub-tiles s = 4 j + i: MFMA s, then the
+    // scale FMAs of MFMA s - 2; the B operand of slab j + 1 is read while
+    // slab j multiplies.
+    v8i bb[2];
+    bb[0] = load_frag(cur->b, brow(0) + lr, q);
+    v4f pr[3];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const v8i bnext = j < 7 ? load_frag(cur->b, brow(j + 1) + lr, q) : bcur;
+    for (int s = 0; s < 32; ++s) {
+      const int j = s >> 2, i = s & 3;
+      if (i == 0 && j < 7) bb[(j + 1) & 1] = load_frag(cur->b, brow(j + 1) + lr, q);
+      const v4f zero = {0.0f, 0.0f, 0.0f, 0.0f};
+      pr[s % 3] = mfma_fp8_16x16x128(af[i], bb[j & 1], zero);
+      if (s >= 2) {
+        const int ps = s - 2;
+        const int blk = (kGateUp && (ps >> 2) >= 4) ? 1 : 0;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const v4f zero = {0.0f, 0.0f, 0.0f, 0.0f};
-        const v4f p = mfma_fp8_16x16x128(af[i], bcur, zero);
-        const int s = j * 4 + i;
-        if (s > 0) {
-          const int pi = (s - 1) & 3, pj = (s - 1) >> 2;
-          const int blk = (kGateUp && pj >= 4) ? 1 : 0;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) acc[pi][pj][r] = __builtin_fmaf(pprev[r], sc[blk][pi][r], acc[pi][pj][r]);
-        }
-        pprev = p;
-        sched_mfma_then_4valu();
+        for (int r = 0; r < 4; ++r)
+          acc[ps & 3][ps >> 2][r] = __builtin_fmaf(pr[ps % 3][r], sc[blk][ps & 3][r], acc[ps & 3][ps >> 2][r]);
       }
-      bcur = bnext;
+      // keep this order: the FMAs above read a result two MFMAs old, so they
+      // neither wait for the matrix core nor delay the next MFMA
+      __builtin_amdgcn_sched_barrier(0);
     }
-    {
-      const int blk = kGateUp ? 1 : 0;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) acc[3][7][r] = __builtin_fmaf(pprev[r], sc[blk][3][r], acc[3][7][r]);
-    }
-    // loads retire in issue order: this waits for the stage copy while the
-    // kPInst prefetches issued after it stay in flight across the barrier
-    wait_vm_prefetch<kPInst>();
-    stage_barrier();
+    for (int ps = 30; ps < 32; ++ps)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        acc[ps & 3][ps >> 2][r] = __builtin_fmaf(pr[ps % 3][r], sc[kGateUp ? 1 : 0][ps & 3][r], acc[ps & 3][ps >> 2][r]);
   };
 
   // ---- main loop: two LDS stages, the copy of the next group in flight. The
   // last step re-fetches its own group into the idle stage (never read).
-  {
-    const int64_t ko = 0;
-#pragma unroll
-    for (int u = 0; u < kAInst; ++u)
-      lds_dma16(a_base + ko + a_off[u], st0.a + (wave * kAInst + u) * 1024);
-#pragma unroll
-    for (int u = 0; u < kBInst; ++u) {
-      const uint8_t* base = (kGateUp && (wave * kBInst + u) * 8 >= 128) ? b_base_hi : b_base;
-      lds_dma16(base + ko + b_off[u], st0.b + (wave * kBInst + u) * 1024);
-    }
-    lds_dma4(xs_base + xs_off, st0.xs + xs_dst);
-    prefetch(KB > 1 ? 1 : 0);
-    wait_vm_prefetch<kPInst>();
-    __syncthreads();
+  issue(0, &st0);
+  wait_vm<0>();
+  __syncthreads();  // stage 0 and the weight scales are visible to every wave
+  for (int64_t kb = 0; kb < KB; ++kb) {
+    const bool odd = (kb & 1) != 0;
+    issue(kb + 1 < KB ? kb + 1 : kb, odd ? &st0 : &st1);
+    compute(odd ? &st1 : &st0, kb);
+    wait_vm_lds<0>();  // this wave's copies of the next group have landed
+    bar();             // ... everyone's; and nobody reads this group's stage any more
   }
-  auto clampk = [&](int64_t k) { return k < KB ? k : KB - 1; };
-  for (int64_t kb = 0; kb < KB; kb += 2) {
-    step(&st0, &st1, kb, clampk(kb + 1), clampk(kb + 2));
-    if (kb + 1 >= KB) break;
-    step(&st1, &st0, kb + 1, clampk(kb + 2), clampk(kb + 3));
-  }
-  wait_vm0();
 
   if (kGateUp) {
     // ---- SwiGLU: h = SiLU(g) * u, lanes hold matching gate (j) and up (j + 4) values
