@@ -60,22 +60,33 @@ struct Stage {
 
 }  // namespace
 
+// Wave layout: 8 wavefronts; a wavefront owns 64 rows x WC weight rows
+// (WC = 128 for BM = 256, 64 for BM = 128), NJ = WC / 16 column slabs. For
+// gate/up a wavefront's slabs are WC/2 gate rows and the WC/2 matching up
+// rows, so SwiGLU pairs values held by the same lane.
+constexpr int kTileWaves = 8;
+
 template <bool kGateUp, int BM>
-__global__ __launch_bounds__(BM / 32 * 64) void gemm_tiled_kernel(
+__global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
     const uint8_t* __restrict__ aq, const float* __restrict__ as,  // [M x K] codes, [K/128 x M] scales
     const uint8_t* __restrict__ bq, const float* __restrict__ bs,  // [N x K] codes, [N/128 x K/128] scales
     uint8_t* __restrict__ hq, float* __restrict__ hs, float* __restrict__ h_tap,
     uint16_t* __restrict__ out, float* __restrict__ out_tap, int64_t M, int64_t K, int64_t N, int64_t I) {
-  constexpr int NW = BM / 32;  // wavefronts: BM/64 along rows x 2 along weight rows
-  static_assert(NW == 4 || NW == 8, "BM must be 128 or 256");
-  __shared__ Stage<BM> st0, st1;
-  __shared__ float sRed[2][BM];
+  static_assert(BM == 128 || BM == 256, "BM must be 128 or 256");
+  constexpr int NW = kTileWaves;
+  constexpr int WC = BM == 256 ? 128 : 64;  // weight rows (output columns) per wavefront
+  constexpr int NCW = BNR / WC;             // wavefronts along the weight rows
+  constexpr int NJ = WC / 16;               // 16-wide column slabs per wavefront
+  // LDS ring of kStages stages: 3 for BM = 128 (3 x 49.9 KB), 2 for BM = 256
+  constexpr int kStages = BM == 128 ? 3 : 2;
+  __shared__ Stage<BM> stg[kStages];
+  __shared__ float sRed[NCW][BM];
   __shared__ float sW[2][kMaxKGroups];  // the two weight-block scale rows used by this workgroup
 
   const int t = threadIdx.x, lane = t & 63;
   // wavefront index made visibly uniform: scale loads and LDS bases go scalar
   const int wave = wave_uniform(t >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / NCW, wn = wave % NCW;
   const int q = lane >> 4, lr = lane & 15;
   int64_t tile_r, tile_c;
   xcd_grouped_tile(blockIdx.x, (M + BM - 1) / BM, gridDim.x / ((M + BM - 1) / BM), tile_r, tile_c);
@@ -117,8 +128,8 @@ __global__ __launch_bounds__(BM / 32 * 64) void gemm_tiled_kernel(
   const int xs_dst = wave < BM / 64 ? wave * 64 : BM;
   const float* xs_base = as + m0;
 
-  // (down: the wave's 128 columns may lie past N in the last column tile)
-  const bool nb_ok = kGateUp || n0 + 128 * wn < N;
+  // (down: the wave's columns may lie past N in the last column tile)
+  const bool nb_ok = kGateUp || n0 + WC * wn < N;
   // The workgroup's weight-block scales for all K-groups, staged in LDS once:
   // gate/up rows {gate block, up block}; down rows {block of wn = 0, wn = 1}.
   {
@@ -130,11 +141,11 @@ __global__ __launch_bounds__(BM / 32 * 64) void gemm_tiled_kernel(
     }
   }
 
-  float acc[4][8][4];
+  float acc[4][NJ][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 8; ++j)
+    for (int j = 0; j < NJ; ++j)
 #pragma unroll
       for (int r = 0; r < 4; ++r) acc[i][j][r] = 0.0f;
 
@@ -154,10 +165,11 @@ __global__ __launch_bounds__(BM / 32 * 64) void gemm_tiled_kernel(
 
   // Multiplies K-group kb from stage cur.
   auto compute = [&](const Stage<BM>* cur, int64_t kb) {
-    // gate/up: slabs 0-3 are gate rows, 4-7 the matching up rows (two weight
-    // blocks); down: one block
-    const float w0 = nb_ok ? sW[kGateUp ? 0 : wn][kb] : 0.0f;
-    const float w1 = nb_ok ? sW[kGateUp ? 1 : wn][kb] : 0.0f;
+    // gate/up: slabs 0..NJ/2-1 are gate rows, the rest the matching up rows
+    // (two weight blocks); down: the wave's columns lie in one block
+    const int dblk = (WC * wn) / 128;
+    const float w0 = nb_ok ? sW[kGateUp ? 0 : dblk][kb] : 0.0f;
+    const float w1 = nb_ok ? sW[kGateUp ? 1 : dblk][kb] : 0.0f;
     v8i af[4];
     float sc[kGateUp ? 2 : 1][4][4];  // RN32(x_scale * w_scale)
 #pragma unroll
@@ -176,23 +188,23 @@ __global__ __launch_bounds__(BM / 32 * 64) void gemm_tiled_kernel(
       }
     }
     auto brow = [&](int j) {
-      return kGateUp ? (j < 4 ? 64 * wn + 16 * j : 128 + 64 * wn + 16 * (j - 4)) : 128 * wn + 16 * j;
+      return kGateUp ? (j < NJ / 2 ? (WC / 2) * wn + 16 * j : 128 + (WC / 2) * wn + 16 * (j - NJ / 2)) : WC * wn + 16 * j;
     };
-    // Software pipeline over the 32 sub-tiles s = 4 j + i: MFMA s, then the
+    // Software pipeline over the 4 NJ sub-tiles s = 4 j + i: MFMA s, then the
     // scale FMAs of MFMA s - 2; the B operand of slab j + 1 is read while
     // slab j multiplies.
     v8i bb[2];
     bb[0] = load_frag(cur->b, brow(0) + lr, q);
     v4f pr[3];
 #pragma unroll
-    for (int s = 0; s < 32; ++s) {
+    for (int s = 0; s < 4 * NJ; ++s) {
       const int j = s >> 2, i = s & 3;
-      if (i == 0 && j < 7) bb[(j + 1) & 1] = load_frag(cur->b, brow(j + 1) + lr, q);
+      if (i == 0 && j < NJ - 1) bb[(j + 1) & 1] = load_frag(cur->b, brow(j + 1) + lr, q);
       const v4f zero = {0.0f, 0.0f, 0.0f, 0.0f};
       pr[s % 3] = mfma_fp8_16x16x128(af[i], bb[j & 1], zero);
       if (s >= 2) {
         const int ps = s - 2;
-        const int blk = (kGateUp && (ps >> 2) >= 4) ? 1 : 0;
+        const int blk = (kGateUp && (ps >> 2) >= NJ / 2) ? 1 : 0;
 #pragma unroll
         for (int r = 0; r < 4; ++r)
           acc[ps & 3][ps >> 2][r] = __builtin_fmaf(pr[ps % 3][r], sc[blk][ps & 3][r], acc[ps & 3][ps >> 2][r]);
@@ -202,28 +214,35 @@ __global__ __launch_bounds__(BM / 32 * 64) void gemm_tiled_kernel(
       __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
-    for (int ps = 30; ps < 32; ++ps)
+    for (int ps = 4 * NJ - 2; ps < 4 * NJ; ++ps)
 #pragma unroll
       for (int r = 0; r < 4; ++r)
         acc[ps & 3][ps >> 2][r] = __builtin_fmaf(pr[ps % 3][r], sc[kGateUp ? 1 : 0][ps & 3][r], acc[ps & 3][ps >> 2][r]);
   };
 
-  // ---- main loop: two LDS stages, the copy of the next group in flight. The
-  // last step re-fetches its own group into the idle stage (never read).
-  issue(0, &st0);
-  wait_vm<0>();
-  __syncthreads();  // stage 0 and the weight scales are visible to every wave
+  // ---- main loop over a ring of kStages stages, the copies of the next
+  // kStages - 1 groups in flight. Steps past the end re-fetch the last group
+  // into an idle stage (never read), so every step waits for the same count.
+  constexpr int kPer = kAInst + kBInst + 1;  // copies per wave per group
+  auto clampk = [&](int64_t k) { return k < KB ? k : KB - 1; };
+#pragma unroll
+  for (int s = 0; s < kStages - 1; ++s) issue(clampk(s), &stg[s]);
+  __syncthreads();  // the weight scales are visible to every wave
+  int cur = 0;      // stage of group kb
   for (int64_t kb = 0; kb < KB; ++kb) {
-    const bool odd = (kb & 1) != 0;
-    issue(kb + 1 < KB ? kb + 1 : kb, odd ? &st0 : &st1);
-    compute(odd ? &st1 : &st0, kb);
-    wait_vm_lds<0>();  // this wave's copies of the next group have landed
-    bar();             // ... everyone's; and nobody reads this group's stage any more
+    wait_vm_lds<(kStages - 2) * kPer>();  // group kb has landed (later ones may still fly)
+    bar();  // ... for every wave; and the stage of group kb - 1 is read by no one
+    const int nxt = cur == 0 ? kStages - 1 : cur - 1;  // == (kb + kStages - 1) % kStages
+    issue(clampk(kb + kStages - 1), &stg[nxt]);
+    compute(&stg[cur], kb);
+    cur = cur + 1 == kStages ? 0 : cur + 1;
   }
+  wait_vm<0>();
+  __syncthreads();  // every wave is done with the ring
 
   if (kGateUp) {
-    // ---- SwiGLU: h = SiLU(g) * u, lanes hold matching gate (j) and up (j + 4) values
-    float h[4][4][4];
+    // ---- SwiGLU: h = SiLU(g) * u, lanes hold matching gate (j) and up (j + NJ/2) values
+    float h[4][NJ / 2][4];
     float am[4][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -231,8 +250,8 @@ __global__ __launch_bounds__(BM / 32 * 64) void gemm_tiled_kernel(
       for (int r = 0; r < 4; ++r) {
         float a = 0.0f;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const float v = swiglu_fast(acc[i][j][r], acc[i][j + 4][r]);
+        for (int j = 0; j < NJ / 2; ++j) {
+          const float v = swiglu_fast(acc[i][j][r], acc[i][j + NJ / 2][r]);
           h[i][j][r] = v;
           a = __builtin_fmaxf(a, __builtin_fabsf(v));
         }
@@ -246,18 +265,21 @@ __global__ __launch_bounds__(BM / 32 * 64) void gemm_tiled_kernel(
     }
     __syncthreads();
     // ---- 1x128 quantization of each row's h-group; codes staged in LDS for coalesced stores
-    uint8_t* codes = st0.a;  // BM x 128 bytes, free after the main loop
+    uint8_t* codes = stg[0].a;  // BM x 128 bytes, free after the main loop
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int row = 64 * wm + 16 * i + 4 * q + r;
-        const float s = __builtin_fmaxf(sRed[0][row], sRed[1][row]) / kE4M3Max;
+        float amax = sRed[0][row];
+#pragma unroll
+        for (int c = 1; c < NCW; ++c) amax = __builtin_fmaxf(amax, sRed[c][row]);
+        const float s = amax / kE4M3Max;
         const bool fast = scale_is_fast(s);
         const float rs = fast_rcp(s);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int col = 64 * wn + 16 * j + lr;
+        for (int j = 0; j < NJ / 2; ++j) {
+          const int col = (WC / 2) * wn + 16 * j + lr;
           const float v = h[i][j][r];
           uint32_t c = 0u;
           if (s != 0.0f) c = fast ? enc1_div_fast(v, s, rs) : enc1_e4m3(qdiv(v, s));
@@ -272,8 +294,12 @@ __global__ __launch_bounds__(BM / 32 * 64) void gemm_tiled_kernel(
         *reinterpret_cast<uint4*>(hq + (m0 + row) * I + by * 128 + ch * 16) =
             *reinterpret_cast<const uint4*>(codes + row * 128 + ch * 16);
     }
-    for (int row = t; row < BM; row += NW * 64)
-      if (m0 + row < M) hs[by * M + m0 + row] = __builtin_fmaxf(sRed[0][row], sRed[1][row]) / kE4M3Max;
+    for (int row = t; row < BM; row += NW * 64) {
+      float amax = sRed[0][row];
+#pragma unroll
+      for (int c = 1; c < NCW; ++c) amax = __builtin_fmaxf(amax, sRed[c][row]);
+      if (m0 + row < M) hs[by * M + m0 + row] = amax / kE4M3Max;
+    }
   } else {
     // ---- bf16 output, nearest-even from the fp32 accumulator
 #pragma unroll
@@ -283,8 +309,8 @@ __global__ __launch_bounds__(BM / 32 * 64) void gemm_tiled_kernel(
         const int64_t row = m0 + 64 * wm + 16 * i + 4 * q + r;
         if (row >= M) continue;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int64_t col = n0 + 128 * wn + 16 * j + lr;
+        for (int j = 0; j < NJ; ++j) {
+          const int64_t col = n0 + WC * wn + 16 * j + lr;
           if (col < N) {
             out[row * N + col] = static_cast<uint16_t>(f32_to_bf16(acc[i][j][r]));
             if (out_tap != nullptr) out_tap[row * N + col] = acc[i][j][r];
@@ -315,7 +341,7 @@ hipError_t launch_tiled(hipStream_t st, const uint8_t* aq, const float* as, cons
                         int64_t N, int64_t I) {
   const int64_t ny = kGateUp ? I / 128 : (N + BNR - 1) / BNR;
   const dim3 grid(static_cast<unsigned>(((M + BM - 1) / BM) * ny));
-  hipLaunchKernelGGL((gemm_tiled_kernel<kGateUp, BM>), grid, dim3(BM / 32 * 64), 0, st, aq, as, bq, bs, hq, hs,
+  hipLaunchKernelGGL((gemm_tiled_kernel<kGateUp, BM>), grid, dim3(kTileWaves * 64), 0, st, aq, as, bq, bs, hq, hs,
                      h_tap, out, out_tap, M, K, N, I);
   return hipGetLastError();
 }
