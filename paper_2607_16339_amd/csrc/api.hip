@@ -95,8 +95,11 @@ int choose_path(int64_t M, int64_t H, int64_t I, Path* p) {
   return LACACHE_OK;
 }
 
-// Scratch of the skinny gate/up stage: the fp32 h.
-size_t skinny_scratch_bytes(int64_t M, int64_t I) { return skinny_gateup_ws_bytes(M, I); }
+// fp32 scratch of the GEMM stages: the skinny gate/up h (M <= 64), or the
+// split-K partials of the tiled down GEMM.
+size_t scratch_bytes(int64_t M, int64_t H, int64_t I) {
+  return M <= kSkinnyMaxM ? skinny_gateup_ws_bytes(M, I) : tiled_down_ws_bytes(M, H, I);
+}
 
 // ---------------------------------------------------------------------------
 // Library-owned workspace: one grow-only device buffer per device.
@@ -135,10 +138,11 @@ int get_workspace(size_t bytes, void** out) {
 }
 
 // Workspace layout (every region 256-byte aligned):
-//   [skinny scratch: fp32 h (M x I), only when M <= kSkinnyMaxM]
+//   [scratch: the skinny gate/up h (M <= kSkinnyMaxM) or the split-K partials
+//    of the tiled down GEMM; may be empty]
 //   [xq: M x H][xs: H/128 x M fp32][hq: M x I][hs: I/128 x M fp32]
 struct FfnWs {
-  void* skinny;  // skinny-path scratch
+  void* scratch;
   uint8_t* xq;
   float* xs;
   uint8_t* hq;
@@ -149,8 +153,8 @@ FfnWs ffn_layout(void* base, int64_t M, int64_t H, int64_t I) {
   FfnWs w{};
   char* b = static_cast<char*>(base);
   size_t off = 0;
-  w.skinny = b;
-  off += M <= kSkinnyMaxM ? skinny_scratch_bytes(M, I) : 0;
+  w.scratch = b;
+  off += align256(scratch_bytes(M, H, I));
   w.xq = reinterpret_cast<uint8_t*>(b + off);
   off += align256(static_cast<size_t>(M * H));
   w.xs = reinterpret_cast<float*>(b + off);
@@ -171,9 +175,9 @@ int run_gateup(hipStream_t st, Path path, const uint8_t* xq, const float* xs, co
 }
 
 int run_down(hipStream_t st, Path path, const uint8_t* hq, const float* hs, const uint8_t* wq, const float* ws,
-             uint16_t* out, float* tap, int64_t M, int64_t H, int64_t I) {
+             uint16_t* out, float* tap, int64_t M, int64_t H, int64_t I, void* scratch) {
   if (path == Path::kSkinny) return hip_status(launch_down_skinny(st, hq, hs, wq, ws, out, tap, M, H, I));
-  return hip_status(launch_down_tiled(st, hq, hs, wq, ws, out, tap, M, H, I));
+  return hip_status(launch_down_tiled(st, hq, hs, wq, ws, out, tap, M, H, I, scratch));
 }
 
 int validate_ffn(const uint16_t* x, const uint16_t* norm_w, const uint8_t* wgu_q, const float* wgu_s,
@@ -196,8 +200,8 @@ int ffn_core(hipStream_t st, const uint16_t* x, const uint16_t* norm_w, const ui
              const uint8_t* wd_q, const float* wd_s, uint16_t* out, int64_t M, int64_t H, int64_t I, Path path,
              const FfnWs& w) {
   if (launch_rmsnorm_quant(st, x, norm_w, w.xq, w.xs, M, H) != hipSuccess) return LACACHE_ERR_HIP;
-  RETURN_IF(run_gateup(st, path, w.xq, w.xs, wgu_q, wgu_s, w.hq, w.hs, nullptr, M, H, I, w.skinny));
-  return run_down(st, path, w.hq, w.hs, wd_q, wd_s, out, nullptr, M, H, I);
+  RETURN_IF(run_gateup(st, path, w.xq, w.xs, wgu_q, wgu_s, w.hq, w.hs, nullptr, M, H, I, w.scratch));
+  return run_down(st, path, w.hq, w.hs, wd_q, wd_s, out, nullptr, M, H, I, w.scratch);
 }
 
 }  // namespace
@@ -244,7 +248,7 @@ int lacache_gateup_swiglu_quant(void* stream, const uint8_t* xq, const float* xs
     return LACACHE_ERR_INVALID_ARG;
   hipStream_t st = static_cast<hipStream_t>(stream);
   void* skinny = nullptr;
-  if (path == Path::kSkinny) RETURN_IF(get_workspace(skinny_scratch_bytes(M, I), &skinny));
+  if (path == Path::kSkinny) RETURN_IF(get_workspace(skinny_gateup_ws_bytes(M, I), &skinny));
   return run_gateup(st, path, xq, xs, wgu_q, wgu_s, hq, hs, h_tap, M, H, I, skinny);
 }
 
@@ -261,7 +265,10 @@ int lacache_down_proj(void* stream, const uint8_t* hq, const float* hs, const ui
   if (!disjoint({rng(out, M * H * 2), rng(out_tap, out_tap ? M * H * 4 : 0)},
                 {rng(hq, M * I), rng(hs, (I / 128) * M * 4), rng(wd_q, H * I), rng(wd_s, (H / 128) * (I / 128) * 4)}))
     return LACACHE_ERR_INVALID_ARG;
-  return run_down(static_cast<hipStream_t>(stream), path, hq, hs, wd_q, wd_s, out, out_tap, M, H, I);
+  void* scratch = nullptr;
+  if (path == Path::kTiled && tiled_down_ws_bytes(M, H, I) > 0)
+    RETURN_IF(get_workspace(tiled_down_ws_bytes(M, H, I), &scratch));
+  return run_down(static_cast<hipStream_t>(stream), path, hq, hs, wd_q, wd_s, out, out_tap, M, H, I, scratch);
 }
 
 size_t lacache_ffn_workspace_bytes(int64_t M, int64_t H, int64_t I, int group) {

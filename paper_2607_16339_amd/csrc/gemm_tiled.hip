@@ -71,7 +71,8 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
     const uint8_t* __restrict__ aq, const float* __restrict__ as,  // [M x K] codes, [K/128 x M] scales
     const uint8_t* __restrict__ bq, const float* __restrict__ bs,  // [N x K] codes, [N/128 x K/128] scales
     uint8_t* __restrict__ hq, float* __restrict__ hs, float* __restrict__ h_tap,
-    uint16_t* __restrict__ out, float* __restrict__ out_tap, int64_t M, int64_t K, int64_t N, int64_t I) {
+    uint16_t* __restrict__ out, float* __restrict__ out_tap, float* __restrict__ part, int64_t M, int64_t K,
+    int64_t N, int64_t I, int KS) {
   static_assert(BM == 128 || BM == 256, "BM must be 128 or 256");
   constexpr int NW = kTileWaves;
   constexpr int WC = BM == 256 ? 128 : 64;  // weight rows (output columns) per wavefront
@@ -88,11 +89,16 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
   const int wave = wave_uniform(t >> 6);
   const int wm = wave / NCW, wn = wave % NCW;
   const int q = lane >> 4, lr = lane & 15;
+  // down with KS > 1: the KS workgroups of a tile split its K range and
+  // store fp32 partials; a second kernel adds them in split order
+  const int split = static_cast<int>(blockIdx.x % KS);
   int64_t tile_r, tile_c;
-  xcd_grouped_tile(blockIdx.x, (M + BM - 1) / BM, gridDim.x / ((M + BM - 1) / BM), tile_r, tile_c);
+  const int64_t row_tiles = (M + BM - 1) / BM;
+  xcd_grouped_tile(blockIdx.x / KS, row_tiles, (gridDim.x / KS) / row_tiles, tile_r, tile_c);
   const int64_t m0 = tile_r * BM;
   const int64_t by = tile_c;  // gate/up: h-group; down: 256-column tile
   const int64_t KB = K / 128;
+  const int64_t kb0 = split * KB / KS, kb1 = (split + 1) * KB / KS;
   const int64_t n0 = kGateUp ? 0 : by * BNR;
 
   // ---- direct-to-LDS copy plan. A wave's load instruction fills 64
@@ -224,12 +230,12 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
   // kStages - 1 groups in flight. Steps past the end re-fetch the last group
   // into an idle stage (never read), so every step waits for the same count.
   constexpr int kPer = kAInst + kBInst + 1;  // copies per wave per group
-  auto clampk = [&](int64_t k) { return k < KB ? k : KB - 1; };
+  auto clampk = [&](int64_t k) { return k < kb1 ? k : kb1 - 1; };
 #pragma unroll
-  for (int s = 0; s < kStages - 1; ++s) issue(clampk(s), &stg[s]);
+  for (int s = 0; s < kStages - 1; ++s) issue(clampk(kb0 + s), &stg[s]);
   __syncthreads();  // the weight scales are visible to every wave
   int cur = 0;      // stage of group kb
-  for (int64_t kb = 0; kb < KB; ++kb) {
+  for (int64_t kb = kb0; kb < kb1; ++kb) {
     wait_vm_lds<(kStages - 2) * kPer>();  // group kb has landed (later ones may still fly)
     bar();  // ... for every wave; and the stage of group kb - 1 is read by no one
     const int nxt = cur == 0 ? kStages - 1 : cur - 1;  // == (kb + kStages - 1) % kStages
@@ -312,8 +318,12 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
         for (int j = 0; j < NJ; ++j) {
           const int64_t col = n0 + WC * wn + 16 * j + lr;
           if (col < N) {
-            out[row * N + col] = static_cast<uint16_t>(f32_to_bf16(acc[i][j][r]));
-            if (out_tap != nullptr) out_tap[row * N + col] = acc[i][j][r];
+            if (KS > 1) {
+              part[(split * M + row) * N + col] = acc[i][j][r];
+            } else {
+              out[row * N + col] = static_cast<uint16_t>(f32_to_bf16(acc[i][j][r]));
+              if (out_tap != nullptr) out_tap[row * N + col] = acc[i][j][r];
+            }
           }
         }
       }
@@ -321,28 +331,42 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
 }
 
 template __global__ void gemm_tiled_kernel<true, 256>(const uint8_t*, const float*, const uint8_t*, const float*,
-                                                     uint8_t*, float*, float*, uint16_t*, float*, int64_t, int64_t,
-                                                     int64_t, int64_t);
+                                                     uint8_t*, float*, float*, uint16_t*, float*, float*, int64_t,
+                                                     int64_t, int64_t, int64_t, int);
 template __global__ void gemm_tiled_kernel<true, 128>(const uint8_t*, const float*, const uint8_t*, const float*,
-                                                     uint8_t*, float*, float*, uint16_t*, float*, int64_t, int64_t,
-                                                     int64_t, int64_t);
+                                                     uint8_t*, float*, float*, uint16_t*, float*, float*, int64_t,
+                                                     int64_t, int64_t, int64_t, int);
 template __global__ void gemm_tiled_kernel<false, 256>(const uint8_t*, const float*, const uint8_t*, const float*,
-                                                      uint8_t*, float*, float*, uint16_t*, float*, int64_t, int64_t,
-                                                      int64_t, int64_t);
+                                                      uint8_t*, float*, float*, uint16_t*, float*, float*, int64_t,
+                                                      int64_t, int64_t, int64_t, int);
 template __global__ void gemm_tiled_kernel<false, 128>(const uint8_t*, const float*, const uint8_t*, const float*,
-                                                      uint8_t*, float*, float*, uint16_t*, float*, int64_t, int64_t,
-                                                      int64_t, int64_t);
+                                                      uint8_t*, float*, float*, uint16_t*, float*, float*, int64_t,
+                                                      int64_t, int64_t, int64_t, int);
 
 namespace {
 
+// out = RNE_bf16(sum of the KS partials, in split order); 4 columns per thread.
+__global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restrict__ part, uint16_t* __restrict__ out,
+                                                           float* __restrict__ out_tap, int64_t MN, int KS) {
+  const int64_t e = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 4;
+  if (e >= MN) return;
+  float4 acc = *reinterpret_cast<const float4*>(part + e);
+  for (int sp = 1; sp < KS; ++sp) {
+    const float4 p = *reinterpret_cast<const float4*>(part + sp * MN + e);
+    acc.x += p.x; acc.y += p.y; acc.z += p.z; acc.w += p.w;
+  }
+  *reinterpret_cast<uint2*>(out + e) = make_uint2(pack_bf16x2(acc.x, acc.y), pack_bf16x2(acc.z, acc.w));
+  if (out_tap != nullptr) *reinterpret_cast<float4*>(out_tap + e) = acc;
+}
+
 template <bool kGateUp, int BM>
 hipError_t launch_tiled(hipStream_t st, const uint8_t* aq, const float* as, const uint8_t* bq, const float* bs,
-                        uint8_t* hq, float* hs, float* h_tap, uint16_t* out, float* out_tap, int64_t M, int64_t K,
-                        int64_t N, int64_t I) {
+                        uint8_t* hq, float* hs, float* h_tap, uint16_t* out, float* out_tap, float* part, int64_t M,
+                        int64_t K, int64_t N, int64_t I, int KS) {
   const int64_t ny = kGateUp ? I / 128 : (N + BNR - 1) / BNR;
-  const dim3 grid(static_cast<unsigned>(((M + BM - 1) / BM) * ny));
+  const dim3 grid(static_cast<unsigned>(((M + BM - 1) / BM) * ny * KS));
   hipLaunchKernelGGL((gemm_tiled_kernel<kGateUp, BM>), grid, dim3(kTileWaves * 64), 0, st, aq, as, bq, bs, hq, hs,
-                     h_tap, out, out_tap, M, K, N, I);
+                     h_tap, out, out_tap, part, M, K, N, I, KS);
   return hipGetLastError();
 }
 
@@ -350,21 +374,46 @@ hipError_t launch_tiled(hipStream_t st, const uint8_t* aq, const float* as, cons
 // one workgroup per CU, else 128.
 bool use_bm256(int64_t M, int64_t col_tiles) { return ((M + 255) / 256) * col_tiles >= 512; }
 
+// K splits of the down GEMM: enough workgroups for about one per CU, each
+// split at least 16 K-groups long.
+int down_splits(int64_t M, int64_t H, int64_t I) {
+  const int64_t tiles = ((M + 127) / 128) * ((H + BNR - 1) / BNR);
+  if (use_bm256(M, (H + BNR - 1) / BNR) || tiles >= 256) return 1;
+  int64_t ks = (256 + tiles - 1) / tiles;
+  const int64_t max_ks = (I / 128) / 16;
+  if (ks > max_ks) ks = max_ks;
+  return ks < 1 ? 1 : static_cast<int>(ks);
+}
+
 }  // namespace
+
+size_t tiled_down_ws_bytes(int64_t M, int64_t H, int64_t I) {
+  const int ks = down_splits(M, H, I);
+  return ks > 1 ? static_cast<size_t>(ks) * static_cast<size_t>(M) * static_cast<size_t>(H) * 4 : 0;
+}
 
 hipError_t launch_gateup_tiled(hipStream_t st, const uint8_t* xq, const float* xs, const uint8_t* wq,
                                const float* ws, uint8_t* hq, float* hs, float* h_tap, int64_t M, int64_t H,
                                int64_t I) {
   if (use_bm256(M, I / 128))
-    return launch_tiled<true, 256>(st, xq, xs, wq, ws, hq, hs, h_tap, nullptr, nullptr, M, H, 2 * I, I);
-  return launch_tiled<true, 128>(st, xq, xs, wq, ws, hq, hs, h_tap, nullptr, nullptr, M, H, 2 * I, I);
+    return launch_tiled<true, 256>(st, xq, xs, wq, ws, hq, hs, h_tap, nullptr, nullptr, nullptr, M, H, 2 * I, I, 1);
+  return launch_tiled<true, 128>(st, xq, xs, wq, ws, hq, hs, h_tap, nullptr, nullptr, nullptr, M, H, 2 * I, I, 1);
 }
 
 hipError_t launch_down_tiled(hipStream_t st, const uint8_t* hq, const float* hs, const uint8_t* wq, const float* ws,
-                             uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I) {
+                             uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I, void* ws_buf) {
   if (use_bm256(M, (H + BNR - 1) / BNR))
-    return launch_tiled<false, 256>(st, hq, hs, wq, ws, nullptr, nullptr, nullptr, out, out_tap, M, I, H, I);
-  return launch_tiled<false, 128>(st, hq, hs, wq, ws, nullptr, nullptr, nullptr, out, out_tap, M, I, H, I);
+    return launch_tiled<false, 256>(st, hq, hs, wq, ws, nullptr, nullptr, nullptr, out, out_tap, nullptr, M, I, H, I,
+                                    1);
+  const int ks = down_splits(M, H, I);
+  float* part = static_cast<float*>(ws_buf);
+  hipError_t e = launch_tiled<false, 128>(st, hq, hs, wq, ws, nullptr, nullptr, nullptr, out, out_tap, part, M, I, H,
+                                          I, ks);
+  if (e != hipSuccess || ks == 1) return e;
+  const int64_t mn = M * H;
+  hipLaunchKernelGGL(split_reduce_kernel, dim3(static_cast<unsigned>((mn / 4 + 255) / 256)), dim3(256), 0, st, part,
+                     out, out_tap, mn, ks);
+  return hipGetLastError();
 }
 
 }  // namespace lacache

@@ -40,8 +40,12 @@ __host__ __device__ inline void xcd_grouped_tile(int64_t bid, int64_t R, int64_t
 hipError_t launch_gateup_tiled(hipStream_t st, const uint8_t* xq, const float* xs, const uint8_t* wq,
                                const float* ws, uint8_t* hq, float* hs, float* h_tap, int64_t M, int64_t H,
                                int64_t I);
+// The down GEMM splits K over several workgroups when there are too few
+// output tiles to fill the chip; it then needs an fp32 scratch buffer of
+// tiled_down_ws_bytes() (0 when it does not split).
+size_t tiled_down_ws_bytes(int64_t M, int64_t H, int64_t I);
 hipError_t launch_down_tiled(hipStream_t st, const uint8_t* hq, const float* hs, const uint8_t* wq, const float* ws,
-                             uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I);
+                             uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I, void* ws_buf);
 
 // Skinny weight-streaming GEMMs (M <= kSkinnyMaxM, H <= 8192, I <= 16384).
 // The gate/up stage needs an fp32 scratch buffer of skinny_gateup_ws_bytes()

@@ -122,6 +122,10 @@ def test_workspace_bytes_and_status_strings(L):
     want = skinny + a256(M * H) + a256(H // 128 * M * 4) + a256(M * I) + a256(I // 128 * M * 4)
     assert L.lacache_ffn_workspace_bytes(M, H, I, 128) == want
     M = 512
+    # the tiled down GEMM splits K 4 ways at M = 512 (64 output tiles): fp32 partials
+    want = a256(4 * M * H * 4) + a256(M * H) + a256(H // 128 * M * 4) + a256(M * I) + a256(I // 128 * M * 4)
+    assert L.lacache_ffn_workspace_bytes(M, H, I, 128) == want
+    M = 8192  # enough tiles: no split, no scratch
     want = a256(M * H) + a256(H // 128 * M * 4) + a256(M * I) + a256(I // 128 * M * 4)
     assert L.lacache_ffn_workspace_bytes(M, H, I, 128) == want
     assert L.lacache_ffn_workspace_bytes(M, H, I, 64) == 0
