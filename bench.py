@@ -40,7 +40,7 @@ KERNEL_SOURCES = {
     "gateup_skinny": ["gemm_skinny.hip", "device.h"],
     "hquant_skinny": ["gemm_skinny.hip", "device.h"],
     "down_skinny": ["gemm_skinny.hip", "device.h"],
-    "reduce_skinny": ["gemm_skinny.hip", "device.h"],
+    "reduce_tiled": ["gemm_tiled.hip", "device.h"],
     "gateup_tiled": ["gemm_tiled.hip", "device.h"],
     "down_tiled": ["gemm_tiled.hip", "device.h"],
 }
@@ -90,14 +90,14 @@ COPY_BYTES = 256 << 20
 
 def kernel_key(name):
     """Short kernel key of a rocprofv3 kernel name."""
-    if "skinny_kernel<true" in name:
+    if "skinny_gateup_kernel" in name:
         return "gateup_skinny"
-    if "skinny_kernel<false" in name:
+    if "skinny_down_kernel" in name:
         return "down_skinny"
     if "skinny_hquant" in name:
         return "hquant_skinny"
-    if "skinny_reduce" in name:
-        return "reduce_skinny"
+    if "split_reduce" in name:
+        return "reduce_tiled"
     if "gemm_tiled_kernel<true" in name:
         return "gateup_tiled"
     if "gemm_tiled_kernel<false" in name:
@@ -227,7 +227,7 @@ def main():
         with torch.cuda.graph(g):
             for i in range(args.steps):
                 step(i)
-        for _ in range(max(1, args.warmup // args.steps)):
+        for _ in range(max(3, args.warmup // args.steps)):
             g.replay()
         torch.cuda.synchronize()
         got = out.clone()
