@@ -87,6 +87,18 @@ int lacache_rmsnorm_quant(void* stream, const uint16_t* x, const uint16_t* norm_
                           int64_t M, int64_t H, int group);
 
 /*
+ * The same with the residual add before the norm fused in (Sec. 3.4: the
+ * quantization is fused with the AddNorm before the gate-up linear):
+ *   resid [M x H] bf16 (input and output): resid = RNE_bf16(float(resid) +
+ *         float(y)), written in place, and the norm reads the new value
+ *   y     [M x H] bf16 (input), must not overlap resid
+ * Bit for bit the same as lacache_add_bf16(resid, y) followed by
+ * lacache_rmsnorm_quant(resid, ...), in one kernel.
+ */
+int lacache_add_rmsnorm_quant(void* stream, uint16_t* resid, const uint16_t* y, const uint16_t* norm_w,
+                              uint8_t* xq, float* xs, int64_t M, int64_t H, int group);
+
+/*
  * FP8 gate/up GEMM with per-group dequantization, fused SwiGLU and 1x128
  * re-quantization (Sec. 3.4: quantization fused with the SwiGLU before the
  * ffout linear).
@@ -129,6 +141,19 @@ int lacache_down_proj(void* stream, const uint8_t* hq, const float* hs, const ui
 int lacache_ffn_fp8(void* stream, const uint16_t* x, const uint16_t* norm_w, const uint8_t* wgu_q,
                     const float* wgu_s, const uint8_t* wd_q, const float* wd_s, uint16_t* out,
                     int64_t M, int64_t H, int64_t I, int group);
+
+/*
+ * The FFN with the AddNorm before it: resid = RNE_bf16(resid + y) in place,
+ * then out = FFN(resid) (Sec. 3.4). Bit for bit the same as
+ * lacache_add_bf16(resid, y) followed by lacache_ffn_fp8(resid, ..., out),
+ * one kernel less. In a stack of FFN layers with residual connections,
+ * layer l > 1 passes the previous layer's out as y. resid, y and out must
+ * not overlap each other or the weights. Uses the library workspace like
+ * lacache_ffn_fp8.
+ */
+int lacache_ffn_fp8_addnorm(void* stream, uint16_t* resid, const uint16_t* y, const uint16_t* norm_w,
+                            const uint8_t* wgu_q, const float* wgu_s, const uint8_t* wd_q, const float* wd_s,
+                            uint16_t* out, int64_t M, int64_t H, int64_t I, int group);
 
 /* Bytes of workspace lacache_ffn_fp8_ws needs for this shape (0 on bad arguments). */
 size_t lacache_ffn_workspace_bytes(int64_t M, int64_t H, int64_t I, int group);

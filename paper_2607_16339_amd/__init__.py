@@ -55,6 +55,15 @@ def lacache_rmsnorm_quant(x, norm_w, xq, xs, group=GROUP, stream=None):
         _ptr(xs, (torch.float32,), "xs", (H // group, M)), M, H, group), "lacache_rmsnorm_quant")
 
 
+def lacache_add_rmsnorm_quant(resid, y, norm_w, xq, xs, group=GROUP, stream=None):
+    """resid [M, H] bf16 += y (in place, nearest-even), then the norm + quantization of resid."""
+    M, H = resid.shape
+    check(lib().lacache_add_rmsnorm_quant(
+        _stream(stream, resid), _ptr(resid, _BF16, "resid"), _ptr(y, _BF16, "y", (M, H)),
+        _ptr(norm_w, _BF16, "norm_w", (H,)), _ptr(xq, _U8, "xq", (M, H)),
+        _ptr(xs, (torch.float32,), "xs", (H // group, M)), M, H, group), "lacache_add_rmsnorm_quant")
+
+
 def lacache_gateup_swiglu_quant(xq, xs, wgu_q, wgu_s, hq, hs, h_tap=None, group=GROUP, stream=None):
     """xq [M, H], wgu_q [2I, H] -> hq [M, I] e4m3, hs [I/128, M] fp32 (h_tap [M, I] fp32 optional)."""
     M, H = xq.shape
@@ -91,6 +100,13 @@ def lacache_ffn_fp8(x, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, group=GROUP, strea
     """The whole FP8 FFN of one layer: x [M, H] bf16 -> out [M, H] bf16."""
     check(lib().lacache_ffn_fp8(_stream(stream, x), *_ffn_args(x, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, group)),
           "lacache_ffn_fp8")
+
+
+def lacache_ffn_fp8_addnorm(resid, y, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, group=GROUP, stream=None):
+    """resid += y (in place), then out = the FP8 FFN of resid."""
+    args = _ffn_args(resid, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, group)
+    check(lib().lacache_ffn_fp8_addnorm(_stream(stream, resid), args[0], _ptr(y, _BF16, "y", tuple(resid.shape)),
+                                        *args[1:]), "lacache_ffn_fp8_addnorm")
 
 
 def lacache_ffn_workspace_bytes(M, H, I, group=GROUP):

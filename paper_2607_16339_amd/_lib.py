@@ -22,6 +22,8 @@ _P, _I64, _I = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
 SIGNATURES = {
     "lacache_quant_weights": (_I, [_P, _P, _P, _P, _I64, _I64, _I]),
     "lacache_rmsnorm_quant": (_I, [_P, _P, _P, _P, _P, _I64, _I64, _I]),
+    "lacache_add_rmsnorm_quant": (_I, [_P, _P, _P, _P, _P, _P, _I64, _I64, _I]),
+    "lacache_ffn_fp8_addnorm": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I]),
     "lacache_gateup_swiglu_quant": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I]),
     "lacache_down_proj": (_I, [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I]),
     "lacache_ffn_fp8": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I]),

@@ -196,10 +196,12 @@ int validate_ffn(const uint16_t* x, const uint16_t* norm_w, const uint8_t* wgu_q
   return LACACHE_OK;
 }
 
-int ffn_core(hipStream_t st, const uint16_t* x, const uint16_t* norm_w, const uint8_t* wgu_q, const float* wgu_s,
-             const uint8_t* wd_q, const float* wd_s, uint16_t* out, int64_t M, int64_t H, int64_t I, Path path,
-             const FfnWs& w) {
-  if (launch_rmsnorm_quant(st, x, norm_w, w.xq, w.xs, M, H) != hipSuccess) return LACACHE_ERR_HIP;
+// y non-null: x = RNE_bf16(x + y) in place first (x is then written).
+int ffn_core(hipStream_t st, const uint16_t* x, const uint16_t* y, const uint16_t* norm_w, const uint8_t* wgu_q,
+             const float* wgu_s, const uint8_t* wd_q, const float* wd_s, uint16_t* out, int64_t M, int64_t H,
+             int64_t I, Path path, const FfnWs& w) {
+  if (launch_rmsnorm_quant(st, const_cast<uint16_t*>(x), norm_w, w.xq, w.xs, M, H, y) != hipSuccess)
+    return LACACHE_ERR_HIP;
   RETURN_IF(run_gateup(st, path, w.xq, w.xs, wgu_q, wgu_s, w.hq, w.hs, nullptr, M, H, I, w.scratch));
   return run_down(st, path, w.hq, w.hs, wd_q, wd_s, out, nullptr, M, H, I, w.scratch);
 }
@@ -228,7 +230,24 @@ int lacache_rmsnorm_quant(void* stream, const uint16_t* x, const uint16_t* norm_
   if (!ptrs_ok({x, norm_w, xq, xs})) return LACACHE_ERR_INVALID_ARG;
   if (!disjoint({rng(xq, M * H), rng(xs, (H / 128) * M * 4)}, {rng(x, M * H * 2), rng(norm_w, H * 2)}))
     return LACACHE_ERR_INVALID_ARG;
-  return hip_status(launch_rmsnorm_quant(static_cast<hipStream_t>(stream), x, norm_w, xq, xs, M, H));
+  // (x is only read: no y)
+  return hip_status(launch_rmsnorm_quant(static_cast<hipStream_t>(stream), const_cast<uint16_t*>(x), norm_w, xq, xs,
+                                         M, H));
+}
+
+int lacache_add_rmsnorm_quant(void* stream, uint16_t* resid, const uint16_t* y, const uint16_t* norm_w, uint8_t* xq,
+                              float* xs, int64_t M, int64_t H, int group) {
+  RETURN_IF(check_group(group));
+  RETURN_IF(check_m(M));
+  RETURN_IF(check_dim(H, kMaxH));
+  if (M == 0) return LACACHE_OK;
+  if (!ptrs_ok({resid, y, norm_w, xq, xs})) return LACACHE_ERR_INVALID_ARG;
+  const size_t mh = static_cast<size_t>(M * H);
+  if (!disjoint({rng(resid, mh * 2), rng(xq, mh), rng(xs, (H / 128) * M * 4)},
+                {rng(y, mh * 2), rng(norm_w, H * 2)}) ||
+      !disjoint({rng(resid, mh * 2)}, {rng(xq, mh), rng(xs, (H / 128) * M * 4)}))
+    return LACACHE_ERR_INVALID_ARG;
+  return hip_status(launch_rmsnorm_quant(static_cast<hipStream_t>(stream), resid, norm_w, xq, xs, M, H, y));
 }
 
 int lacache_gateup_swiglu_quant(void* stream, const uint8_t* xq, const float* xs, const uint8_t* wgu_q,
@@ -288,7 +307,26 @@ int lacache_ffn_fp8(void* stream, const uint16_t* x, const uint16_t* norm_w, con
   hipStream_t st = static_cast<hipStream_t>(stream);
   void* base = nullptr;
   RETURN_IF(get_workspace(ffn_layout(nullptr, M, H, I).total, &base));
-  return ffn_core(st, x, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, M, H, I, path, ffn_layout(base, M, H, I));
+  return ffn_core(st, x, nullptr, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, M, H, I, path, ffn_layout(base, M, H, I));
+}
+
+int lacache_ffn_fp8_addnorm(void* stream, uint16_t* resid, const uint16_t* y, const uint16_t* norm_w,
+                            const uint8_t* wgu_q, const float* wgu_s, const uint8_t* wd_q, const float* wd_s,
+                            uint16_t* out, int64_t M, int64_t H, int64_t I, int group) {
+  RETURN_IF(validate_ffn(resid, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, M, H, I, group));
+  if (M == 0) return LACACHE_OK;
+  const size_t mh = static_cast<size_t>(M * H);
+  if (!ptrs_ok({y}) || !disjoint({rng(resid, mh * 2), rng(out, mh * 2)},
+                                 {rng(y, mh * 2), rng(norm_w, H * 2), rng(wgu_q, 2 * I * H),
+                                  rng(wgu_s, (2 * I / 128) * (H / 128) * 4), rng(wd_q, H * I),
+                                  rng(wd_s, (H / 128) * (I / 128) * 4)}))
+    return LACACHE_ERR_INVALID_ARG;
+  Path path;
+  RETURN_IF(choose_path(M, H, I, &path));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  void* base = nullptr;
+  RETURN_IF(get_workspace(ffn_layout(nullptr, M, H, I).total, &base));
+  return ffn_core(st, resid, y, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, M, H, I, path, ffn_layout(base, M, H, I));
 }
 
 int lacache_ffn_fp8_ws(void* stream, const uint16_t* x, const uint16_t* norm_w, const uint8_t* wgu_q,
@@ -306,7 +344,8 @@ int lacache_ffn_fp8_ws(void* stream, const uint16_t* x, const uint16_t* norm_w, 
                 {rng(x, mh * 2), rng(out, mh * 2), rng(norm_w, H * 2), rng(wgu_q, 2 * I * H),
                  rng(wgu_s, (2 * I / 128) * (H / 128) * 4), rng(wd_q, H * I), rng(wd_s, (H / 128) * (I / 128) * 4)}))
     return LACACHE_ERR_INVALID_ARG;
-  return ffn_core(static_cast<hipStream_t>(stream), x, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, M, H, I, path, lay);
+  return ffn_core(static_cast<hipStream_t>(stream), x, nullptr, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, M, H, I, path,
+                  lay);
 }
 
 int lacache_add_bf16(void* stream, uint16_t* x_inout, const uint16_t* y, int64_t n) {

@@ -9,8 +9,9 @@
 namespace lacache {
 
 hipError_t launch_quant_weights(hipStream_t st, const uint16_t* w, uint8_t* wq, float* ws, int64_t N, int64_t K);
-hipError_t launch_rmsnorm_quant(hipStream_t st, const uint16_t* x, const uint16_t* nw, uint8_t* xq, float* xs,
-                                int64_t M, int64_t H);
+// With y non-null: x = RNE_bf16(x + y) in place first (the fused AddNorm).
+hipError_t launch_rmsnorm_quant(hipStream_t st, uint16_t* x, const uint16_t* nw, uint8_t* xq, float* xs, int64_t M,
+                                int64_t H, const uint16_t* y = nullptr);
 hipError_t launch_add_bf16(hipStream_t st, uint16_t* x, const uint16_t* y, int64_t n);
 hipError_t launch_encode_e4m3(hipStream_t st, const float* v, uint8_t* codes, int64_t n);
 

@@ -69,9 +69,12 @@ hipError_t launch_quant_weights(hipStream_t st, const uint16_t* w, uint8_t* wq, 
 // lane ends with the same bits); each wavefront of the row computes it, and
 // quantizes the passes t with t mod (1 << wpr_log2) equal to its index in the
 // row (several wavefronts per row shorten the path of a small-M call).
+// With y (the fused AddNorm), the row is first x = RNE_bf16(float(x) +
+// float(y)), written back in place; a row then has one wavefront, which reads
+// all of it before writing any of it.
 // ---------------------------------------------------------------------------
 template <int T>
-__global__ __launch_bounds__(256) void rmsnorm_quant_kernel(const uint16_t* __restrict__ x,
+__global__ __launch_bounds__(256) void rmsnorm_quant_kernel(uint16_t* x, const uint16_t* __restrict__ y,
                                                             const uint16_t* __restrict__ nw,
                                                             uint8_t* __restrict__ xq, float* __restrict__ xs,
                                                             int64_t M, int H, int wpr_log2) {
@@ -81,18 +84,30 @@ __global__ __launch_bounds__(256) void rmsnorm_quant_kernel(const uint16_t* __re
   const int64_t row = (static_cast<int64_t>(blockIdx.x) * (blockDim.x >> 6) + wave) >> wpr_log2;
   if (row >= M) return;  // uniform per wavefront; no workgroup barrier below
   const int nchunk = H >> 3;
-  const uint4* xr = reinterpret_cast<const uint4*>(x + row * H);
+  const uint4* xr = reinterpret_cast<const uint4*>(x + row * H);  // (read before any write of the row)
   const uint4* wr = reinterpret_cast<const uint4*>(nw);
   // every load of the row and of the norm weight is issued before any is
   // used (clamped indices keep them unconditional), so the wavefront waits
   // for memory once
-  uint4 xv[T], wv[T];
+  uint4 xv[T], wv[T], yv[T];
 #pragma unroll
   for (int t = 0; t < T; ++t) {
     const int c = t * 64 + lane;
     const int cc = c < nchunk ? c : nchunk - 1;
     xv[t] = xr[cc];
     wv[t] = wr[cc];
+    if (y != nullptr) yv[t] = reinterpret_cast<const uint4*>(y + row * H)[cc];
+  }
+  if (y != nullptr) {  // the residual add, written back in place
+    uint4* xw = reinterpret_cast<uint4*>(x + row * H);
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      uint32_t* a = reinterpret_cast<uint32_t*>(&xv[t]);
+      const uint32_t* b = reinterpret_cast<const uint32_t*>(&yv[t]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) a[e] = pack_bf16x2(bf16lo(a[e]) + bf16lo(b[e]), bf16hi(a[e]) + bf16hi(b[e]));
+      if (t * 64 + lane < nchunk) xw[t * 64 + lane] = xv[t];
+    }
   }
 #pragma unroll
   for (int t = 0; t < T; ++t)
@@ -141,18 +156,18 @@ __global__ __launch_bounds__(256) void rmsnorm_quant_kernel(const uint16_t* __re
   }
 }
 
-hipError_t launch_rmsnorm_quant(hipStream_t st, const uint16_t* x, const uint16_t* nw, uint8_t* xq, float* xs,
-                                int64_t M, int64_t H) {
+hipError_t launch_rmsnorm_quant(hipStream_t st, uint16_t* x, const uint16_t* nw, uint8_t* xq, float* xs, int64_t M,
+                                int64_t H, const uint16_t* y) {
   const int T = static_cast<int>((H + 511) / 512);
-  // small M: up to 4 wavefronts per row (one row per workgroup); large M: one
-  // wavefront per row, 4 rows per workgroup
+  // small M: up to 4 wavefronts per row (one row per workgroup); large M, or
+  // the in-place residual add: one wavefront per row, 4 rows per workgroup
   int wl = 0;
-  if (M <= 1024) wl = T >= 4 ? 2 : (T >= 2 ? 1 : 0);
+  if (M <= 1024 && y == nullptr) wl = T >= 4 ? 2 : (T >= 2 ? 1 : 0);
   const int64_t waves = M << wl;
-  const int per_block = M <= 1024 ? (1 << wl) : 4;
+  const int per_block = wl > 0 ? (1 << wl) : 4;
   dim3 grid(static_cast<unsigned>((waves + per_block - 1) / per_block)), block(64 * per_block);
   const int h = static_cast<int>(H);
-#define NQ(T_) hipLaunchKernelGGL(rmsnorm_quant_kernel<T_>, grid, block, 0, st, x, nw, xq, xs, M, h, wl)
+#define NQ(T_) hipLaunchKernelGGL(rmsnorm_quant_kernel<T_>, grid, block, 0, st, x, y, nw, xq, xs, M, h, wl)
   if (T <= 1) NQ(1);
   else if (T <= 2) NQ(2);
   else if (T <= 4) NQ(4);

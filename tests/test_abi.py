@@ -96,6 +96,26 @@ def test_stage_validation(L):
     assert L.lacache_encode_e4m3(None, p[0], None, 4) == INVALID
 
 
+def test_addnorm_validation(L):
+    f = Fake()
+    p = [f() for _ in range(10)]
+    # stage: resid += y, then norm + quant
+    assert L.lacache_add_rmsnorm_quant(None, p[0], p[0], p[2], p[3], p[4], 4, 256, 128) == INVALID  # y is resid
+    assert L.lacache_add_rmsnorm_quant(None, p[0], None, p[2], p[3], p[4], 4, 256, 128) == INVALID
+    assert L.lacache_add_rmsnorm_quant(None, p[0], p[1], p[2], p[0] + 512, p[4], 4, 256, 128) == INVALID  # xq in resid
+    assert L.lacache_add_rmsnorm_quant(None, p[0], p[1], p[2], p[3], p[4], 0, 256, 128) == OK
+    assert L.lacache_add_rmsnorm_quant(None, p[0], p[1], p[2], p[3], p[4], 4, 256, 64) == UNSUP
+
+    def fused(resid, y, out, M=32, group=128):
+        return L.lacache_ffn_fp8_addnorm(None, resid, y, p[2], p[3], p[4], p[5], p[6], out, M, 4096, 12288, group)
+    assert fused(p[0], p[1], p[7], group=64) == UNSUP
+    assert fused(p[0], p[0], p[7]) == INVALID         # y is resid
+    assert fused(p[0], p[1], p[1]) == INVALID         # out is y
+    assert fused(p[0], p[1], p[0] + 1024) == INVALID  # out overlaps resid
+    assert fused(p[0], None, p[7]) == INVALID
+    assert fused(p[0], p[1], p[7], M=0) == OK
+
+
 def test_path_policy(L):
     assert L.lacache_set_path_policy(7) == INVALID
     prev = L.lacache_set_path_policy(1)

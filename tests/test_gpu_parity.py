@@ -341,6 +341,37 @@ def test_skinny_and_tiled_paths_agree(big_layer):
     assert d.max().item() < 2e-2, d.max().item()
 
 
+@pytest.mark.parametrize("M", [1, 32, 200, 512])
+def test_addnorm_fused_equals_add_then_ffn(big_layer, M):
+    """The AddNorm entry points: resid = RNE(resid + y) in place, the norm of
+    the new resid bit-exact against the oracle, and the fused FFN call equal,
+    bit for bit, to the residual add followed by the plain FFN call."""
+    _say("addnorm M=%d" % M)
+    H, I = 4096, 12288
+    w = synth.Workload(92, "addnorm", M, H, I, act="outlier", outlier_ratio=0.01)
+    xb = synth.make_x(w, layer=1)
+    yb = synth.make_x(w, layer=2, step=1)
+    y = dev_bf16(yb)
+    want = O.residual_add(xb, yb)
+    r1 = dev_bf16(xb)
+    xq = torch.full((M, H), 0xFF, dtype=torch.uint8, device=DEV)
+    xs = torch.full((H // 128, M), float("nan"), dtype=torch.float32, device=DEV)
+    lc.lacache_add_rmsnorm_quant(r1, y, big_layer.norm_w, xq, xs)
+    torch.cuda.synchronize()
+    assert np.array_equal(host_bf16(r1), want)
+    check_norm_exact(want, big_layer.bits["norm_w"], host(xq), host(xs))
+    r2 = dev_bf16(xb)
+    out2 = torch.empty((M, H), dtype=torch.bfloat16, device=DEV)
+    lc.lacache_ffn_fp8_addnorm(r2, y, big_layer.norm_w, big_layer.wgu_q, big_layer.wgu_s, big_layer.wd_q,
+                               big_layer.wd_s, out2)
+    r3 = dev_bf16(xb)
+    lc.lacache_add_bf16(r3, y)
+    out3 = lc.ffn_fp8(r3, big_layer.norm_w, big_layer.wgu_q, big_layer.wgu_s, big_layer.wd_q, big_layer.wd_s)
+    torch.cuda.synchronize()
+    assert np.array_equal(host_bf16(r2), want)
+    assert np.array_equal(host_bf16(out2), host_bf16(out3))
+
+
 def test_residual_add_bit_exact():
     rng = np.random.default_rng(5)
     n = 1_000_003
