@@ -270,8 +270,9 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
         for (int r = 0; r < 4; ++r) sRed[wn][64 * wm + 16 * i + 4 * q + r] = am[i][r];
     }
     __syncthreads();
-    // ---- 1x128 quantization of each row's h-group; codes staged in LDS for coalesced stores
-    uint8_t* codes = stg[0].a;  // BM x 128 bytes, free after the main loop
+    // ---- 1x128 quantization of each row's h-group. A lane's codes for one
+    // column slab are gathered four lanes at a time into a 32-bit word (lanes
+    // 4m..4m+3 hold four consecutive columns) and stored from lane 4m.
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -281,25 +282,36 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
 #pragma unroll
         for (int c = 1; c < NCW; ++c) amax = __builtin_fmaxf(amax, sRed[c][row]);
         const float s = amax / kE4M3Max;
-        const bool fast = scale_is_fast(s);
         const float rs = fast_rcp(s);
+        // codes of q0 * (1 -+ 2^-20), q0 = h * rs: where every pair agrees they
+        // are E(RN32(h / s)) (see enc1_div_fast); else the division decides
+        uint32_t cw[NJ / 2];
+        bool agree = true;
+#pragma unroll
+        for (int j = 0; j < NJ / 2; ++j) {
+          const float q0 = h[i][j][r] * rs;
+          const float d = __builtin_fabsf(q0) * 0x1p-20f;
+          const uint32_t w = static_cast<uint32_t>(__builtin_amdgcn_cvt_pk_fp8_f32(clip448(q0 - d), clip448(q0 + d), 0, false));
+          cw[j] = w & 0xFFu;
+          agree = agree && (w & 0xFFu) == ((w >> 8) & 0xFFu);
+        }
+        if (s == 0.0f) {
+#pragma unroll
+          for (int j = 0; j < NJ / 2; ++j) cw[j] = 0u;
+        } else if (!(agree && scale_is_fast(s))) {
+#pragma unroll
+          for (int j = 0; j < NJ / 2; ++j) cw[j] = enc1_e4m3(qdiv(h[i][j][r], s));
+        }
 #pragma unroll
         for (int j = 0; j < NJ / 2; ++j) {
           const int col = (WC / 2) * wn + 16 * j + lr;
-          const float v = h[i][j][r];
-          uint32_t c = 0u;
-          if (s != 0.0f) c = fast ? enc1_div_fast(v, s, rs) : enc1_e4m3(qdiv(v, s));
-          codes[row * 128 + col] = static_cast<uint8_t>(c);
+          uint32_t c = cw[j];
+          c |= static_cast<uint32_t>(__shfl_down(static_cast<int>(c), 1, 64)) << 8;
+          c |= static_cast<uint32_t>(__shfl_down(static_cast<int>(c), 2, 64)) << 16;
+          if ((lr & 3) == 0 && m0 + row < M) *reinterpret_cast<uint32_t*>(hq + (m0 + row) * I + by * 128 + col) = c;
           if (h_tap != nullptr && m0 + row < M) h_tap[(m0 + row) * I + by * 128 + col] = h[i][j][r];
         }
       }
-    __syncthreads();
-    for (int c = t; c < BM * 8; c += NW * 64) {
-      const int row = c >> 3, ch = c & 7;
-      if (m0 + row < M)
-        *reinterpret_cast<uint4*>(hq + (m0 + row) * I + by * 128 + ch * 16) =
-            *reinterpret_cast<const uint4*>(codes + row * 128 + ch * 16);
-    }
     for (int row = t; row < BM; row += NW * 64) {
       float amax = sRed[0][row];
 #pragma unroll
