@@ -22,6 +22,9 @@ ffn     the FFN steps: weight block quantization, RMSNorm + group quantization,
 csweep  ctypes wrapper of ``e4m3_sweep.c``: the same e4m3 encoder in plain C,
         used only to check a device encoder over all 2^32 fp32 bit patterns
         fast enough for a test.
+attention  the first-layer attention and the FACache schedule (Sec. 3.3,
+        Eqs. 2-6): plain softmax attention, the online-softmax update and
+        the populate / resume steps of the cached state.
 """
 
-from . import bf16, e4m3, ffn  # noqa: F401
+from . import attention, bf16, e4m3, ffn  # noqa: F401
