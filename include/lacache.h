@@ -172,6 +172,47 @@ int lacache_add_bf16(void* stream, uint16_t* x_inout, const uint16_t* y, int64_t
 int lacache_encode_e4m3(void* stream, const float* v, uint8_t* codes, int64_t n);
 
 /*
+ * First-layer attention with FACache (Sec. 3.3, FACache; Eqs. 2-6).
+ *
+ * LaCache keeps the first transformer layer in bf16 and runs its attention
+ * as a FlashAttention-style scan over blocks of 64 keys, carrying per query
+ * row the running max m, the running sum l and the unnormalized output O~
+ * (Eqs. 2-6), and finishing with O = O~ / l. Within one SAR block of the
+ * generation only the rows of the current block C = [c_begin, c_end) change
+ * between denoising steps; FACache stores the state of every query block of
+ * 64 rows that has no row in C (a block "inside U"), taken over the key
+ * blocks that also have no row in C, and later steps resume from it.
+ *   q, k, v [heads x N x d] bf16    (input) one attention problem per head
+ *   o       [heads x N x d] bf16    (output) softmax(q k^T / sqrt(d)) v per
+ *                                   head, bidirectional (no mask)
+ *   cache_m, cache_l [heads x N] fp32, cache_o [heads x N x d] fp32
+ *                                   the FACache state of row n of head h at
+ *                                   index h*N + n (cache_o rows of d values):
+ *                                   m in base-2 units (max of q.k log2(e) /
+ *                                   sqrt(d)), l and O~ relative to it; only
+ *                                   the rows of query blocks inside U are
+ *                                   written or read
+ *   mode 0  populate: full attention; also writes the cache rows of the
+ *           query blocks inside U (their state after the key blocks inside U);
+ *   mode 1  resume: query blocks inside U load their cached state and scan
+ *           only the key blocks that overlap C; the result equals plain
+ *           attention of the current inputs when, since the mode-0 call with
+ *           the same c_begin, c_end, only rows of C of q, k and v changed;
+ *   mode 2  plain attention; the cache pointers are not used (may be NULL).
+ * d must be 128 and N a multiple of 64 (LACACHE_ERR_UNSUPPORTED otherwise);
+ * heads <= 4096, N <= 2^20; 0 <= c_begin <= c_end <= N, mode in 0..2
+ * (LACACHE_ERR_INVALID_ARG otherwise). heads == 0 or N == 0 launches nothing.
+ * The cache is written in mode 0 and read in mode 1; o must not overlap any
+ * other buffer, and in mode 0 the cache must not overlap q, k, v or o.
+ * Arithmetic: bf16 products accumulated in fp32 (MFMA), scores scaled and
+ * exponentiated in base 2, P rounded to bf16 for the P V product, m, l and
+ * O~ kept in fp32, o rounded to bf16.
+ */
+int lacache_facache_attention(void* stream, const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* o,
+                              float* cache_m, float* cache_l, float* cache_o, int64_t heads, int64_t N, int64_t d,
+                              int64_t c_begin, int64_t c_end, int mode);
+
+/*
  * Kernel-path policy for the GEMM stages, process-wide:
  *   0 = automatic (the skinny weight-streaming kernels for M <= 64,
  *       H <= 8192 and I <= 16384, the tiled MFMA kernels otherwise), 1 = always skinny

@@ -21,6 +21,10 @@ constexpr int64_t kMaxH = 16384;
 constexpr int64_t kMaxI = 65536;
 constexpr int64_t kMaxM = int64_t(1) << 24;
 constexpr int64_t kMaxN = 2 * kMaxI;
+constexpr int64_t kAttnHeadDim = 128;
+constexpr int64_t kAttnBlock = 64;
+constexpr int64_t kAttnMaxHeads = 4096;
+constexpr int64_t kAttnMaxN = int64_t(1) << 20;
 
 std::atomic<int> g_policy{0};
 
@@ -363,6 +367,30 @@ int lacache_encode_e4m3(void* stream, const float* v, uint8_t* codes, int64_t n)
   if (!ptrs_ok({v, codes})) return LACACHE_ERR_INVALID_ARG;
   if (overlap(rng(v, n * 4), rng(codes, n))) return LACACHE_ERR_INVALID_ARG;
   return hip_status(launch_encode_e4m3(static_cast<hipStream_t>(stream), v, codes, n));
+}
+
+int lacache_facache_attention(void* stream, const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* o,
+                              float* cache_m, float* cache_l, float* cache_o, int64_t heads, int64_t N, int64_t d,
+                              int64_t c_begin, int64_t c_end, int mode) {
+  if (heads < 0 || N < 0 || mode < 0 || mode > 2) return LACACHE_ERR_INVALID_ARG;
+  if (c_begin < 0 || c_begin > c_end || c_end > N) return LACACHE_ERR_INVALID_ARG;
+  if (d != kAttnHeadDim || N % kAttnBlock != 0 || heads > kAttnMaxHeads || N > kAttnMaxN)
+    return LACACHE_ERR_UNSUPPORTED;
+  if (heads == 0 || N == 0) return LACACHE_OK;
+  if (!ptrs_ok({q, k, v, o})) return LACACHE_ERR_INVALID_ARG;
+  const size_t act = static_cast<size_t>(heads * N * d) * 2;
+  const Range ro = rng(o, act), rq = rng(q, act), rk = rng(k, act), rv = rng(v, act);
+  if (mode == 2) {
+    if (!disjoint({ro}, {rq, rk, rv})) return LACACHE_ERR_INVALID_ARG;
+  } else {
+    if (!ptrs_ok({cache_m, cache_l, cache_o})) return LACACHE_ERR_INVALID_ARG;
+    const size_t st = static_cast<size_t>(heads * N) * 4;
+    const Range rm = rng(cache_m, st), rl = rng(cache_l, st), rc = rng(cache_o, st * d);
+    const bool ok = mode == 0 ? disjoint({ro, rm, rl, rc}, {rq, rk, rv}) : disjoint({ro}, {rq, rk, rv, rm, rl, rc});
+    if (!ok) return LACACHE_ERR_INVALID_ARG;
+  }
+  return hip_status(launch_facache_attention(static_cast<hipStream_t>(stream), q, k, v, o, cache_m, cache_l, cache_o,
+                                             heads, N, c_begin, c_end, mode));
 }
 
 int lacache_set_path_policy(int policy) {

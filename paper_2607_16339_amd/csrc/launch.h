@@ -60,4 +60,10 @@ hipError_t launch_gateup_skinny(hipStream_t st, const uint8_t* xq, const float* 
 hipError_t launch_down_skinny(hipStream_t st, const uint8_t* hq, const float* hs, const uint8_t* wq, const float* ws,
                               uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I);
 
+// First-layer attention with FACache: heads x N x 128 bf16, N % 64 == 0;
+// mode 0 populate, 1 resume, 2 plain (cache pointers unused).
+hipError_t launch_facache_attention(hipStream_t st, const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                                    uint16_t* o, float* cm, float* cl, float* co, int64_t heads, int64_t N, int64_t c0,
+                                    int64_t c1, int mode);
+
 }  // namespace lacache

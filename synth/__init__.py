@@ -125,3 +125,67 @@ def make_x(w: Workload, layer: int = 1, step: int = 0, rows=None) -> np.ndarray:
     if rows is not None:
         x = x[rows]
     return to_bf16_bits(x)
+
+
+# ---------------------------------------------------------------------------
+# First-layer attention inputs (FACache)
+# ---------------------------------------------------------------------------
+
+KIND_Q, KIND_K, KIND_V, KIND_SINK = range(10, 14)
+SINK_GAIN = 4.0
+
+
+@dataclass(frozen=True)
+class AttnWorkload:
+    wid: int
+    name: str
+    heads: int          # attention problems (sequences x heads)
+    N: int              # tokens per sequence: prompt + generated
+    c_begin: int        # current SAR block C = [c_begin, c_end)
+    c_end: int
+    d: int = 128
+    qk_std: float = 1.5
+    sinks: int = 2      # key rows per head with SINK_GAIN x the norm
+    notes: str = field(default="", compare=False)
+
+
+ATTN_WORKLOADS = {
+    "attn_tiny_h2_n256": AttnWorkload(
+        100, "attn_tiny_h2_n256", 2, 256, 96, 160, notes="C straddles two key blocks"),
+    "attn_sar512_h32": AttnWorkload(
+        101, "attn_sar512_h32", 32, 512, 288, 320,
+        notes="LLaDA-8B layer 1: 32 heads x 128; 256 prompt + 256 generated tokens, block 32, second block"),
+    "attn_batch8x1024_h32": AttnWorkload(
+        102, "attn_batch8x1024_h32", 256, 1024, 544, 576,
+        notes="8 sequences x 32 heads; 512 prompt + 512 generated tokens, block 32, second block"),
+}
+
+
+def attn_rng(w: AttnWorkload, step: int, kind: int) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence([SEED_ROOT, w.wid, 0, step, kind])))
+
+
+def make_qkv(w: AttnWorkload, step: int = 0, heads=None):
+    """bf16 (q, k, v) [heads, N, d] of denoising step `step` of the SAR block.
+
+    q, k ~ N(0, qk_std^2) and v ~ N(0, 1) per element; `sinks` key rows per
+    head (drawn once) are scaled by SINK_GAIN, giving a few dominant keys.
+    Step 0 draws every row; a later step redraws only the rows of C, so the
+    rows outside C stay those of step 0 (the premise of FACache). `heads`
+    selects a subset of the heads (the draw is the same)."""
+    shape = (w.heads, w.N, w.d)
+    out = []
+    for kind, std in ((KIND_Q, w.qk_std), (KIND_K, w.qk_std), (KIND_V, 1.0)):
+        a = attn_rng(w, 0, kind).standard_normal(shape, dtype=np.float32) * np.float32(std)
+        if kind == KIND_K and w.sinks:
+            rows = attn_rng(w, 0, KIND_SINK).integers(0, w.N, size=(w.heads, w.sinks))
+            for h in range(w.heads):
+                a[h, rows[h]] *= np.float32(SINK_GAIN)
+        if step > 0:
+            g = attn_rng(w, step, kind)
+            a[:, w.c_begin:w.c_end] = g.standard_normal((w.heads, w.c_end - w.c_begin, w.d),
+                                                        dtype=np.float32) * np.float32(std)
+        if heads is not None:
+            a = a[heads]
+        out.append(to_bf16_bits(a))
+    return tuple(out)

@@ -116,6 +116,36 @@ def test_addnorm_validation(L):
     assert fused(p[0], p[1], p[7], M=0) == OK
 
 
+def test_facache_attention_validation(L):
+    f = Fake()
+    q, k, v, o, cm, cl, co = (f() for _ in range(7))
+
+    def att(heads=2, N=256, d=128, c0=64, c1=128, mode=0, **over):
+        a = dict(q=q, k=k, v=v, o=o, cm=cm, cl=cl, co=co)
+        a.update(over)
+        return L.lacache_facache_attention(None, a["q"], a["k"], a["v"], a["o"], a["cm"], a["cl"], a["co"],
+                                           heads, N, d, c0, c1, mode)
+    assert att(d=64) == UNSUP
+    assert att(N=200, c1=100) == UNSUP          # N not a multiple of 64
+    assert att(heads=4097) == UNSUP
+    assert att(N=(1 << 20) + 64, c1=100) == UNSUP
+    assert att(mode=3) == INVALID
+    assert att(mode=-1) == INVALID
+    assert att(heads=-1) == INVALID
+    assert att(c0=130, c1=120) == INVALID       # c_begin > c_end
+    assert att(c0=-1) == INVALID
+    assert att(c1=257) == INVALID               # c_end > N
+    assert att(q=None) == INVALID
+    assert att(o=o + 8) == INVALID              # misaligned
+    assert att(o=q + 4096) == INVALID           # o overlaps q
+    assert att(cm=None) == INVALID              # populate needs the cache
+    assert att(mode=1, co=None) == INVALID      # resume needs the cache
+    assert att(mode=0, cl=k + 64) == INVALID    # cache written over k
+    assert att(mode=1, cm=o + 64) == INVALID    # o written over the cache
+    assert att(mode=0, co=cm) == INVALID        # two cache outputs alias
+    assert att(heads=0) == OK and att(N=0, c0=0, c1=0) == OK  # nothing launched
+
+
 def test_path_policy(L):
     assert L.lacache_set_path_policy(7) == INVALID
     prev = L.lacache_set_path_policy(1)
