@@ -10,6 +10,7 @@ Everything here is fp64 on bf16 inputs (raw uint16 bit patterns):
   attention          softmax(Q K^T * scale) V per head, the definition;
   online_state       the streaming update of Eqs. 2-6 over a list of key
                      blocks, in the paper's order of operations;
+  attention_lse      the row-wise log-sum-exp L of the scaled scores;
   finalize           O = diag(l)^-1 O~;
   facache_blocks     which key/value blocks lie inside U and which overlap C;
   facache_attention  the schedule: populate (first step of a block) or
@@ -38,6 +39,18 @@ def attention(q_bits, k_bits, v_bits, scale=None):
     p = np.exp(s)
     p = p / p.sum(axis=-1, keepdims=True)
     return np.matmul(p, v)
+
+
+def attention_lse(q_bits, k_bits, scale=None):
+    """L = log sum_j exp(s_ij) of the scaled scores s = Q K^T * scale, per head
+    and query row (the log-sum-exp the algorithm of the first layer's
+    FlashAttention also writes out, Appendix, Alg. 1)."""
+    q, k = _f64(q_bits), _f64(k_bits)
+    d = q.shape[-1]
+    scale = 1.0 / np.sqrt(d) if scale is None else scale
+    s = np.matmul(q, np.swapaxes(k, -1, -2)) * scale
+    m = s.max(axis=-1)
+    return m + np.log(np.exp(s - m[..., None]).sum(axis=-1))
 
 
 def empty_state(rows, d):

@@ -111,3 +111,25 @@ def test_facache_schedule_is_plain_attention_across_steps():
     out3, _ = A.facache_attention(q2, k3, v2, c0, c1, blk, cache)
     assert np.allclose(out3[:, :64], out2[:, :64], rtol=0, atol=1e-13)
     assert not np.allclose(A.attention(q2, k3, v2)[:, :64], out2[:, :64], rtol=0, atol=1e-6)
+
+
+def test_lse_closed_form_and_library():
+    # equal keys: every score is s, so L = s + log(n)
+    q = _rand((1, 3, 8), 30)
+    k = np.tile(_rand((1, 1, 8), 31), (1, 5, 1))
+    qf, kf = bf16_to_f32(q[0]).astype(np.float64), bf16_to_f32(k[0, 0]).astype(np.float64)
+    want = qf @ kf / np.sqrt(8) + np.log(5.0)
+    assert np.allclose(A.attention_lse(q, k)[0], want, rtol=0, atol=1e-14)
+    # wide-range scores against torch.logsumexp in fp64
+    q, k = _rand((2, 19, 16), 32, 6.0), _rand((2, 23, 16), 33, 6.0)
+    f = lambda b: torch.from_numpy(bf16_to_f32(b).astype(np.float64))
+    ref = torch.logsumexp(f(q) @ f(k).transpose(-1, -2) / 4.0, dim=-1).numpy()
+    assert np.allclose(A.attention_lse(q, k), ref, rtol=1e-15, atol=1e-12)
+
+
+def test_lse_from_the_online_state():
+    # m + log(l) after any partition is the log-sum-exp
+    q, k, v = _rand((1, 7, 8), 34, 3.0), _rand((1, 30, 8), 35, 3.0), _rand((1, 30, 8), 36)
+    qf, kf, vf = (bf16_to_f32(x[0]).astype(np.float64) for x in (q, k, v))
+    m, l, _ = A.online_state(qf, kf, vf, [(20, 30), (0, 9), (9, 20)], 1 / np.sqrt(8), A.empty_state(7, 8))
+    assert np.allclose(m + np.log(l), A.attention_lse(q, k)[0], rtol=0, atol=1e-13)
