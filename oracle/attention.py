@@ -81,11 +81,12 @@ def finalize(state):
 
 def facache_blocks(N, block, c_begin, c_end):
     """Key/value blocks of `block` rows: those with no row in [c_begin, c_end)
-    (inside U) and those overlapping the current block C."""
+    (inside U) and those overlapping the current block C. An empty C
+    (c_begin == c_end) overlaps no block."""
     u, c = [], []
     for a in range(0, N, block):
         b = min(a + block, N)
-        (c if (a < c_end and c_begin < b) else u).append((a, b))
+        (c if (c_begin < c_end and a < c_end and c_begin < b) else u).append((a, b))
     return u, c
 
 

@@ -92,6 +92,10 @@ def test_block_partition_for_the_current_block():
     assert c == [(0, 64), (64, 128), (128, 192)] and u == [(192, 256)]
     u, c = A.facache_blocks(128, 64, 128, 128)  # empty C
     assert c == [] and u == [(0, 64), (64, 128)]
+    u, c = A.facache_blocks(192, 64, 100, 100)  # empty C inside a block overlaps nothing
+    assert c == [] and u == [(0, 64), (64, 128), (128, 192)]
+    u, c = A.facache_blocks(192, 64, 127, 129)  # two rows straddling a block edge
+    assert c == [(64, 128), (128, 192)] and u == [(0, 64)]
 
 
 def test_facache_schedule_is_plain_attention_across_steps():
