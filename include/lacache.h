@@ -185,6 +185,9 @@ int lacache_encode_e4m3(void* stream, const float* v, uint8_t* codes, int64_t n)
  *   q, k, v [heads x N x d] bf16    (input) one attention problem per head
  *   o       [heads x N x d] bf16    (output) softmax(q k^T / sqrt(d)) v per
  *                                   head, bidirectional (no mask)
+ *   lse     [heads x N] fp32        (optional output, NULL to skip) the
+ *                                   row-wise log-sum-exp of q k^T / sqrt(d),
+ *                                   natural log (Alg. 1 of the Appendix)
  *   cache_m, cache_l [heads x N] fp32, cache_o [heads x N x d] fp32
  *                                   the FACache state of row n of head h at
  *                                   index h*N + n (cache_o rows of d values):
@@ -202,15 +205,17 @@ int lacache_encode_e4m3(void* stream, const float* v, uint8_t* codes, int64_t n)
  * d must be 128 and N a multiple of 64 (LACACHE_ERR_UNSUPPORTED otherwise);
  * heads <= 4096, N <= 2^20; 0 <= c_begin <= c_end <= N, mode in 0..2
  * (LACACHE_ERR_INVALID_ARG otherwise). heads == 0 or N == 0 launches nothing.
- * The cache is written in mode 0 and read in mode 1; o must not overlap any
- * other buffer, and in mode 0 the cache must not overlap q, k, v or o.
+ * The cache is written in mode 0 and read in mode 1; o and lse must not
+ * overlap any other buffer, and in mode 0 the cache must not overlap q, k, v,
+ * o or lse. An empty C (c_begin == c_end) overlaps no block: populate then
+ * stores the state over all keys and resume streams no key block.
  * Arithmetic: bf16 products accumulated in fp32 (MFMA), scores scaled and
  * exponentiated in base 2, P rounded to bf16 for the P V product, m, l and
  * O~ kept in fp32, o rounded to bf16.
  */
 int lacache_facache_attention(void* stream, const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* o,
-                              float* cache_m, float* cache_l, float* cache_o, int64_t heads, int64_t N, int64_t d,
-                              int64_t c_begin, int64_t c_end, int mode);
+                              float* lse, float* cache_m, float* cache_l, float* cache_o, int64_t heads, int64_t N,
+                              int64_t d, int64_t c_begin, int64_t c_end, int mode);
 
 /*
  * Kernel-path policy for the GEMM stages, process-wide:

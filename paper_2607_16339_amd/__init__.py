@@ -132,16 +132,18 @@ def lacache_encode_e4m3(v, codes, stream=None):
                                     _ptr(codes, _U8, "codes", tuple(v.shape)), v.numel()), "lacache_encode_e4m3")
 
 
-def lacache_facache_attention(q, k, v, o, cache_m=None, cache_l=None, cache_o=None, c_begin=0, c_end=0, mode=2,
-                              stream=None):
-    """q, k, v, o: [heads, N, d] bf16; cache_m, cache_l [heads, N] and cache_o
-    [heads, N, d] fp32 (modes 0 populate and 1 resume; unused in mode 2)."""
+def lacache_facache_attention(q, k, v, o, lse=None, cache_m=None, cache_l=None, cache_o=None, c_begin=0, c_end=0,
+                              mode=2, stream=None):
+    """q, k, v, o: [heads, N, d] bf16; lse [heads, N] fp32 or None; cache_m,
+    cache_l [heads, N] and cache_o [heads, N, d] fp32 (modes 0 populate and
+    1 resume; unused in mode 2)."""
     heads, N, d = q.shape
     cache = mode in (0, 1)
     f32 = (torch.float32,)
     check(lib().lacache_facache_attention(
         _stream(stream, q), _ptr(q, _BF16, "q"), _ptr(k, _BF16, "k", (heads, N, d)), _ptr(v, _BF16, "v", (heads, N, d)),
-        _ptr(o, _BF16, "o", (heads, N, d)), _ptr(cache_m, f32, "cache_m", (heads, N), optional=not cache),
+        _ptr(o, _BF16, "o", (heads, N, d)), _ptr(lse, f32, "lse", (heads, N), optional=True),
+        _ptr(cache_m, f32, "cache_m", (heads, N), optional=not cache),
         _ptr(cache_l, f32, "cache_l", (heads, N), optional=not cache),
         _ptr(cache_o, f32, "cache_o", (heads, N, d), optional=not cache), heads, N, d, c_begin, c_end, mode),
         "lacache_facache_attention")

@@ -31,7 +31,7 @@ SIGNATURES = {
     "lacache_ffn_fp8_ws": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I, _P, ctypes.c_size_t]),
     "lacache_add_bf16": (_I, [_P, _P, _P, _I64]),
     "lacache_encode_e4m3": (_I, [_P, _P, _P, _I64]),
-    "lacache_facache_attention": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, _I64, _I]),
+    "lacache_facache_attention": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, _I64, _I]),
     "lacache_set_path_policy": (_I, [_I]),
     "lacache_status_string": (ctypes.c_char_p, [_I]),
     "lacache_release_workspace": (None, []),

@@ -370,27 +370,28 @@ int lacache_encode_e4m3(void* stream, const float* v, uint8_t* codes, int64_t n)
 }
 
 int lacache_facache_attention(void* stream, const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* o,
-                              float* cache_m, float* cache_l, float* cache_o, int64_t heads, int64_t N, int64_t d,
-                              int64_t c_begin, int64_t c_end, int mode) {
+                              float* lse, float* cache_m, float* cache_l, float* cache_o, int64_t heads, int64_t N,
+                              int64_t d, int64_t c_begin, int64_t c_end, int mode) {
   if (heads < 0 || N < 0 || mode < 0 || mode > 2) return LACACHE_ERR_INVALID_ARG;
   if (c_begin < 0 || c_begin > c_end || c_end > N) return LACACHE_ERR_INVALID_ARG;
   if (d != kAttnHeadDim || N % kAttnBlock != 0 || heads > kAttnMaxHeads || N > kAttnMaxN)
     return LACACHE_ERR_UNSUPPORTED;
   if (heads == 0 || N == 0) return LACACHE_OK;
-  if (!ptrs_ok({q, k, v, o})) return LACACHE_ERR_INVALID_ARG;
-  const size_t act = static_cast<size_t>(heads * N * d) * 2;
+  if (!ptrs_ok({q, k, v, o}) || !opt_ptr_ok(lse)) return LACACHE_ERR_INVALID_ARG;
+  const size_t act = static_cast<size_t>(heads * N * d) * 2, st = static_cast<size_t>(heads * N) * 4;
   const Range ro = rng(o, act), rq = rng(q, act), rk = rng(k, act), rv = rng(v, act);
+  const Range rs = lse != nullptr ? rng(lse, st) : Range{0, 0};
   if (mode == 2) {
-    if (!disjoint({ro}, {rq, rk, rv})) return LACACHE_ERR_INVALID_ARG;
+    if (!disjoint({ro, rs}, {rq, rk, rv})) return LACACHE_ERR_INVALID_ARG;
   } else {
     if (!ptrs_ok({cache_m, cache_l, cache_o})) return LACACHE_ERR_INVALID_ARG;
-    const size_t st = static_cast<size_t>(heads * N) * 4;
     const Range rm = rng(cache_m, st), rl = rng(cache_l, st), rc = rng(cache_o, st * d);
-    const bool ok = mode == 0 ? disjoint({ro, rm, rl, rc}, {rq, rk, rv}) : disjoint({ro}, {rq, rk, rv, rm, rl, rc});
+    const bool ok =
+        mode == 0 ? disjoint({ro, rs, rm, rl, rc}, {rq, rk, rv}) : disjoint({ro, rs}, {rq, rk, rv, rm, rl, rc});
     if (!ok) return LACACHE_ERR_INVALID_ARG;
   }
   return hip_status(launch_facache_attention(static_cast<hipStream_t>(stream), q, k, v, o, cache_m, cache_l, cache_o,
-                                             heads, N, c_begin, c_end, mode));
+                                             lse, heads, N, c_begin, c_end, mode));
 }
 
 int lacache_set_path_policy(int policy) {

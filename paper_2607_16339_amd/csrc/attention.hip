@@ -1,22 +1,35 @@
 // First-layer FlashAttention with FACache (Sec. 3.3, FACache; Eqs. 2-6).
 //
-// One workgroup per (head, block of 64 query rows); 4 wavefronts of 16 rows.
-// Key/value blocks of 64 rows stream through LDS; per block every wavefront
-//   * computes S^T = K Q^T with bf16 MFMAs (16x16x32): lane (g, r) of a 16x16
-//     output tile holds keys 4g..4g+3 of query row r, so a query row's
-//     softmax state lives in the 4 lanes r, r+16, r+32, r+48;
+// Work decomposition. A workgroup of 4 wavefronts owns 32*NQ query rows per
+// wavefront (128 or 256 rows per workgroup) of one head and streams 64-key
+// tiles of K and V through a two-stage LDS ring filled by direct
+// global->LDS copies, so the copy of tile i+1 overlaps the MFMAs of tile i.
+// Per tile every wavefront
+//   * computes S^T = K Q^T with bf16 MFMAs 32x32x16 (Q^T stays in registers;
+//     lane (g, r) holds keys 8a + 4g + i of query r, a, i = 0..3);
 //   * updates the online-softmax state (m, l) in the log2 domain (Eqs. 2-5,
-//     with exp2 and the scale folded into the scores);
-//   * accumulates O~^T += V^T P^T (Eq. 6) with P in bf16; lane (g, r) of an
-//     output tile holds dims 4g..4g+3 of query row r.
-// V is stored transposed in LDS so that the key order of the P^T operand,
-// which is fixed by the S^T output layout, can be matched by the V^T operand.
+//     the 1/sqrt(d) scale folded into the exponent); each of the two lanes
+//     that share a query row keeps its own partial l, and the two are added
+//     whenever the whole state is needed;
+//   * accumulates O~^T += V^T P^T (Eq. 6) with P rounded to bf16. The V^T
+//     operand is read from the row-major V tile with the transposing LDS
+//     read (ds_read_b64_tr_b16): each lane gets 4 consecutive keys of one
+//     dimension, matching the key order P^T inherits from the S^T layout.
 //
-// FACache: a query block with no row in the current block C (inside U)
-// streams the key blocks inside U first; in populate mode it then stores its
-// state (m, l, O~) in the cache before streaming the blocks that overlap C.
-// In resume mode it loads the cached state and streams only the blocks that
-// overlap C. Query blocks overlapping C stream everything from scratch.
+// Key order and FACache. Every query row streams the key blocks inside U
+// (ascending), then those overlapping the current block C (ascending). After
+// the U blocks the two partial sums l are merged, and in populate mode the
+// wavefronts whose 64-row block lies inside U store (m, l, O~) in the cache.
+// In resume mode those wavefronts load that state and compute only the C
+// blocks (a workgroup with no row in a block overlapping C streams only
+// those); the others recompute everything. All three modes therefore run the
+// same arithmetic in the same order, and a resume on inputs that changed only
+// inside C reproduces plain attention of the new inputs bit for bit.
+//
+// Scheduling. Work item w = (head, query block) in head-major order, heavy
+// query blocks (those overlapping C) first within a head; consecutive work
+// items go to the same XCD (workgroups are dealt to the 8 XCDs round-robin),
+// so the query blocks of a head share that XCD's L2 copy of its K and V.
 #include "device.h"
 #include "launch.h"
 
@@ -24,181 +37,312 @@ namespace lacache {
 namespace {
 
 typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
-typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+typedef short s4 __attribute__((ext_vector_type(4)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) s4 lds_s4;
 
-constexpr int kD = 128;         // head dimension
-constexpr int kBlk = 64;        // query rows and key rows per block
-constexpr int kVtStride = 68;   // V^T row stride in bf16 (136 B: conflict-free 8-byte reads)
+constexpr int kD = 128;                   // head dimension
+constexpr int kKB = 64;                   // keys per tile = rows per FACache block
+constexpr int kWaves = 4;
+constexpr int kTileBytes = kKB * kD * 2;  // one K or V tile (16 KiB)
+constexpr int kStageBytes = 2 * kTileBytes;
+constexpr int kStages = 2;
 
-__device__ __forceinline__ v4f mfma_bf16(bf8 a, bf8 b, v4f c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+struct AttnArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  uint16_t* o;
+  float* cm;
+  float* cl;
+  float* co;
+  float* lse;
+  int64_t N;
+  int nqb;      // query blocks (of 4 * 32 * NQ rows) per head
+  int nkb;      // key blocks (of 64 rows) per head
+  int cb0, nc;  // key blocks overlapping C: [cb0, cb0 + nc)
+  int qbh0;     // first query block overlapping those key blocks
+  int nheavy;   // query blocks overlapping them
+  int total;    // workgroups
+  float scale_log2;
+};
+
+__device__ __forceinline__ v16f mfma32(bf8 a, bf8 b, v16f c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
-__device__ __forceinline__ bf8 as_bf8(uint4 v) {
-  const u4 w = {v.x, v.y, v.z, v.w};
-  return __builtin_bit_cast(bf8, w);
+
+// two transposing 8-byte LDS reads -> one 8-element operand
+__device__ __forceinline__ bf8 read_tr2(const uint8_t* p0, const uint8_t* p1) {
+  const s4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4*)(p0));
+  const s4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4*)(p1));
+  return __builtin_bit_cast(bf8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
-template <int kMode>  // 0: populate the cache, 1: resume from it, 2: plain attention
-__global__ __launch_bounds__(256) void facache_attention_kernel(
-    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
-    uint16_t* __restrict__ o, float* __restrict__ cm, float* __restrict__ cl, float* __restrict__ co, int64_t N,
-    int64_t c0, int64_t c1, float scale_log2) {
-  __shared__ __align__(16) uint16_t Ks[kBlk * kD];         // [key][dim], 16-byte chunks xor-swizzled by key
-  __shared__ __align__(16) uint16_t Vt[kD * kVtStride];    // [dim][key]
+__device__ __forceinline__ uint32_t pack_bf16_rne(float lo, float hi) {
+  return pack_bf16x2(lo, hi);
+}
 
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int g = lane >> 4, r = lane & 15;
-  const int64_t nqb = N / kBlk;
-  const int64_t h = blockIdx.x / nqb, qb = blockIdx.x % nqb;
-  const int64_t hb = h * N * kD;
-  const int64_t row = qb * kBlk + wave * 16 + r;  // this lane's query row
+template <int kMode, int NQ>  // kMode 0: populate, 1: resume, 2: plain attention
+__global__ __launch_bounds__(256, NQ == 1 ? 2 : 1) void facache_attention_kernel(AttnArgs a) {
+  __shared__ __align__(16) uint8_t smem[kStages * kStageBytes];
+  constexpr int QR = 32 * NQ, WR = kWaves * QR;
+  const int t = threadIdx.x, lane = t & 63, wave = wave_uniform(t >> 6);
+  const int g = lane >> 5, r = lane & 31;
 
-  bf8 qf[4];  // Q^T operands: query row r, dims 32 kk + 8 g ..
-#pragma unroll
-  for (int kk = 0; kk < 4; ++kk) qf[kk] = as_bf8(*reinterpret_cast<const uint4*>(q + hb + row * kD + 32 * kk + 8 * g));
+  // work item: consecutive items on one XCD
+  const int bid = blockIdx.x, xcd = bid & 7, slot = bid >> 3;
+  const int per = a.total >> 3, rem = a.total & 7;
+  const int w = xcd < rem ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
+  const int64_t h = w / a.nqb;
+  const int j = w - static_cast<int>(h) * a.nqb;
+  const bool heavy = j < a.nheavy;
+  const int qb = heavy ? a.qbh0 + j : (j - a.nheavy < a.qbh0 ? j - a.nheavy : j);
+  const int64_t row0 = static_cast<int64_t>(qb) * WR + wave * QR;  // this wavefront's first query row
+  const bool valid = row0 < a.N;
+  const int64_t qblk = row0 / kKB;
+  const bool in_u = !(qblk >= a.cb0 && qblk < a.cb0 + a.nc);
+  const bool use_cache = kMode == 1 && in_u;  // this wavefront resumes from the cache
+  const bool light = kMode == 1 && !heavy;     // ... and so does every wavefront of the workgroup
+  const int nU = a.nkb - a.nc;
+  const int nlist = light ? a.nc : a.nkb;
+  const int64_t hN = h * a.N;
+  const uint16_t* kh = a.k + hN * kD;
+  const uint16_t* vh = a.v + hN * kD;
 
-  const bool q_in_u = !(qb * kBlk < c1 && c0 < (qb + 1) * kBlk);  // no row of this block in C
-  float m = -__builtin_inff(), l = 0.0f;
-  float ot[8][4];  // O~^T tiles: dims 16 dt + 4 g + i of row r
+  // Q^T operands: query row0 + 32 qi + r, dims 16 kk + 8 g ..
+  bf8 qf[NQ][8];
 #pragma unroll
-  for (int dt = 0; dt < 8; ++dt)
+  for (int qi = 0; qi < NQ; ++qi) {
+    const int64_t row = valid ? row0 + 32 * qi + r : 0;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) ot[dt][i] = 0.0f;
+    for (int kk = 0; kk < 8; ++kk) qf[qi][kk] = *reinterpret_cast<const bf8*>(a.q + (hN + row) * kD + 16 * kk + 8 * g);
+  }
 
-  // one key/value block: stage it, then Eqs. 2-6 for this wave's 16 rows
-  auto process = [&](int64_t kb) {
-    __syncthreads();  // every wave is done with the previous block
-    const int64_t kr0 = kb * kBlk;
+  float m[NQ], l[NQ];
+  v16f ot[NQ][4];  // O~^T: element 4 b + i of tile dt = dim 32 dt + 8 b + 4 g + i of query r
+  if (use_cache && valid) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int c = t + 256 * j;          // 16-byte chunk of the 64 x 128 tile
-      const int key = c >> 4, ch = c & 15;
-      const uint4 kv = *reinterpret_cast<const uint4*>(k + hb + (kr0 + key) * kD + 8 * ch);
-      *reinterpret_cast<uint4*>(Ks + key * kD + 8 * (ch ^ (key & 15))) = kv;
-      const uint4 vv = *reinterpret_cast<const uint4*>(v + hb + (kr0 + key) * kD + 8 * ch);
-      const uint32_t w[4] = {vv.x, vv.y, vv.z, vv.w};
+    for (int qi = 0; qi < NQ; ++qi) {
+      const int64_t sb = hN + row0 + 32 * qi + r;
+      m[qi] = a.cm[sb];
+      l[qi] = g == 0 ? a.cl[sb] : 0.0f;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        Vt[(8 * ch + 2 * e) * kVtStride + key] = static_cast<uint16_t>(w[e] & 0xFFFFu);
-        Vt[(8 * ch + 2 * e + 1) * kVtStride + key] = static_cast<uint16_t>(w[e] >> 16);
-      }
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          const float4 c4 = *reinterpret_cast<const float4*>(a.co + sb * kD + 32 * dt + 8 * b + 4 * g);
+          ot[qi][dt][4 * b + 0] = c4.x;
+          ot[qi][dt][4 * b + 1] = c4.y;
+          ot[qi][dt][4 * b + 2] = c4.z;
+          ot[qi][dt][4 * b + 3] = c4.w;
+        }
     }
-    __syncthreads();
-    // S^T = K Q^T: 4 key tiles of 16, K-dim 128 in 4 steps
-    float s[4][4];
+  } else {
 #pragma unroll
-    for (int kt = 0; kt < 4; ++kt) {
-      const int key = 16 * kt + r;
-      v4f acc = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int qi = 0; qi < NQ; ++qi) {
+      m[qi] = -__builtin_inff();
+      l[qi] = 0.0f;
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        const bf8 kf = as_bf8(*reinterpret_cast<const uint4*>(Ks + key * kD + 8 * ((4 * kk + g) ^ (key & 15))));
-        acc = mfma_bf16(kf, qf[kk], acc);
-      }
+      for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) s[kt][i] = acc[i] * scale_log2;
+        for (int e = 0; e < 16; ++e) ot[qi][dt][e] = 0.0f;
     }
-    // online softmax of row r (the 4 lanes r + 16 g share it)
-    float mx = s[0][0];
+  }
+
+  // i-th key block of this workgroup's list
+  auto key_block = [&](int i) -> int {
+    if (light) return a.cb0 + i;
+    return i < nU ? (i < a.cb0 ? i : i + a.nc) : a.cb0 + (i - nU);
+  };
+  // Copy K and V tiles of list entry i into stage s. LDS slot p (16 bytes)
+  // holds key p / 16, 16-byte chunk (p % 16) ^ swizzle(key): K swizzles by
+  // key % 16 (conflict-free 16-byte MFMA operand reads), V by 4 (key % 4)
+  // (conflict-free transposing reads).
+  const uint32_t smem_u32 = lds_u32(smem);
+  auto issue = [&](int i, int s) {
+    const int64_t kr0 = static_cast<int64_t>(key_block(i)) * kKB;
+    const uint32_t kl = smem_u32 + s * kStageBytes, vl = kl + kTileBytes;
 #pragma unroll
-    for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) mx = __builtin_fmaxf(mx, s[kt][i]);
-    mx = __builtin_fmaxf(mx, __shfl_xor(mx, 16, 64));
-    mx = __builtin_fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = __builtin_fmaxf(m, mx);                 // Eq. 2
-    const float alpha = __builtin_amdgcn_exp2f(m - m_new);      // Eq. 3
-    float p[4][4], ps = 0.0f;
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        p[kt][i] = __builtin_amdgcn_exp2f(s[kt][i] - m_new);   // Eq. 4
-        ps += p[kt][i];
-      }
-    ps += __shfl_xor(ps, 16, 64);
-    ps += __shfl_xor(ps, 32, 64);
-    l = alpha * l + ps;                                         // Eq. 5
-    m = m_new;
-#pragma unroll
-    for (int dt = 0; dt < 8; ++dt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) ot[dt][i] *= alpha;
-    // P^T operands: key step ks covers key tiles 2 ks (slots 8g..8g+3) and
-    // 2 ks + 1 (slots 8g+4..8g+7), keys 4g..4g+3 of each
-    bf8 pb[2];
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      const uint4 pw = make_uint4(pack_bf16x2(p[2 * ks][0], p[2 * ks][1]), pack_bf16x2(p[2 * ks][2], p[2 * ks][3]),
-                                  pack_bf16x2(p[2 * ks + 1][0], p[2 * ks + 1][1]),
-                                  pack_bf16x2(p[2 * ks + 1][2], p[2 * ks + 1][3]));
-      pb[ks] = as_bf8(pw);
-    }
-    // O~^T += V^T P^T (Eq. 6): V^T operand of dim 16 dt + r, the same key order
-#pragma unroll
-    for (int dt = 0; dt < 8; ++dt) {
-      v4f acc = {ot[dt][0], ot[dt][1], ot[dt][2], ot[dt][3]};
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        const uint16_t* vr = Vt + (16 * dt + r) * kVtStride + 32 * ks + 4 * g;
-        const uint2 lo = *reinterpret_cast<const uint2*>(vr);
-        const uint2 hi = *reinterpret_cast<const uint2*>(vr + 16);
-        acc = mfma_bf16(as_bf8(make_uint4(lo.x, lo.y, hi.x, hi.y)), pb[ks], acc);
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) ot[dt][i] = acc[i];
+    for (int n = 0; n < 4; ++n) {
+      const int p0 = n * 256 + wave * 64, p = p0 + lane;
+      const int key = p >> 4, cp = p & 15;
+      dma16(kh + (kr0 + key) * kD + 8 * (cp ^ (key & 15)), kl + 16 * p0);
+      dma16(vh + (kr0 + key) * kD + 8 * (cp ^ (4 * (key & 3))), vl + 16 * p0);
     }
   };
 
-  // a block [a, a + 64) overlaps C = [c0, c1) when a < c1 and c0 < a + 64
-  auto overlaps_c = [&](int64_t kb) { return kb * kBlk < c1 && c0 < (kb + 1) * kBlk; };
-  const int64_t nkb = N / kBlk;
-  const int64_t sb = h * N + row;  // state index of this row
-  if (kMode == 1 && q_in_u) {
-    m = cm[sb];
-    l = cl[sb];
+  // per-lane LDS offsets
+  const int G = lane >> 4, io = lane & 15;
+  // V^T operand (transposing read): the lane addresses key 4 (G/2) + io/4 (+ 16 ks + 8 hh)
+  // and dims 32 dt + 16 (G%2) + 4 (io%4); chunk swizzle 4 (key % 4) = 4 (io/4)
+  const int e_sw = io >> 2;
+  const int v_base = (4 * (G >> 1) + (io >> 2)) * 256 + (2 * (G & 1) + ((io & 3) >> 1)) * 16 + 8 * (io & 1);
+  const float c = a.scale_log2;
+
+  auto compute = [&](int s) {
+    const uint8_t* Kt = smem + s * kStageBytes;
+    const uint8_t* Vt = Kt + kTileBytes;
+    // S^T = K Q^T
+    v16f sa[NQ][2];
 #pragma unroll
-    for (int dt = 0; dt < 8; ++dt) {
-      const float4 c4 = *reinterpret_cast<const float4*>(co + sb * kD + 16 * dt + 4 * g);
-      ot[dt][0] = c4.x; ot[dt][1] = c4.y; ot[dt][2] = c4.z; ot[dt][3] = c4.w;
-    }
-  } else {
-    for (int64_t kb = 0; kb < nkb; ++kb)
-      if (!overlaps_c(kb)) process(kb);  // the key blocks inside U
-    if (kMode == 0 && q_in_u) {
-      if (g == 0) {
-        cm[sb] = m;
-        cl[sb] = l;
+    for (int qi = 0; qi < NQ; ++qi)
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) sa[qi][tt][e] = 0.0f;
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int kk = 0; kk < 8; ++kk) {
+        const int key = 32 * tt + r;
+        const bf8 kf = *reinterpret_cast<const bf8*>(Kt + key * 256 + (((2 * kk + g) ^ (key & 15)) << 4));
+#pragma unroll
+        for (int qi = 0; qi < NQ; ++qi) sa[qi][tt] = mfma32(kf, qf[qi][kk], sa[qi][tt]);
       }
+    // online softmax (Eqs. 2-5) and the P^T operands
+    bf8 pb[NQ][4];
 #pragma unroll
-      for (int dt = 0; dt < 8; ++dt)
-        *reinterpret_cast<float4*>(co + sb * kD + 16 * dt + 4 * g) = make_float4(ot[dt][0], ot[dt][1], ot[dt][2], ot[dt][3]);
+    for (int qi = 0; qi < NQ; ++qi) {
+      float mx = sa[qi][0][0];
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) mx = __builtin_fmaxf(mx, sa[qi][tt][e]);
+      mx = __builtin_fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float mn = __builtin_fmaxf(m[qi], mx * c);         // Eq. 2
+      const float alpha = __builtin_amdgcn_exp2f(m[qi] - mn);  // Eq. 3
+      m[qi] = mn;
+      float ps = 0.0f;
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sa[qi][tt][e], c, -mn));  // Eq. 4
+          sa[qi][tt][e] = p;
+          ps += p;
+        }
+      l[qi] = alpha * l[qi] + ps;  // Eq. 5 (this lane's keys)
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) ot[qi][dt][e] *= alpha;
+      // step ks covers keys 16 ks .. 16 ks + 15: elements 8 (ks % 2) .. + 7 of S^T tile ks / 2
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const int tt = ks >> 1, e0 = 8 * (ks & 1);
+        const uint4 w4 = make_uint4(pack_bf16_rne(sa[qi][tt][e0 + 0], sa[qi][tt][e0 + 1]),
+                                    pack_bf16_rne(sa[qi][tt][e0 + 2], sa[qi][tt][e0 + 3]),
+                                    pack_bf16_rne(sa[qi][tt][e0 + 4], sa[qi][tt][e0 + 5]),
+                                    pack_bf16_rne(sa[qi][tt][e0 + 6], sa[qi][tt][e0 + 7]));
+        pb[qi][ks] = __builtin_bit_cast(bf8, w4);
+      }
+    }
+    // O~^T += V^T P^T (Eq. 6)
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) {
+      const uint8_t* vd = Vt + v_base + 64 * (dt ^ e_sw);
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const bf8 vf = read_tr2(vd + (16 * ks) * 256, vd + (16 * ks + 8) * 256);
+#pragma unroll
+        for (int qi = 0; qi < NQ; ++qi) ot[qi][dt] = mfma32(vf, pb[qi][ks], ot[qi][dt]);
+      }
+    }
+  };
+
+  // merge the two partial sums of a row into the lane with g == 0
+  auto merge_l = [&]() {
+#pragma unroll
+    for (int qi = 0; qi < NQ; ++qi) {
+      const float tot = l[qi] + __shfl_xor(l[qi], 32, 64);
+      l[qi] = g == 0 ? tot : 0.0f;
+    }
+  };
+
+  if (nlist > 0) issue(0, 0);
+  for (int i = 0; i < nlist; ++i) {
+    const int s = i & 1;
+    wait_vm<0>();  // this thread's copies of tile i have landed
+    bar();         // everyone's have; everyone is done reading the other stage
+    if (i + 1 < nlist) issue(i + 1, s ^ 1);
+    if (valid && !(use_cache && !light && i < nU)) compute(s);  // a resuming wavefront skips the U blocks
+    if (!light && i == nU - 1) {
+      merge_l();
+      if (kMode == 0 && in_u && valid) {
+#pragma unroll
+        for (int qi = 0; qi < NQ; ++qi) {
+          const int64_t sb = hN + row0 + 32 * qi + r;
+          if (g == 0) {
+            a.cm[sb] = m[qi];
+            a.cl[sb] = l[qi];
+          }
+#pragma unroll
+          for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+            for (int b = 0; b < 4; ++b)
+              *reinterpret_cast<float4*>(a.co + sb * kD + 32 * dt + 8 * b + 4 * g) =
+                  make_float4(ot[qi][dt][4 * b], ot[qi][dt][4 * b + 1], ot[qi][dt][4 * b + 2], ot[qi][dt][4 * b + 3]);
+        }
+      }
     }
   }
-  for (int64_t kb = 0; kb < nkb; ++kb)
-    if (overlaps_c(kb)) process(kb);  // the key blocks overlapping C
 
-  const float inv = 1.0f / l;
+  if (!valid) return;
 #pragma unroll
-  for (int dt = 0; dt < 8; ++dt)
-    *reinterpret_cast<uint2*>(o + hb + row * kD + 16 * dt + 4 * g) =
-        make_uint2(pack_bf16x2(ot[dt][0] * inv, ot[dt][1] * inv), pack_bf16x2(ot[dt][2] * inv, ot[dt][3] * inv));
+  for (int qi = 0; qi < NQ; ++qi) {
+    const int64_t sb = hN + row0 + 32 * qi + r;
+    const float lt = l[qi] + __shfl_xor(l[qi], 32, 64);
+    const float inv = 1.0f / lt;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int b = 0; b < 4; ++b)
+        *reinterpret_cast<uint2*>(a.o + sb * kD + 32 * dt + 8 * b + 4 * g) =
+            make_uint2(pack_bf16_rne(ot[qi][dt][4 * b] * inv, ot[qi][dt][4 * b + 1] * inv),
+                       pack_bf16_rne(ot[qi][dt][4 * b + 2] * inv, ot[qi][dt][4 * b + 3] * inv));
+    if (a.lse != nullptr && g == 0) a.lse[sb] = (m[qi] + __log2f(lt)) * 0.69314718055994531f;
+  }
+}
+
+template <int NQ>
+hipError_t launch_nq(hipStream_t st, AttnArgs a, int64_t heads, int mode) {
+  constexpr int WR = kWaves * 32 * NQ;
+  a.nqb = static_cast<int>((a.N + WR - 1) / WR);
+  a.qbh0 = a.nc > 0 ? a.cb0 * kKB / WR : 0;
+  a.nheavy = a.nc > 0 ? static_cast<int>(((a.cb0 + a.nc) * int64_t(kKB) - 1) / WR) - a.qbh0 + 1 : 0;
+  a.total = static_cast<int>(heads * a.nqb);
+  const dim3 grid(static_cast<unsigned>(a.total)), block(256);
+  if (mode == 0)
+    hipLaunchKernelGGL((facache_attention_kernel<0, NQ>), grid, block, 0, st, a);
+  else if (mode == 1)
+    hipLaunchKernelGGL((facache_attention_kernel<1, NQ>), grid, block, 0, st, a);
+  else
+    hipLaunchKernelGGL((facache_attention_kernel<2, NQ>), grid, block, 0, st, a);
+  return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_facache_attention(hipStream_t st, const uint16_t* q, const uint16_t* k, const uint16_t* v,
-                                    uint16_t* o, float* cm, float* cl, float* co, int64_t heads, int64_t N, int64_t c0,
-                                    int64_t c1, int mode) {
-  const dim3 grid(static_cast<unsigned>(heads * (N / kBlk))), block(256);
-  const float scale_log2 = 1.4426950408889634f / 11.313708498984761f;  // log2(e) / sqrt(128)
-  if (mode == 0)
-    hipLaunchKernelGGL(facache_attention_kernel<0>, grid, block, 0, st, q, k, v, o, cm, cl, co, N, c0, c1, scale_log2);
-  else if (mode == 1)
-    hipLaunchKernelGGL(facache_attention_kernel<1>, grid, block, 0, st, q, k, v, o, cm, cl, co, N, c0, c1, scale_log2);
-  else
-    hipLaunchKernelGGL(facache_attention_kernel<2>, grid, block, 0, st, q, k, v, o, cm, cl, co, N, c0, c1, scale_log2);
-  return hipGetLastError();
+                                    uint16_t* o, float* cm, float* cl, float* co, float* lse, int64_t heads, int64_t N,
+                                    int64_t c0, int64_t c1, int mode) {
+  AttnArgs a{};
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.o = o;
+  a.cm = cm;
+  a.cl = cl;
+  a.co = co;
+  a.lse = lse;
+  a.N = N;
+  a.nkb = static_cast<int>(N / kKB);
+  if (c0 < c1) {
+    a.cb0 = static_cast<int>(c0 / kKB);
+    a.nc = static_cast<int>((c1 + kKB - 1) / kKB) - a.cb0;
+  }
+  a.scale_log2 = 1.4426950408889634f / 11.313708498984761f;  // log2(e) / sqrt(128)
+  return launch_nq<1>(st, a, heads, mode);
 }
 
 }  // namespace lacache

@@ -63,7 +63,7 @@ hipError_t launch_down_skinny(hipStream_t st, const uint8_t* hq, const float* hs
 // First-layer attention with FACache: heads x N x 128 bf16, N % 64 == 0;
 // mode 0 populate, 1 resume, 2 plain (cache pointers unused).
 hipError_t launch_facache_attention(hipStream_t st, const uint16_t* q, const uint16_t* k, const uint16_t* v,
-                                    uint16_t* o, float* cm, float* cl, float* co, int64_t heads, int64_t N, int64_t c0,
-                                    int64_t c1, int mode);
+                                    uint16_t* o, float* cm, float* cl, float* co, float* lse, int64_t heads, int64_t N,
+                                    int64_t c0, int64_t c1, int mode);
 
 }  // namespace lacache

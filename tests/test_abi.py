@@ -118,12 +118,12 @@ def test_addnorm_validation(L):
 
 def test_facache_attention_validation(L):
     f = Fake()
-    q, k, v, o, cm, cl, co = (f() for _ in range(7))
+    q, k, v, o, cm, cl, co, lse = (f() for _ in range(8))
 
     def att(heads=2, N=256, d=128, c0=64, c1=128, mode=0, **over):
-        a = dict(q=q, k=k, v=v, o=o, cm=cm, cl=cl, co=co)
+        a = dict(q=q, k=k, v=v, o=o, lse=None, cm=cm, cl=cl, co=co)
         a.update(over)
-        return L.lacache_facache_attention(None, a["q"], a["k"], a["v"], a["o"], a["cm"], a["cl"], a["co"],
+        return L.lacache_facache_attention(None, a["q"], a["k"], a["v"], a["o"], a["lse"], a["cm"], a["cl"], a["co"],
                                            heads, N, d, c0, c1, mode)
     assert att(d=64) == UNSUP
     assert att(N=200, c1=100) == UNSUP          # N not a multiple of 64
@@ -143,6 +143,10 @@ def test_facache_attention_validation(L):
     assert att(mode=0, cl=k + 64) == INVALID    # cache written over k
     assert att(mode=1, cm=o + 64) == INVALID    # o written over the cache
     assert att(mode=0, co=cm) == INVALID        # two cache outputs alias
+    assert att(lse=lse + 4) == INVALID          # misaligned lse
+    assert att(mode=2, lse=v + 128) == INVALID  # lse written over v
+    assert att(mode=1, lse=cl) == INVALID       # lse written over the cache it reads
+    assert att(mode=0, lse=o + 256) == INVALID  # lse overlaps o
     assert att(heads=0) == OK and att(N=0, c0=0, c1=0) == OK  # nothing launched
 
 

@@ -53,9 +53,10 @@ class Run:
     def set_inputs(self, q, k, v):
         self.q.copy_(_dev(q)), self.k.copy_(_dev(k)), self.v.copy_(_dev(v))
 
-    def __call__(self, c0, c1, mode):
+    def __call__(self, c0, c1, mode, lse=None):
         o = torch.empty_like(self.q)
-        lc.lacache_facache_attention(self.q, self.k, self.v, o, self.cm, self.cl, self.co, c0, c1, mode)
+        lc.lacache_facache_attention(self.q, self.k, self.v, o, lse=lse, cache_m=self.cm, cache_l=self.cl,
+                                     cache_o=self.co, c_begin=c0, c_end=c1, mode=mode)
         torch.cuda.synchronize()
         return o
 
@@ -75,7 +76,8 @@ def _bits_equal(a, b):
     return torch.equal(a.view(torch.int16), b.view(torch.int16))
 
 
-@pytest.mark.parametrize("c0,c1", [(96, 160), (60, 130), (0, 256), (128, 128), (0, 0), (192, 256), (0, 64)])
+@pytest.mark.parametrize("c0,c1", [(96, 160), (60, 130), (0, 256), (128, 128), (0, 0), (100, 100), (192, 256),
+                                   (0, 64), (127, 129)])
 def test_modes_against_oracle_tiny(c0, c1):
     w = synth.ATTN_WORKLOADS["attn_tiny_h2_n256"]
     q, k, v = synth.make_qkv(w, 0)
@@ -192,3 +194,27 @@ def test_deterministic_and_stream_ordered():
         lc.lacache_facache_attention(r.q, r.k, r.v, o, c_begin=w.c_begin, c_end=w.c_end, mode=2, stream=s)
     s.synchronize()
     assert _bits_equal(a, o)
+
+
+def _check_lse(lse, q, k, what):
+    """|L - L_ref| <= max_j 128 u sum_i |q_i k_ji| / sqrt(d) (the fp32 score sums)
+    + 1e-5 (1 + |L_ref|) (exp2, log2 and the sum of l)."""
+    got = lse.cpu().numpy().astype(np.float64)
+    ref = A.attention_lse(q, k)
+    qf, kf = (np.abs(bf16_to_f32(x)).astype(np.float64) for x in (q, k))
+    dot_bound = (qf @ np.swapaxes(kf, -1, -2)).max(axis=-1) * 128 * 2.0 ** -24 / math.sqrt(q.shape[-1])
+    err = np.abs(got - ref)
+    worst = float((err / (dot_bound + 1e-5 * (1 + np.abs(ref)))).max())
+    _say("%s: max |err| %.3e, worst err/bound %.3f" % (what, float(err.max()), worst))
+    assert worst <= 1.0, what
+
+
+@pytest.mark.parametrize("name", ["attn_tiny_h2_n256", "attn_sar512_h32"])
+def test_lse_in_every_mode(name):
+    w = synth.ATTN_WORKLOADS[name]
+    q, k, v = synth.make_qkv(w, 0)
+    r = Run(q, k, v)
+    for mode in (2, 0, 1):
+        lse = torch.full((w.heads, w.N), float("nan"), dtype=torch.float32, device=DEV)
+        r(w.c_begin, w.c_end, mode, lse=lse)
+        _check_lse(lse, q, k, "%s lse mode %d" % (name, mode))
