@@ -1,9 +1,9 @@
 // First-layer FlashAttention with FACache (Sec. 3.3, FACache; Eqs. 2-6).
 //
-// Work decomposition. A workgroup of 4 wavefronts owns 32*NQ query rows per
-// wavefront (128 or 256 rows per workgroup) of one head and streams 64-key
-// tiles of K and V through a two-stage LDS ring filled by direct
-// global->LDS copies, so the copy of tile i+1 overlaps the MFMAs of tile i.
+// Work decomposition. A workgroup of W wavefronts owns 32 query rows per
+// wavefront (32 W rows) of one head and streams 64-key tiles of K and V
+// through an S-stage LDS ring filled by direct global->LDS copies, so the
+// copies of the next S - 1 tiles overlap the MFMAs of the current one.
 // Per tile every wavefront
 //   * computes S^T = K Q^T with bf16 MFMAs 32x32x16 (Q^T stays in registers;
 //     lane (g, r) holds keys 8a + 4g + i of query r, a, i = 0..3);
@@ -43,10 +43,9 @@ typedef __attribute__((address_space(3))) s4 lds_s4;
 
 constexpr int kD = 128;                   // head dimension
 constexpr int kKB = 64;                   // keys per tile = rows per FACache block
-constexpr int kWaves = 4;
+constexpr int kQR = 32;                   // query rows per wavefront
 constexpr int kTileBytes = kKB * kD * 2;  // one K or V tile (16 KiB)
 constexpr int kStageBytes = 2 * kTileBytes;
-constexpr int kStages = 2;
 
 struct AttnArgs {
   const uint16_t* q;
@@ -58,7 +57,7 @@ struct AttnArgs {
   float* co;
   float* lse;
   int64_t N;
-  int nqb;      // query blocks (of 4 * 32 * NQ rows) per head
+  int nqb;      // query blocks (of 32 W rows) per head
   int nkb;      // key blocks (of 64 rows) per head
   int cb0, nc;  // key blocks overlapping C: [cb0, cb0 + nc)
   int qbh0;     // first query block overlapping those key blocks
@@ -82,10 +81,12 @@ __device__ __forceinline__ uint32_t pack_bf16_rne(float lo, float hi) {
   return pack_bf16x2(lo, hi);
 }
 
-template <int kMode, int NQ>  // kMode 0: populate, 1: resume, 2: plain attention
-__global__ __launch_bounds__(256, NQ == 1 ? 2 : 1) void facache_attention_kernel(AttnArgs a) {
-  __shared__ __align__(16) uint8_t smem[kStages * kStageBytes];
-  constexpr int QR = 32 * NQ, WR = kWaves * QR;
+// kMode 0: populate, 1: resume, 2: plain attention; W wavefronts, S stages
+template <int kMode, int W, int S>
+__global__ __launch_bounds__(64 * W, 2) void facache_attention_kernel(AttnArgs a) {
+  __shared__ __align__(16) uint8_t smem[S * kStageBytes];
+  constexpr int QR = kQR, WR = W * QR;
+  constexpr int kPer = 2 * 1024 / (64 * W);  // copies per thread per tile
   const int t = threadIdx.x, lane = t & 63, wave = wave_uniform(t >> 6);
   const int g = lane >> 5, r = lane & 31;
 
@@ -109,44 +110,31 @@ __global__ __launch_bounds__(256, NQ == 1 ? 2 : 1) void facache_attention_kernel
   const uint16_t* kh = a.k + hN * kD;
   const uint16_t* vh = a.v + hN * kD;
 
-  // Q^T operands: query row0 + 32 qi + r, dims 16 kk + 8 g ..
-  bf8 qf[NQ][8];
+  // Q^T operands: query row0 + r, dims 16 kk + 8 g ..
+  const int64_t sb = hN + (valid ? row0 + r : 0);  // this lane's query row (state index)
+  bf8 qf[8];
 #pragma unroll
-  for (int qi = 0; qi < NQ; ++qi) {
-    const int64_t row = valid ? row0 + 32 * qi + r : 0;
-#pragma unroll
-    for (int kk = 0; kk < 8; ++kk) qf[qi][kk] = *reinterpret_cast<const bf8*>(a.q + (hN + row) * kD + 16 * kk + 8 * g);
-  }
+  for (int kk = 0; kk < 8; ++kk) qf[kk] = *reinterpret_cast<const bf8*>(a.q + sb * kD + 16 * kk + 8 * g);
 
-  float m[NQ], l[NQ];
-  v16f ot[NQ][4];  // O~^T: element 4 b + i of tile dt = dim 32 dt + 8 b + 4 g + i of query r
+  float m = -__builtin_inff(), l = 0.0f;
+  v16f ot[4];  // O~^T: element 4 b + i of tile dt = dim 32 dt + 8 b + 4 g + i of query r
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) ot[dt][e] = 0.0f;
   if (use_cache && valid) {
+    m = a.cm[sb];
+    l = g == 0 ? a.cl[sb] : 0.0f;
 #pragma unroll
-    for (int qi = 0; qi < NQ; ++qi) {
-      const int64_t sb = hN + row0 + 32 * qi + r;
-      m[qi] = a.cm[sb];
-      l[qi] = g == 0 ? a.cl[sb] : 0.0f;
+    for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
-      for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-        for (int b = 0; b < 4; ++b) {
-          const float4 c4 = *reinterpret_cast<const float4*>(a.co + sb * kD + 32 * dt + 8 * b + 4 * g);
-          ot[qi][dt][4 * b + 0] = c4.x;
-          ot[qi][dt][4 * b + 1] = c4.y;
-          ot[qi][dt][4 * b + 2] = c4.z;
-          ot[qi][dt][4 * b + 3] = c4.w;
-        }
-    }
-  } else {
-#pragma unroll
-    for (int qi = 0; qi < NQ; ++qi) {
-      m[qi] = -__builtin_inff();
-      l[qi] = 0.0f;
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) ot[qi][dt][e] = 0.0f;
-    }
+      for (int b = 0; b < 4; ++b) {
+        const float4 c4 = *reinterpret_cast<const float4*>(a.co + sb * kD + 32 * dt + 8 * b + 4 * g);
+        ot[dt][4 * b + 0] = c4.x;
+        ot[dt][4 * b + 1] = c4.y;
+        ot[dt][4 * b + 2] = c4.z;
+        ot[dt][4 * b + 3] = c4.w;
+      }
   }
 
   // i-th key block of this workgroup's list
@@ -159,12 +147,12 @@ __global__ __launch_bounds__(256, NQ == 1 ? 2 : 1) void facache_attention_kernel
   // key % 16 (conflict-free 16-byte MFMA operand reads), V by 4 (key % 4)
   // (conflict-free transposing reads).
   const uint32_t smem_u32 = lds_u32(smem);
-  auto issue = [&](int i, int s) {
+  auto issue = [&](int i, int st) {
     const int64_t kr0 = static_cast<int64_t>(key_block(i)) * kKB;
-    const uint32_t kl = smem_u32 + s * kStageBytes, vl = kl + kTileBytes;
+    const uint32_t kl = smem_u32 + st * kStageBytes, vl = kl + kTileBytes;
 #pragma unroll
-    for (int n = 0; n < 4; ++n) {
-      const int p0 = n * 256 + wave * 64, p = p0 + lane;
+    for (int n = 0; n < kPer / 2; ++n) {
+      const int p0 = n * 64 * W + wave * 64, p = p0 + lane;
       const int key = p >> 4, cp = p & 15;
       dma16(kh + (kr0 + key) * kD + 8 * (cp ^ (key & 15)), kl + 16 * p0);
       dma16(vh + (kr0 + key) * kD + 8 * (cp ^ (4 * (key & 3))), vl + 16 * p0);
@@ -179,63 +167,57 @@ __global__ __launch_bounds__(256, NQ == 1 ? 2 : 1) void facache_attention_kernel
   const int v_base = (4 * (G >> 1) + (io >> 2)) * 256 + (2 * (G & 1) + ((io & 3) >> 1)) * 16 + 8 * (io & 1);
   const float c = a.scale_log2;
 
-  auto compute = [&](int s) {
-    const uint8_t* Kt = smem + s * kStageBytes;
+  auto compute = [&](int st) {
+    const uint8_t* Kt = smem + st * kStageBytes;
     const uint8_t* Vt = Kt + kTileBytes;
     // S^T = K Q^T
-    v16f sa[NQ][2];
+    v16f sa[2];
 #pragma unroll
-    for (int qi = 0; qi < NQ; ++qi)
+    for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
-      for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) sa[qi][tt][e] = 0.0f;
+      for (int e = 0; e < 16; ++e) sa[tt][e] = 0.0f;
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
       for (int kk = 0; kk < 8; ++kk) {
         const int key = 32 * tt + r;
         const bf8 kf = *reinterpret_cast<const bf8*>(Kt + key * 256 + (((2 * kk + g) ^ (key & 15)) << 4));
-#pragma unroll
-        for (int qi = 0; qi < NQ; ++qi) sa[qi][tt] = mfma32(kf, qf[qi][kk], sa[qi][tt]);
+        sa[tt] = mfma32(kf, qf[kk], sa[tt]);
       }
     // online softmax (Eqs. 2-5) and the P^T operands
-    bf8 pb[NQ][4];
+    float mx = sa[0][0];
 #pragma unroll
-    for (int qi = 0; qi < NQ; ++qi) {
-      float mx = sa[qi][0][0];
+    for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
-      for (int tt = 0; tt < 2; ++tt)
+      for (int e = 0; e < 16; ++e) mx = __builtin_fmaxf(mx, sa[tt][e]);
+    mx = __builtin_fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float mn = __builtin_fmaxf(m, mx * c);         // Eq. 2
+    const float alpha = __builtin_amdgcn_exp2f(m - mn);  // Eq. 3
+    m = mn;
+    float ps = 0.0f;
 #pragma unroll
-        for (int e = 0; e < 16; ++e) mx = __builtin_fmaxf(mx, sa[qi][tt][e]);
-      mx = __builtin_fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float mn = __builtin_fmaxf(m[qi], mx * c);         // Eq. 2
-      const float alpha = __builtin_amdgcn_exp2f(m[qi] - mn);  // Eq. 3
-      m[qi] = mn;
-      float ps = 0.0f;
+    for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
-      for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sa[qi][tt][e], c, -mn));  // Eq. 4
-          sa[qi][tt][e] = p;
-          ps += p;
-        }
-      l[qi] = alpha * l[qi] + ps;  // Eq. 5 (this lane's keys)
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) ot[qi][dt][e] *= alpha;
-      // step ks covers keys 16 ks .. 16 ks + 15: elements 8 (ks % 2) .. + 7 of S^T tile ks / 2
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const int tt = ks >> 1, e0 = 8 * (ks & 1);
-        const uint4 w4 = make_uint4(pack_bf16_rne(sa[qi][tt][e0 + 0], sa[qi][tt][e0 + 1]),
-                                    pack_bf16_rne(sa[qi][tt][e0 + 2], sa[qi][tt][e0 + 3]),
-                                    pack_bf16_rne(sa[qi][tt][e0 + 4], sa[qi][tt][e0 + 5]),
-                                    pack_bf16_rne(sa[qi][tt][e0 + 6], sa[qi][tt][e0 + 7]));
-        pb[qi][ks] = __builtin_bit_cast(bf8, w4);
+      for (int e = 0; e < 16; ++e) {
+        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sa[tt][e], c, -mn));  // Eq. 4
+        sa[tt][e] = p;
+        ps += p;
       }
+    l = alpha * l + ps;  // Eq. 5 (this lane's keys)
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) ot[dt][e] *= alpha;
+    // step ks covers keys 16 ks .. 16 ks + 15: elements 8 (ks % 2) .. + 7 of S^T tile ks / 2
+    bf8 pb[4];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const int tt = ks >> 1, e0 = 8 * (ks & 1);
+      const uint4 w4 = make_uint4(pack_bf16_rne(sa[tt][e0 + 0], sa[tt][e0 + 1]),
+                                  pack_bf16_rne(sa[tt][e0 + 2], sa[tt][e0 + 3]),
+                                  pack_bf16_rne(sa[tt][e0 + 4], sa[tt][e0 + 5]),
+                                  pack_bf16_rne(sa[tt][e0 + 6], sa[tt][e0 + 7]));
+      pb[ks] = __builtin_bit_cast(bf8, w4);
     }
     // O~^T += V^T P^T (Eq. 6)
 #pragma unroll
@@ -244,80 +226,73 @@ __global__ __launch_bounds__(256, NQ == 1 ? 2 : 1) void facache_attention_kernel
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
         const bf8 vf = read_tr2(vd + (16 * ks) * 256, vd + (16 * ks + 8) * 256);
-#pragma unroll
-        for (int qi = 0; qi < NQ; ++qi) ot[qi][dt] = mfma32(vf, pb[qi][ks], ot[qi][dt]);
+        ot[dt] = mfma32(vf, pb[ks], ot[dt]);
       }
     }
   };
 
   // merge the two partial sums of a row into the lane with g == 0
   auto merge_l = [&]() {
-#pragma unroll
-    for (int qi = 0; qi < NQ; ++qi) {
-      const float tot = l[qi] + __shfl_xor(l[qi], 32, 64);
-      l[qi] = g == 0 ? tot : 0.0f;
-    }
+    const float tot = l + __shfl_xor(l, 32, 64);
+    l = g == 0 ? tot : 0.0f;
   };
 
-  if (nlist > 0) issue(0, 0);
+#pragma unroll
+  for (int i = 0; i < S - 1; ++i)
+    if (i < nlist) issue(i, i);
   for (int i = 0; i < nlist; ++i) {
-    const int s = i & 1;
-    wait_vm<0>();  // this thread's copies of tile i have landed
-    bar();         // everyone's have; everyone is done reading the other stage
-    if (i + 1 < nlist) issue(i + 1, s ^ 1);
-    if (valid && !(use_cache && !light && i < nU)) compute(s);  // a resuming wavefront skips the U blocks
+    // this thread's copies of tile i have landed (those of the next S - 2 may be in flight) ...
+    if (i + S - 2 < nlist)
+      wait_vm<(S - 2) * kPer>();
+    else
+      wait_vm<0>();
+    bar();  // ... and everyone's have; everyone is done reading the stage refilled next
+    if (i + S - 1 < nlist) issue(i + S - 1, (i + S - 1) % S);
+    if (valid && !(use_cache && !light && i < nU)) compute(i % S);  // a resuming wavefront skips the U blocks
     if (!light && i == nU - 1) {
       merge_l();
       if (kMode == 0 && in_u && valid) {
-#pragma unroll
-        for (int qi = 0; qi < NQ; ++qi) {
-          const int64_t sb = hN + row0 + 32 * qi + r;
-          if (g == 0) {
-            a.cm[sb] = m[qi];
-            a.cl[sb] = l[qi];
-          }
-#pragma unroll
-          for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-            for (int b = 0; b < 4; ++b)
-              *reinterpret_cast<float4*>(a.co + sb * kD + 32 * dt + 8 * b + 4 * g) =
-                  make_float4(ot[qi][dt][4 * b], ot[qi][dt][4 * b + 1], ot[qi][dt][4 * b + 2], ot[qi][dt][4 * b + 3]);
+        if (g == 0) {
+          a.cm[sb] = m;
+          a.cl[sb] = l;
         }
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+          for (int b = 0; b < 4; ++b)
+            *reinterpret_cast<float4*>(a.co + sb * kD + 32 * dt + 8 * b + 4 * g) =
+                make_float4(ot[dt][4 * b], ot[dt][4 * b + 1], ot[dt][4 * b + 2], ot[dt][4 * b + 3]);
       }
     }
   }
 
   if (!valid) return;
+  const float lt = l + __shfl_xor(l, 32, 64);
+  const float inv = 1.0f / lt;
 #pragma unroll
-  for (int qi = 0; qi < NQ; ++qi) {
-    const int64_t sb = hN + row0 + 32 * qi + r;
-    const float lt = l[qi] + __shfl_xor(l[qi], 32, 64);
-    const float inv = 1.0f / lt;
+  for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-      for (int b = 0; b < 4; ++b)
-        *reinterpret_cast<uint2*>(a.o + sb * kD + 32 * dt + 8 * b + 4 * g) =
-            make_uint2(pack_bf16_rne(ot[qi][dt][4 * b] * inv, ot[qi][dt][4 * b + 1] * inv),
-                       pack_bf16_rne(ot[qi][dt][4 * b + 2] * inv, ot[qi][dt][4 * b + 3] * inv));
-    if (a.lse != nullptr && g == 0) a.lse[sb] = (m[qi] + __log2f(lt)) * 0.69314718055994531f;
-  }
+    for (int b = 0; b < 4; ++b)
+      *reinterpret_cast<uint2*>(a.o + sb * kD + 32 * dt + 8 * b + 4 * g) =
+          make_uint2(pack_bf16_rne(ot[dt][4 * b] * inv, ot[dt][4 * b + 1] * inv),
+                     pack_bf16_rne(ot[dt][4 * b + 2] * inv, ot[dt][4 * b + 3] * inv));
+  if (a.lse != nullptr && g == 0) a.lse[sb] = (m + __log2f(lt)) * 0.69314718055994531f;
 }
 
-template <int NQ>
-hipError_t launch_nq(hipStream_t st, AttnArgs a, int64_t heads, int mode) {
-  constexpr int WR = kWaves * 32 * NQ;
+template <int W, int S>
+hipError_t launch_ws(hipStream_t st, AttnArgs a, int64_t heads, int mode) {
+  constexpr int WR = W * kQR;
   a.nqb = static_cast<int>((a.N + WR - 1) / WR);
   a.qbh0 = a.nc > 0 ? a.cb0 * kKB / WR : 0;
   a.nheavy = a.nc > 0 ? static_cast<int>(((a.cb0 + a.nc) * int64_t(kKB) - 1) / WR) - a.qbh0 + 1 : 0;
   a.total = static_cast<int>(heads * a.nqb);
-  const dim3 grid(static_cast<unsigned>(a.total)), block(256);
+  const dim3 grid(static_cast<unsigned>(a.total)), block(64 * W);
   if (mode == 0)
-    hipLaunchKernelGGL((facache_attention_kernel<0, NQ>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((facache_attention_kernel<0, W, S>), grid, block, 0, st, a);
   else if (mode == 1)
-    hipLaunchKernelGGL((facache_attention_kernel<1, NQ>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((facache_attention_kernel<1, W, S>), grid, block, 0, st, a);
   else
-    hipLaunchKernelGGL((facache_attention_kernel<2, NQ>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((facache_attention_kernel<2, W, S>), grid, block, 0, st, a);
   return hipGetLastError();
 }
 
@@ -342,7 +317,7 @@ hipError_t launch_facache_attention(hipStream_t st, const uint16_t* q, const uin
     a.nc = static_cast<int>((c1 + kKB - 1) / kKB) - a.cb0;
   }
   a.scale_log2 = 1.4426950408889634f / 11.313708498984761f;  // log2(e) / sqrt(128)
-  return launch_nq<1>(st, a, heads, mode);
+  return launch_ws<4, 2>(st, a, heads, mode);
 }
 
 }  // namespace lacache
