@@ -77,8 +77,11 @@ __device__ __forceinline__ bf8 read_tr2(const uint8_t* p0, const uint8_t* p1) {
   return __builtin_bit_cast(bf8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
+// two fp32 -> bf16 (round to nearest even) in one v_cvt_pk_bf16_f32
+typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t pack_bf16_rne(float lo, float hi) {
-  return pack_bf16x2(lo, hi);
+  const bf2 v = {static_cast<__bf16>(lo), static_cast<__bf16>(hi)};
+  return __builtin_bit_cast(uint32_t, v);
 }
 
 // kMode 0: populate, 1: resume, 2: plain attention; W wavefronts, S stages
@@ -176,10 +179,11 @@ __global__ __launch_bounds__(64 * W, 2) void facache_attention_kernel(AttnArgs a
     for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
       for (int e = 0; e < 16; ++e) sa[tt][e] = 0.0f;
+    // the two key tiles alternate, so consecutive MFMAs are independent
 #pragma unroll
-    for (int tt = 0; tt < 2; ++tt)
+    for (int kk = 0; kk < 8; ++kk)
 #pragma unroll
-      for (int kk = 0; kk < 8; ++kk) {
+      for (int tt = 0; tt < 2; ++tt) {
         const int key = 32 * tt + r;
         const bf8 kf = *reinterpret_cast<const bf8*>(Kt + key * 256 + (((2 * kk + g) ^ (key & 15)) << 4));
         sa[tt] = mfma32(kf, qf[kk], sa[tt]);
@@ -220,15 +224,15 @@ __global__ __launch_bounds__(64 * W, 2) void facache_attention_kernel(AttnArgs a
       pb[ks] = __builtin_bit_cast(bf8, w4);
     }
     // O~^T += V^T P^T (Eq. 6)
+    // the four dimension tiles alternate, so consecutive MFMAs are independent
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt) {
-      const uint8_t* vd = Vt + v_base + 64 * (dt ^ e_sw);
+    for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
+      for (int dt = 0; dt < 4; ++dt) {
+        const uint8_t* vd = Vt + v_base + 64 * (dt ^ e_sw);
         const bf8 vf = read_tr2(vd + (16 * ks) * 256, vd + (16 * ks + 8) * 256);
         ot[dt] = mfma32(vf, pb[ks], ot[dt]);
       }
-    }
   };
 
   // merge the two partial sums of a row into the lane with g == 0
