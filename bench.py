@@ -51,7 +51,8 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=50)
     p.add_argument("--warmup", type=int, default=10)
-    p.add_argument("--workload", default="block32_h4096_i12288")
+    p.add_argument("--workload", default="block32_h4096_i12288",
+                   help="an FFN workload, or an attention workload (attn_*): the first-layer FACache attention")
     p.add_argument("--weight-sets", type=int, default=4)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--eager", action="store_true",
@@ -173,6 +174,9 @@ def main():
     import paper_2607_16339_amd as lc
     import synth
 
+    if args.workload.startswith("attn_"):
+        attention_main(args)
+        return
     w = synth.WORKLOADS[args.workload]
     M, H, I = w.M, w.H, w.I
     dev = torch.device("cuda:0")
@@ -413,6 +417,150 @@ def cpu_baseline(w, sets, out, dev):
             "sample": "%d calls of %d of %d rows (one layer each; the FFN is row-independent): %.2f s"
                       % (calls, rows, w.M, t),
             "tokens_per_s": round(rows * calls / t, 3)}
+
+
+PEAK_BF16_TFLOPS = 2500.0  # dense bf16 MFMA
+
+
+def attention_flop_bytes(w, mode):
+    """Algorithmic FLOPs and HBM bytes of one FACache attention call. Plain
+    and populate: every query row against every key (4 N^2 d per head: the
+    score and the P V products). Resume: the rows of the 64-row query blocks
+    inside U against the keys of the key blocks overlapping C only, the other
+    rows against every key; their cached state (m, l, O~ in fp32) is read
+    instead. Bytes: q, k, v read and o written once (bf16), plus the cache
+    written (populate) or read (resume)."""
+    N, d, B = w.N, w.d, 64
+    cb0 = w.c_begin // B
+    nc = (w.c_end + B - 1) // B - cb0 if w.c_begin < w.c_end else 0
+    rows_u = N - nc * B
+    if mode == 1:
+        pairs = rows_u * nc * B + nc * B * N
+    else:
+        pairs = N * N
+    flop = 4.0 * d * pairs * w.heads
+    io = 4 * w.heads * N * d * 2
+    cache = w.heads * rows_u * (2 + d) * 4 if mode in (0, 1) else 0
+    return flop, io + cache
+
+
+def attention_main(args):
+    """One line for the first-layer FACache attention: a step is one resume
+    call (a later denoising step of a SAR block, the FACache hot path); the
+    plain and populate calls are timed beside it."""
+    import numpy as np
+    import torch
+
+    import paper_2607_16339_amd as lc
+    import synth
+
+    w = synth.ATTN_WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    lc.lib()
+
+    def dev_bf16(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16).copy()).view(torch.bfloat16).to(dev)
+
+    q0, k0, v0 = (dev_bf16(a) for a in synth.make_qkv(w, step=0))
+    q1, k1, v1 = (dev_bf16(a) for a in synth.make_qkv(w, step=1))
+    o = torch.empty_like(q0)
+    cm = torch.empty((w.heads, w.N), dtype=torch.float32, device=dev)
+    cl = torch.empty_like(cm)
+    co = torch.empty((w.heads, w.N, w.d), dtype=torch.float32, device=dev)
+
+    def call(mode, q, k, v):
+        lc.lacache_facache_attention(q, k, v, o, cache_m=cm, cache_l=cl, cache_o=co, c_begin=w.c_begin,
+                                     c_end=w.c_end, mode=mode)
+
+    # populate on step 0, then resume on step 1 (rows of C redrawn) must equal plain on step 1
+    call(0, q0, k0, v0)
+    call(1, q1, k1, v1)
+    torch.cuda.synchronize()
+    got = o.clone()
+    call(2, q1, k1, v1)
+    torch.cuda.synchronize()
+    if not torch.equal(got.view(torch.int16), o.view(torch.int16)):
+        raise RuntimeError("resume on a later step differs from plain attention of its inputs")
+
+    stream = torch.cuda.current_stream()
+    reps = max(min(args.steps, 64), 8)
+
+    def time_mode(mode, q, k, v):
+        for _ in range(args.warmup):
+            call(mode, q, k, v)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(reps):
+                call(mode, q, k, v)
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        nrep = 3
+        e0.record(stream)
+        for _ in range(nrep):
+            g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        del g
+        return e0.elapsed_time(e1) / (nrep * reps)
+
+    ms = {"plain": time_mode(2, q1, k1, v1), "populate": time_mode(0, q0, k0, v0)}
+    call(0, q0, k0, v0)  # the cache of step 0, then resume steps on step 1's inputs
+    ms["resume"] = time_mode(1, q1, k1, v1)
+
+    fl = {m: attention_flop_bytes(w, i)[0] for m, i in (("plain", 2), ("populate", 0), ("resume", 1))}
+    by = {m: attention_flop_bytes(w, i)[1] for m, i in (("plain", 2), ("populate", 0), ("resume", 1))}
+    tf = {m: fl[m] / (ms[m] * 1e-3) / 1e12 for m in ms}
+    # the step's kernel is the resume call: about 40 FLOP per algorithmic byte,
+    # far below the bf16 ridge (2500 / 8 = 312), so it is bound by HBM; the
+    # plain call (2 N d FLOP per byte) is bound by the MFMA rate
+    gbs = by["resume"] / (ms["resume"] * 1e-3) / 1e9
+    roof = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+            "frac": round(gbs / PEAK_HBM_GBPS, 4), "traffic": None,
+            "kernel": "facache_attention_kernel<1> (resume)", "kernel_ms": round(ms["resume"], 5),
+            "algorithmic_bytes": by["resume"]}
+    roof_plain = {"bound": "mfma", "achieved": round(tf["plain"], 1), "peak": PEAK_BF16_TFLOPS,
+                  "unit": "TFLOP/s", "frac": round(tf["plain"] / PEAK_BF16_TFLOPS, 4),
+                  "kernel": "facache_attention_kernel<2> (plain)", "kernel_ms": round(ms["plain"], 5),
+                  "algorithmic_flop": fl["plain"]}
+    line = {
+        "metric": "FACache first-layer attention, resume step: tokens/s (bf16, d=128)",
+        "value": round(w.heads * w.N / (ms["resume"] * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": reps, "warmup": args.warmup, "ms_per_step": round(ms["resume"], 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16 (fp32 accumulate)", "data": "synthetic",
+        "config": {"workload": w.name, "heads": w.heads, "N": w.N, "d": w.d, "c_begin": w.c_begin,
+                   "c_end": w.c_end},
+        "ms": {k: round(v, 5) for k, v in ms.items()},
+        "tflops_algorithmic": {k: round(v, 1) for k, v in tf.items()},
+        "hbm_GBps_algorithmic": {k: round(by[k] / (ms[k] * 1e-3) / 1e9, 1) for k in ms},
+        "resume_speedup_vs_plain": round(ms["plain"] / ms["resume"], 3),
+        "timing": "HIP graph of %d back-to-back calls per mode, 3 replays" % reps,
+        "roofline": roof, "roofline_plain": roof_plain,
+    }
+    if not args.no_cpu_baseline and not args.profile_only:
+        import oracle.attention as A
+        bits = synth.make_qkv(w, step=1, heads=[0])
+        t0 = time.perf_counter()
+        n = 0
+        while time.perf_counter() - t0 < 10.0 and n < 64:
+            A.attention(*bits)
+            n += 1
+        t = time.perf_counter() - t0
+        line["cpu_baseline"] = {"value": round(n * w.N / t, 3), "unit": "tokens/s", "cores": _threads(),
+                                "kind": "oracle",
+                                "sample": "%d plain attention calls of head 0 (%d x %d, fp64): %.2f s"
+                                          % (n, w.N, w.d, t)}
+    print(json.dumps(line), flush=True)
+
+
+def _threads():
+    try:
+        from threadpoolctl import threadpool_info
+        return max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # noqa: BLE001
+        return os.cpu_count() or 1
 
 
 if __name__ == "__main__":
