@@ -169,6 +169,9 @@ __device__ __forceinline__ void wait_vm_lds() {
   static_assert(N >= 0 && N < 64, "vmcnt field");
   __builtin_amdgcn_s_waitcnt(0x0070 | (N & 15) | ((N >> 4) << 14));
 }
+// s_waitcnt lgkmcnt(0): this wave's LDS accesses are done (copies in flight
+// are not waited for).
+__device__ __forceinline__ void wait_lds() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 // Workgroup barrier without a memory fence (a fence would drain the copies in
 // flight); the empty asm statements keep LDS accesses from moving across it.
 __device__ __forceinline__ void bar() {
