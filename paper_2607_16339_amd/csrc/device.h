@@ -75,6 +75,33 @@ __device__ __forceinline__ bool enc8_div_fast(const float (&y)[8], float rs, uin
 }
 __device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
 
+// The bracket of enc1_div_fast with the factors folded into the reciprocal:
+// rl = RN32(rcp(s) (1 - 2^-20)), rh = RN32(rcp(s) (1 + 2^-20)). For a group
+// with amax = max|y| and s = RN32(amax / 448) >= 2^-100, and rcp within 2^-22
+// of 1/s, every y of the group has
+//   |y rl| < |RN32(y / s)| < |y rh|  (y != 0; both products have its sign),
+// since (1 - 2^-20) (1 + 2^-22) (1 + 2^-24)^2 < 1 - 2^-21 < 1 - 2^-24, and
+// likewise above; and |y rh| < 448 (1 + 2^-19) < 464, below the conversion's
+// NaN threshold, so no clip is needed. Where the codes of y rl and y rh agree,
+// that is E(RN32(y / s)) (the encoder is monotone).
+struct FastQuant {
+  float rl, rh;
+};
+__device__ __forceinline__ FastQuant fast_quant(float s) {
+  const float rs = __builtin_amdgcn_rcpf(s);
+  return {rs * (1.0f - 0x1p-20f), rs * (1.0f + 0x1p-20f)};
+}
+// Codes of four values by the bracket: returns the codes from y rl in lo and
+// whether they equal the codes from y rh.
+__device__ __forceinline__ bool enc4_bracket(float a, float b, float c, float d, FastQuant f, uint32_t& lo) {
+  int w0 = __builtin_amdgcn_cvt_pk_fp8_f32(a * f.rl, b * f.rl, 0, false);
+  w0 = __builtin_amdgcn_cvt_pk_fp8_f32(c * f.rl, d * f.rl, w0, true);
+  int w1 = __builtin_amdgcn_cvt_pk_fp8_f32(a * f.rh, b * f.rh, 0, false);
+  w1 = __builtin_amdgcn_cvt_pk_fp8_f32(c * f.rh, d * f.rh, w1, true);
+  lo = static_cast<uint32_t>(w0);
+  return w0 == w1;
+}
+
 // SiLU(g) * u in fp32 with the hardware exp2 and reciprocal (a few ulp).
 __device__ __forceinline__ float swiglu_fast(float g, float u) {
   const float e = __builtin_amdgcn_exp2f(-g * 1.44269504088896341f);
@@ -152,6 +179,17 @@ __device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
 // 4 bytes per lane global -> LDS: lane l lands at lds + 4 l.
 __device__ __forceinline__ void dma4(const void* g, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+}
+// The same with a wave-uniform 64-bit base in SGPRs and a 32-bit per-lane
+// byte offset (the global instructions' scalar-base form): no 64-bit address
+// arithmetic per lane.
+__device__ __forceinline__ void dma16s(const void* sbase, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase), "s"(lds)
+               : "memory", "m0");
+}
+__device__ __forceinline__ void dma4s(const void* sbase, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1" ::"v"(voff), "s"(sbase), "s"(lds)
+               : "memory", "m0");
 }
 #pragma clang diagnostic pop
 

@@ -147,7 +147,7 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
   const uint8_t* b_base = bq;
   const uint8_t* b_base_hi = bq;
   const float* s_base = as;  // scales: base of this wave's source (wave-uniform) ...
-  uint32_t s_off = 0;        // ... this lane's offset in floats
+  uint32_t s_off = 0;        // ... this lane's byte offset
   int64_t s_step = 0;        // ... and the stride per K-group
   uint32_t a_off[kAInst], b_off[kBInst];
   auto enter = [&](int w) {
@@ -177,7 +177,7 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
     if (xs_wave) {
       const int row = wave * 64 + lane;
       s_base = as + it.m0;
-      s_off = static_cast<uint32_t>(row < alim ? row : alim);
+      s_off = static_cast<uint32_t>(row < alim ? row : alim) * 4u;
       s_step = M;
     } else {
       // gate/up: {gate block, up block}; down: {block of columns n0.., the next
@@ -185,22 +185,22 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
       const int r0 = kGateUp ? it.col : n0 / 128;
       const int r1 = kGateUp ? static_cast<int>(I / 128) + it.col : (n0 + 128 < N ? n0 / 128 + 1 : r0);
       s_base = bs;
-      s_off = static_cast<uint32_t>((lane == 0 ? r0 : r1) * KB);
+      s_off = static_cast<uint32_t>((lane == 0 ? r0 : r1) * KB) * 4u;
       s_step = 1;
     }
   };
   // Copies of K-group kb of the cursor's item into stage dst (asynchronous).
   auto issue_group = [&](int kb, Stage<BM>* dst) {
-    const int64_t ko = kb * 128;
+    const int64_t ko = static_cast<int64_t>(kb) * 128;
     const int la = static_cast<int>(lds_u32(dst->a)), lb = static_cast<int>(lds_u32(dst->b));
 #pragma unroll
-    for (int u = 0; u < kAInst; ++u) dma16(a_base + ko + a_off[u], wave_uniform(la + (wave * kAInst + u) * 1024));
+    for (int u = 0; u < kAInst; ++u) dma16s(a_base + ko, a_off[u], wave_uniform(la + (wave * kAInst + u) * 1024));
 #pragma unroll
     for (int u = 0; u < kBInst; ++u) {
       const uint8_t* base = (kGateUp && (wave * kBInst + u) * 8 >= 128) ? b_base_hi : b_base;
-      dma16(base + ko + b_off[u], wave_uniform(lb + (wave * kBInst + u) * 1024));
+      dma16s(base + ko, b_off[u], wave_uniform(lb + (wave * kBInst + u) * 1024));
     }
-    dma4(s_base + kb * s_step + s_off, wave_uniform(static_cast<int>(lds_u32(dst->xs)) + xs_dst * 4));
+    dma4s(s_base + kb * s_step, s_off, wave_uniform(static_cast<int>(lds_u32(dst->xs)) + xs_dst * 4));
   };
   // The next K-group in the workgroup's sequence. Past the last one the last
   // group is copied again into the idle stage (never read), so every step
@@ -326,26 +326,17 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
 #pragma unroll
         for (int c = 1; c < NCW; ++c) amax = __builtin_fmaxf(amax, sRed[c][row]);
         const float s = amax / kE4M3Max;
-        const float rs = fast_rcp(s);
+        const FastQuant fq = fast_quant(s);
         const bool fast = scale_is_fast(s);
         const bool ok = grow < M;
 #pragma unroll
         for (int j = 0; j < NJ / 2; ++j) {
-          // codes of q0 (1 -+ 2^-20), q0 = h rs: where every pair agrees they
-          // are E(RN32(h / s)) (see enc1_div_fast); else the division decides
-          float lo[4], hi[4];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float q0 = acc[i][j][r] * rs;
-            const float d = __builtin_fabsf(q0) * 0x1p-20f;
-            lo[r] = q0 - d;
-            hi[r] = q0 + d;
-          }
-          uint32_t code = enc4_e4m3(lo[0], lo[1], lo[2], lo[3]);
-          const uint32_t code2 = enc4_e4m3(hi[0], hi[1], hi[2], hi[3]);
+          // E(RN32(h / s)) by the bracket where it decides, else by the division
+          uint32_t code;
+          const bool agree = enc4_bracket(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3], fq, code);
           if (s == 0.0f)
             code = 0u;
-          else if (!(fast && code == code2))
+          else if (!(fast && agree))
             code = enc4_e4m3(qdiv(acc[i][j][0], s), qdiv(acc[i][j][1], s), qdiv(acc[i][j][2], s),
                              qdiv(acc[i][j][3], s));
           const int64_t col = static_cast<int64_t>(it.col) * 128 + (WC / 2) * wn + 16 * j + 4 * q;
