@@ -56,13 +56,14 @@ __device__ __forceinline__ v8i load_frag(const uint8_t* tile, int row, int q) {
   return f;
 }
 
-// One LDS stage: A tile, B tile, BM activation scales, then the two
-// weight-block scales of the K-group (slots BM and BM + 1 of a 64-slot spare).
+// One LDS stage: A tile, B tile, BM activation scales, the two weight-block
+// scales of the K-group (slots BM and BM + 1 of a 64-slot region written by
+// one copy instruction), and 64 spare slots for duplicate scale copies.
 template <int BM>
 struct Stage {
   uint8_t a[BM * 128];
   uint8_t b[BNR * 128];
-  alignas(16) float xs[BM + 64];
+  alignas(16) float xs[BM + 128];
 };
 
 // A work item: output tile (row tile, column tile) and its K range.
@@ -128,27 +129,33 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
   const int C = static_cast<int>(kGateUp ? I / 128 : (N + BNR - 1) / BNR);
   const int G = static_cast<int>(gridDim.x);
 
-  // ---- direct-to-LDS copy plan. A wave's load instruction fills 64
-  // consecutive 16-byte LDS slots (8 tile rows); lane l fills slot l, i.e.
-  // row 8g + l/8, physical chunk l%8, so it fetches logical chunk
-  // (l%8) ^ swz(row) of that row. Rows past M (or N) fetch a clamped row;
-  // their results are never stored. Activation scales: waves 0..BM/64-1 copy
-  // rows 64w..64w+63 (one float per lane); the other waves copy the two
+  // ---- direct-to-LDS copy plan. Only the first kCopyWaves wavefronts (one
+  // per SIMD) copy: a wavefront stalls while the memory pipeline takes its
+  // copy instructions, and the other wavefront of its SIMD keeps the matrix
+  // core busy meanwhile (all eight copying at once left it idle). A copy
+  // instruction fills 64 consecutive 16-byte LDS slots (8 tile rows); lane l
+  // fills slot l, i.e. row 8g + l/8, physical chunk l%8, so it fetches logical
+  // chunk (l%8) ^ swz(row) of that row. Rows past M (or N) fetch a clamped
+  // row; their results are never stored. Scales: each copy wavefront copies
+  // the activation scales of rows 64 (w mod BM/64) .. + 63 (one float per
+  // lane; copies beyond the first go to the spare slots) and the two
   // weight-block scales (lane 0 the first block, the others the second).
-  constexpr int kAInst = BM / 8 / NW;  // per wave
-  constexpr int kBInst = BNR / 8 / NW;
-  constexpr int kPer = kAInst + kBInst + 1;  // copies per wave per K-group
-  const bool xs_wave = wave < BM / 64;
-  const int xs_dst = xs_wave ? wave * 64 : BM;
+  constexpr int kCopyWaves = 4;
+  constexpr int kAInst = BM / 8 / kCopyWaves;  // per copy wavefront
+  constexpr int kBInst = BNR / 8 / kCopyWaves;
+  constexpr int kPer = kAInst + kBInst + 2;  // copies per copy wavefront per K-group
+  const bool copy_wave = wave < kCopyWaves;
+  const int xband = wave % (BM / 64);
+  const int xs_dst = wave < BM / 64 ? wave * 64 : BM + 64;
 
   // issue cursor: the item whose K-groups are being copied
   int iw = blockIdx.x, ikb = 0, ikb1 = 0;
   const uint8_t* a_base = aq;
   const uint8_t* b_base = bq;
   const uint8_t* b_base_hi = bq;
-  const float* s_base = as;  // scales: base of this wave's source (wave-uniform) ...
-  uint32_t s_off = 0;        // ... this lane's byte offset
-  int64_t s_step = 0;        // ... and the stride per K-group
+  const float* x_base = as;  // activation scales of the tile's rows (wave-uniform)
+  uint32_t x_off = 0;        // ... this lane's byte offset (stride M floats per K-group)
+  uint32_t w_off = 0;        // this lane's weight-block scale row, as a byte offset into bs
   uint32_t a_off[kAInst], b_off[kBInst];
   auto enter = [&](int w) {
     const Item it = item_at(w, R, C, KS, KB, BM);
@@ -174,23 +181,20 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
       const int r = row < blim ? row : blim;
       b_off[u] = static_cast<uint32_t>(r) * static_cast<uint32_t>(K) + ((lane & 7) ^ swz(row)) * 16;
     }
-    if (xs_wave) {
-      const int row = wave * 64 + lane;
-      s_base = as + it.m0;
-      s_off = static_cast<uint32_t>(row < alim ? row : alim) * 4u;
-      s_step = M;
-    } else {
+    {
+      const int row = xband * 64 + lane;
+      x_base = as + it.m0;
+      x_off = static_cast<uint32_t>(row < alim ? row : alim) * 4u;
       // gate/up: {gate block, up block}; down: {block of columns n0.., the next
       // one (or the same past N)}
       const int r0 = kGateUp ? it.col : n0 / 128;
       const int r1 = kGateUp ? static_cast<int>(I / 128) + it.col : (n0 + 128 < N ? n0 / 128 + 1 : r0);
-      s_base = bs;
-      s_off = static_cast<uint32_t>((lane == 0 ? r0 : r1) * KB) * 4u;
-      s_step = 1;
+      w_off = static_cast<uint32_t>((lane == 0 ? r0 : r1) * KB) * 4u;
     }
   };
   // Copies of K-group kb of the cursor's item into stage dst (asynchronous).
   auto issue_group = [&](int kb, Stage<BM>* dst) {
+    if (!copy_wave) return;
     const int64_t ko = static_cast<int64_t>(kb) * 128;
     const int la = static_cast<int>(lds_u32(dst->a)), lb = static_cast<int>(lds_u32(dst->b));
 #pragma unroll
@@ -200,7 +204,9 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
       const uint8_t* base = (kGateUp && (wave * kBInst + u) * 8 >= 128) ? b_base_hi : b_base;
       dma16s(base + ko, b_off[u], wave_uniform(lb + (wave * kBInst + u) * 1024));
     }
-    dma4s(s_base + kb * s_step, s_off, wave_uniform(static_cast<int>(lds_u32(dst->xs)) + xs_dst * 4));
+    const int lx = static_cast<int>(lds_u32(dst->xs));
+    dma4s(x_base + static_cast<int64_t>(kb) * M, x_off, wave_uniform(lx + xs_dst * 4));
+    dma4s(bs + kb, w_off, wave_uniform(lx + BM * 4));
   };
   // The next K-group in the workgroup's sequence. Past the last one the last
   // group is copied again into the idle stage (never read), so every step
@@ -281,10 +287,13 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
         for (int r = 0; r < 4; ++r) acc[i][j][r] = 0.0f;
 
     for (int kb = it.kb0; kb < it.kb1; ++kb) {
-      // this wave's copies of the group have landed (later ones may still fly;
-      // loads retire in issue order, so epilogue stores in between only make
-      // the wait longer) ...
-      wait_vm_lds<(S - 2) * kPer>();
+      // a copy wave's copies of the group have landed (later ones may still
+      // fly; loads retire in issue order, so epilogue stores in between only
+      // make the wait longer) ...
+      if (copy_wave)
+        wait_vm_lds<(S - 2) * kPer>();
+      else
+        wait_lds();
       bar();  // ... and every wave's; and the stage of the previous group is read by no one
       issue_next(&stg[cur == 0 ? S - 1 : cur - 1]);  // into the stage freed by the previous group
       compute(&stg[cur]);
