@@ -206,30 +206,48 @@ __global__ __launch_bounds__(kGuWaves * 64) void skinny_gateup_kernel(
     issue(b + D - 1, (b + D - 1) % D);
     const uint8_t* slot = ring + (b % D) * C::kSlot;
     const int bk = block_at(b);
+    // the block's two K-groups (the second may lie past K when K/128 is odd):
+    // all operands first, then every MFMA back to back (they are independent),
+    // then the scale FMAs in K-group order, so the block's latency is one LDS
+    // round trip plus the MFMA issue time rather than a chain of MFMA results
+    const int nk = 2 * bk + 1 < nkb ? 2 : 1;
+    v8i af[2][MT], bf[2][NS];
+    float xa[2][MT][4], wv[2][NS];
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
-      const int kb = 2 * bk + kk;
-      if (kb >= nkb) break;
-      v8i af[MT];
-      float xa[MT][4];
+      const int kb = 2 * bk + (kk < nk ? kk : 0);
 #pragma unroll
       for (int i = 0; i < MT; ++i) {
-        af[i] = ring_frag(slot + i * 16 * kRowBytes, lr, q, kk);
+        af[kk][i] = ring_frag(slot + i * 16 * kRowBytes, lr, q, kk);
         const float4 xv = *reinterpret_cast<const float4*>(sXs + kb * RA + 16 * i + 4 * q);
-        xa[i][0] = xv.x; xa[i][1] = xv.y; xa[i][2] = xv.z; xa[i][3] = xv.w;
+        xa[kk][i][0] = xv.x; xa[kk][i][1] = xv.y; xa[kk][i][2] = xv.z; xa[kk][i][3] = xv.w;
       }
 #pragma unroll
       for (int n = 0; n < NS; ++n) {
-        const v8i bf = ring_frag(slot + C::kA + (wave * NS + n) * 16 * kRowBytes, lr, q, kk);
-        const float w = sWs[(wave * NS + n) * nkb + kb];
+        bf[kk][n] = ring_frag(slot + C::kA + (wave * NS + n) * 16 * kRowBytes, lr, q, kk);
+        wv[kk][n] = sWs[(wave * NS + n) * nkb + kb];
+      }
+    }
+    v4f p[2][NS][MT];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int n = 0; n < NS; ++n)
 #pragma unroll
         for (int i = 0; i < MT; ++i) {
           const v4f zero = {0.0f, 0.0f, 0.0f, 0.0f};
-          const v4f p = mfma_fp8_16x16x128(af[i], bf, zero);
-#pragma unroll
-          for (int r = 0; r < 4; ++r) acc[i][n][r] = __builtin_fmaf(p[r], xa[i][r] * w, acc[i][n][r]);
+          p[kk][n][i] = mfma_fp8_16x16x128(af[kk][i], bf[kk][n], zero);
         }
-      }
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      if (kk >= nk) break;
+#pragma unroll
+      for (int n = 0; n < NS; ++n)
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            acc[i][n][r] = __builtin_fmaf(p[kk][n][i][r], xa[kk][i][r] * wv[kk][n], acc[i][n][r]);
     }
   }
   wait_vm<0>();  // drain the trailing repeat copies
