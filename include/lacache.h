@@ -218,6 +218,85 @@ int lacache_facache_attention(void* stream, const uint16_t* q, const uint16_t* k
                               int64_t d, int64_t c_begin, int64_t c_end, int mode);
 
 /*
+ * Coarse quantization granularities (Sec. 4, Table fp8-granularities): the
+ * paper compares its per-group scheme with "per tensor" and "per token"
+ * quantization of the same FFN linears. Readings: per tensor = one scale for
+ * a whole activation tensor and one for a whole weight; per token = one scale
+ * per activation row and one per weight output channel (row). The quantizer
+ * rules are those of the per-group path (Eqs. 7-8); only the set of values
+ * sharing a scale changes. A coarse scale needs the max over a whole row or
+ * tensor, which one GEMM tile never sees, so these paths quantize in separate
+ * passes and the SwiGLU output goes through HBM in fp32 (the per-group path
+ * fuses both quantizations). Scales are written in the per-group layouts
+ * (every group of a row carries the row's scale; weight block scales are 1
+ * and the per-row weight scales multiply each output column after the K
+ * sum), so the same GEMM kernels run every granularity. For comparison
+ * studies; the per-group calls above are the library's FFN.
+ */
+enum { LACACHE_GRAN_GROUP = 0, LACACHE_GRAN_TOKEN = 1, LACACHE_GRAN_TENSOR = 2 };
+
+/*
+ * Weight quantization at a granularity. GROUP: lacache_quant_weights (w_row_s
+ * unused, may be NULL). TOKEN / TENSOR:
+ *   w       [N x K] bf16                     (input)
+ *   w_q     [N x K] e4m3                     (output)
+ *   w_s     [N/128 x K/128] fp32             (output) all 1.0
+ *   w_row_s [N] fp32                         (output) RN32(max|w[n, :]| / 448)
+ *                                            per row, or the whole matrix's
+ *                                            scale in every entry (TENSOR)
+ * Other granularity values: LACACHE_ERR_INVALID_ARG.
+ */
+int lacache_quant_weights_g(void* stream, const uint16_t* w, uint8_t* w_q, float* w_s, float* w_row_s, int64_t N,
+                            int64_t K, int granularity);
+
+/* The RMSNorm alone: y [M x H] fp32 = RN32(RN32(x * norm_w) * r), the same
+ * values the fused quantizer quantizes (lacache_rmsnorm_quant). */
+int lacache_rmsnorm_f32(void* stream, const uint16_t* x, const uint16_t* norm_w, float* y, int64_t M, int64_t H);
+
+/*
+ * Quantization of fp32 rows v [M x K] (K a multiple of 128) at a granularity:
+ *   q      [M x K] e4m3                      (output)
+ *   s_kgm  [K/128 x M] fp32                  (output) the scale of group kb of
+ *                                            row m at s_kgm[kb*M + m] (for
+ *                                            TOKEN / TENSOR the row's scale in
+ *                                            every group)
+ *   s_rows [M] fp32                          (output, TOKEN / TENSOR; unused
+ *                                            and may be NULL for GROUP) the
+ *                                            row scales
+ */
+int lacache_quant_rows_g(void* stream, const float* v, uint8_t* q, float* s_kgm, float* s_rows, int64_t M, int64_t K,
+                         int granularity);
+
+/*
+ * The gate/up GEMM and SwiGLU without the re-quantization: h [M x I] fp32 =
+ * SiLU(g) * u, g and u the dequantized sums of lacache_gateup_swiglu_quant,
+ * each output column n also multiplied by wgu_row_s[n] ([2I] fp32, gate rows
+ * first) when wgu_row_s is not NULL. Always the tiled kernels.
+ */
+int lacache_gateup_swiglu_f32(void* stream, const uint8_t* xq, const float* xs, const uint8_t* wgu_q,
+                              const float* wgu_s, const float* wgu_row_s, float* h, int64_t M, int64_t H, int64_t I,
+                              int group);
+
+/* lacache_down_proj with output column n also multiplied by wd_row_s[n] ([H]
+ * fp32, NULL for none) before the bf16 rounding. Always the tiled kernels. */
+int lacache_down_proj_g(void* stream, const uint8_t* hq, const float* hs, const uint8_t* wd_q, const float* wd_s,
+                        const float* wd_row_s, uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I,
+                        int group);
+
+/*
+ * The whole FFN at a granularity, with weights from lacache_quant_weights_g
+ * of the same granularity. GROUP: lacache_ffn_fp8 (row scales unused).
+ * TOKEN / TENSOR: RMSNorm -> quantization of its rows -> gate/up + SwiGLU
+ * (fp32 h) -> quantization of h -> down, with a library-owned workspace of
+ * lacache_ffn_g_workspace_bytes(M, H, I) (serialize calls on one device, as
+ * for lacache_ffn_fp8).
+ */
+int lacache_ffn_fp8_g(void* stream, const uint16_t* x, const uint16_t* norm_w, const uint8_t* wgu_q,
+                      const float* wgu_s, const float* wgu_row_s, const uint8_t* wd_q, const float* wd_s,
+                      const float* wd_row_s, uint16_t* out, int64_t M, int64_t H, int64_t I, int granularity);
+size_t lacache_ffn_g_workspace_bytes(int64_t M, int64_t H, int64_t I);
+
+/*
  * Kernel-path policy for the GEMM stages, process-wide:
  *   0 = automatic (the skinny weight-streaming kernels for M <= 64,
  *       H <= 8192 and I <= 16384, the tiled MFMA kernels otherwise), 1 = always skinny

@@ -9,7 +9,8 @@ non-OK status. Every step of the FFN runs in the library's HIP kernels.
 import torch
 
 from ._lib import (LACACHE_ERR_ALLOC, LACACHE_ERR_HIP, LACACHE_ERR_INVALID_ARG, LACACHE_ERR_UNSUPPORTED,  # noqa: F401
-                   LACACHE_OK, LacacheError, check, lib, status_string)
+                   LACACHE_GRAN_GROUP, LACACHE_GRAN_TENSOR, LACACHE_GRAN_TOKEN, LACACHE_OK, LacacheError, check, lib,
+                   status_string)
 
 GROUP = 128
 _U8 = (torch.uint8, torch.float8_e4m3fn)
@@ -147,6 +148,87 @@ def lacache_facache_attention(q, k, v, o, lse=None, cache_m=None, cache_l=None, 
         _ptr(cache_l, f32, "cache_l", (heads, N), optional=not cache),
         _ptr(cache_o, f32, "cache_o", (heads, N, d), optional=not cache), heads, N, d, c_begin, c_end, mode),
         "lacache_facache_attention")
+
+
+# ---- coarse quantization granularities (per token, per tensor) ------------
+
+_F32 = (torch.float32,)
+
+
+def lacache_quant_weights_g(w, w_q, w_s, w_row_s, granularity, stream=None):
+    """Weight quantization at a granularity: w [N, K] bf16 -> w_q [N, K], w_s
+    [N/128, K/128] (1.0 for token/tensor), w_row_s [N] (token/tensor)."""
+    N, K = w.shape
+    check(lib().lacache_quant_weights_g(
+        _stream(stream, w), _ptr(w, _BF16, "w"), _ptr(w_q, _U8, "w_q", (N, K)),
+        _ptr(w_s, _F32, "w_s", (N // GROUP, K // GROUP)),
+        _ptr(w_row_s, _F32, "w_row_s", (N,), optional=granularity == LACACHE_GRAN_GROUP), N, K, granularity),
+        "lacache_quant_weights_g")
+
+
+def lacache_rmsnorm_f32(x, norm_w, y, stream=None):
+    """y [M, H] fp32 = RMSNorm(x) with the fused quantizer's arithmetic."""
+    M, H = x.shape
+    check(lib().lacache_rmsnorm_f32(_stream(stream, x), _ptr(x, _BF16, "x"), _ptr(norm_w, _BF16, "norm_w", (H,)),
+                                    _ptr(y, _F32, "y", (M, H)), M, H), "lacache_rmsnorm_f32")
+
+
+def lacache_quant_rows_g(v, q, s_kgm, s_rows, granularity, stream=None):
+    """fp32 rows v [M, K] -> codes q [M, K], scales s_kgm [K/128, M], row scales s_rows [M]."""
+    M, K = v.shape
+    check(lib().lacache_quant_rows_g(
+        _stream(stream, v), _ptr(v, _F32, "v"), _ptr(q, _U8, "q", (M, K)), _ptr(s_kgm, _F32, "s_kgm", (K // GROUP, M)),
+        _ptr(s_rows, _F32, "s_rows", (M,), optional=granularity == LACACHE_GRAN_GROUP), M, K, granularity),
+        "lacache_quant_rows_g")
+
+
+def lacache_gateup_swiglu_f32(xq, xs, wgu_q, wgu_s, wgu_row_s, h, group=GROUP, stream=None):
+    """h [M, I] fp32 = SiLU(g) u without re-quantization; wgu_row_s [2I] or None."""
+    M, H = xq.shape
+    I = h.shape[1]
+    check(lib().lacache_gateup_swiglu_f32(
+        _stream(stream, xq), _ptr(xq, _U8, "xq"), _ptr(xs, _F32, "xs", (H // group, M)),
+        _ptr(wgu_q, _U8, "wgu_q", (2 * I, H)), _ptr(wgu_s, _F32, "wgu_s", (2 * I // group, H // group)),
+        _ptr(wgu_row_s, _F32, "wgu_row_s", (2 * I,), optional=True), _ptr(h, _F32, "h", (M, I)), M, H, I, group),
+        "lacache_gateup_swiglu_f32")
+
+
+def lacache_down_proj_g(hq, hs, wd_q, wd_s, wd_row_s, out, out_tap=None, group=GROUP, stream=None):
+    """lacache_down_proj with per-column weight scales wd_row_s [H] (or None)."""
+    M, I = hq.shape
+    H = out.shape[1]
+    check(lib().lacache_down_proj_g(
+        _stream(stream, hq), _ptr(hq, _U8, "hq"), _ptr(hs, _F32, "hs", (I // group, M)),
+        _ptr(wd_q, _U8, "wd_q", (H, I)), _ptr(wd_s, _F32, "wd_s", (H // group, I // group)),
+        _ptr(wd_row_s, _F32, "wd_row_s", (H,), optional=True), _ptr(out, _BF16, "out", (M, H)),
+        _ptr(out_tap, _F32, "out_tap", (M, H), optional=True), M, H, I, group), "lacache_down_proj_g")
+
+
+def lacache_ffn_fp8_g(x, norm_w, wgu_q, wgu_s, wgu_row_s, wd_q, wd_s, wd_row_s, out, granularity, stream=None):
+    """The whole FFN at a granularity (weights from lacache_quant_weights_g)."""
+    M, H = x.shape
+    I = wd_q.shape[1]
+    opt = granularity == LACACHE_GRAN_GROUP
+    check(lib().lacache_ffn_fp8_g(
+        _stream(stream, x), _ptr(x, _BF16, "x"), _ptr(norm_w, _BF16, "norm_w", (H,)),
+        _ptr(wgu_q, _U8, "wgu_q", (2 * I, H)), _ptr(wgu_s, _F32, "wgu_s", (2 * I // GROUP, H // GROUP)),
+        _ptr(wgu_row_s, _F32, "wgu_row_s", (2 * I,), optional=opt), _ptr(wd_q, _U8, "wd_q", (H, I)),
+        _ptr(wd_s, _F32, "wd_s", (H // GROUP, I // GROUP)), _ptr(wd_row_s, _F32, "wd_row_s", (H,), optional=opt),
+        _ptr(out, _BF16, "out", (M, H)), M, H, I, granularity), "lacache_ffn_fp8_g")
+
+
+def lacache_ffn_g_workspace_bytes(M, H, I):
+    return int(lib().lacache_ffn_g_workspace_bytes(M, H, I))
+
+
+def quantize_weights_g(w, granularity, stream=None):
+    """Returns (w_q, w_s, w_row_s) for a bf16 weight at a granularity (w_row_s None for GROUP)."""
+    N, K = w.shape
+    w_q = torch.empty((N, K), dtype=torch.uint8, device=w.device)
+    w_s = torch.empty((N // GROUP, K // GROUP), dtype=torch.float32, device=w.device)
+    w_row_s = None if granularity == LACACHE_GRAN_GROUP else torch.empty((N,), dtype=torch.float32, device=w.device)
+    lacache_quant_weights_g(w, w_q, w_s, w_row_s, granularity, stream)
+    return w_q, w_s, w_row_s
 
 
 def lacache_set_path_policy(policy):

@@ -16,6 +16,7 @@ LACACHE_ERR_INVALID_ARG = -1
 LACACHE_ERR_UNSUPPORTED = -2
 LACACHE_ERR_HIP = -3
 LACACHE_ERR_ALLOC = -4
+LACACHE_GRAN_GROUP, LACACHE_GRAN_TOKEN, LACACHE_GRAN_TENSOR = 0, 1, 2
 
 # name -> (restype, argtypes)
 _P, _I64, _I = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
@@ -32,6 +33,13 @@ SIGNATURES = {
     "lacache_add_bf16": (_I, [_P, _P, _P, _I64]),
     "lacache_encode_e4m3": (_I, [_P, _P, _P, _I64]),
     "lacache_facache_attention": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, _I64, _I]),
+    "lacache_quant_weights_g": (_I, [_P, _P, _P, _P, _P, _I64, _I64, _I]),
+    "lacache_rmsnorm_f32": (_I, [_P, _P, _P, _P, _I64, _I64]),
+    "lacache_quant_rows_g": (_I, [_P, _P, _P, _P, _P, _I64, _I64, _I]),
+    "lacache_gateup_swiglu_f32": (_I, [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I]),
+    "lacache_down_proj_g": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I]),
+    "lacache_ffn_fp8_g": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I]),
+    "lacache_ffn_g_workspace_bytes": (ctypes.c_size_t, [_I64, _I64, _I64]),
     "lacache_set_path_policy": (_I, [_I]),
     "lacache_status_string": (ctypes.c_char_p, [_I]),
     "lacache_release_workspace": (None, []),

@@ -352,6 +352,129 @@ int lacache_ffn_fp8_ws(void* stream, const uint16_t* x, const uint16_t* norm_w, 
                   lay);
 }
 
+// ---------------------------------------------------------------------------
+// Coarse quantization granularities (per token, per tensor)
+// ---------------------------------------------------------------------------
+
+int lacache_quant_weights_g(void* stream, const uint16_t* w, uint8_t* w_q, float* w_s, float* w_row_s, int64_t N,
+                            int64_t K, int granularity) {
+  if (granularity == LACACHE_GRAN_GROUP) return lacache_quant_weights(stream, w, w_q, w_s, N, K, 128);
+  if (granularity != LACACHE_GRAN_TOKEN && granularity != LACACHE_GRAN_TENSOR) return LACACHE_ERR_INVALID_ARG;
+  RETURN_IF(check_dim(N, kMaxN));
+  RETURN_IF(check_dim(K, kMaxN));
+  if (!ptrs_ok({w, w_q, w_s, w_row_s})) return LACACHE_ERR_INVALID_ARG;
+  if (!disjoint({rng(w_q, N * K), rng(w_s, (N / 128) * (K / 128) * 4), rng(w_row_s, N * 4)}, {rng(w, N * K * 2)}))
+    return LACACHE_ERR_INVALID_ARG;
+  return hip_status(launch_quant_weights_rows(static_cast<hipStream_t>(stream), w, w_q, w_s, w_row_s, N, K,
+                                              granularity == LACACHE_GRAN_TENSOR));
+}
+
+int lacache_rmsnorm_f32(void* stream, const uint16_t* x, const uint16_t* norm_w, float* y, int64_t M, int64_t H) {
+  RETURN_IF(check_m(M));
+  RETURN_IF(check_dim(H, kMaxH));
+  if (M == 0) return LACACHE_OK;
+  if (!ptrs_ok({x, norm_w, y})) return LACACHE_ERR_INVALID_ARG;
+  if (!disjoint({rng(y, M * H * 4)}, {rng(x, M * H * 2), rng(norm_w, H * 2)})) return LACACHE_ERR_INVALID_ARG;
+  return hip_status(launch_rmsnorm_f32(static_cast<hipStream_t>(stream), x, norm_w, y, M, H));
+}
+
+int lacache_quant_rows_g(void* stream, const float* v, uint8_t* q, float* s_kgm, float* s_rows, int64_t M, int64_t K,
+                         int granularity) {
+  if (granularity < LACACHE_GRAN_GROUP || granularity > LACACHE_GRAN_TENSOR) return LACACHE_ERR_INVALID_ARG;
+  RETURN_IF(check_m(M));
+  RETURN_IF(check_dim(K, kMaxI));
+  if (M == 0) return LACACHE_OK;
+  const bool group = granularity == LACACHE_GRAN_GROUP;
+  if (!ptrs_ok({v, q, s_kgm}) || (!group && !ptrs_ok({s_rows})) || !opt_ptr_ok(s_rows)) return LACACHE_ERR_INVALID_ARG;
+  if (!disjoint({rng(q, M * K), rng(s_kgm, (K / 128) * M * 4), rng(s_rows, (!group && s_rows) ? M * 4 : 0)},
+                {rng(v, M * K * 4)}))
+    return LACACHE_ERR_INVALID_ARG;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (group) return hip_status(launch_quant_groups_f32(st, v, q, s_kgm, M, K));
+  return hip_status(launch_quant_rows_f32(st, v, q, s_kgm, s_rows, M, K, granularity == LACACHE_GRAN_TENSOR));
+}
+
+int lacache_gateup_swiglu_f32(void* stream, const uint8_t* xq, const float* xs, const uint8_t* wgu_q,
+                              const float* wgu_s, const float* wgu_row_s, float* h, int64_t M, int64_t H, int64_t I,
+                              int group) {
+  RETURN_IF(check_group(group));
+  RETURN_IF(check_m(M));
+  RETURN_IF(check_dim(H, kMaxH));
+  RETURN_IF(check_dim(I, kMaxI));
+  if (M == 0) return LACACHE_OK;
+  if (!ptrs_ok({xq, xs, wgu_q, wgu_s, h}) || !opt_ptr_ok(wgu_row_s)) return LACACHE_ERR_INVALID_ARG;
+  if (!disjoint({rng(h, M * I * 4)}, {rng(xq, M * H), rng(xs, (H / 128) * M * 4), rng(wgu_q, 2 * I * H),
+                                      rng(wgu_s, (2 * I / 128) * (H / 128) * 4),
+                                      rng(wgu_row_s, wgu_row_s ? 2 * I * 4 : 0)}))
+    return LACACHE_ERR_INVALID_ARG;
+  return hip_status(launch_gateup_tiled(static_cast<hipStream_t>(stream), xq, xs, wgu_q, wgu_s, nullptr, nullptr, h, M,
+                                        H, I, wgu_row_s));
+}
+
+int lacache_down_proj_g(void* stream, const uint8_t* hq, const float* hs, const uint8_t* wd_q, const float* wd_s,
+                        const float* wd_row_s, uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I,
+                        int group) {
+  RETURN_IF(check_group(group));
+  RETURN_IF(check_m(M));
+  RETURN_IF(check_dim(H, kMaxH));
+  RETURN_IF(check_dim(I, kMaxI));
+  if (M == 0) return LACACHE_OK;
+  if (!ptrs_ok({hq, hs, wd_q, wd_s, out}) || !opt_ptr_ok(out_tap) || !opt_ptr_ok(wd_row_s))
+    return LACACHE_ERR_INVALID_ARG;
+  if (!disjoint({rng(out, M * H * 2), rng(out_tap, out_tap ? M * H * 4 : 0)},
+                {rng(hq, M * I), rng(hs, (I / 128) * M * 4), rng(wd_q, H * I), rng(wd_s, (H / 128) * (I / 128) * 4),
+                 rng(wd_row_s, wd_row_s ? H * 4 : 0)}))
+    return LACACHE_ERR_INVALID_ARG;
+  void* scratch = nullptr;
+  if (tiled_down_ws_bytes(M, H, I) > 0) RETURN_IF(get_workspace(tiled_down_ws_bytes(M, H, I), &scratch));
+  return hip_status(launch_down_tiled(static_cast<hipStream_t>(stream), hq, hs, wd_q, wd_s, out, out_tap, M, H, I,
+                                      scratch, wd_row_s));
+}
+
+size_t lacache_ffn_g_workspace_bytes(int64_t M, int64_t H, int64_t I) {
+  if (check_m(M) != LACACHE_OK || check_dim(H, kMaxH) != LACACHE_OK || check_dim(I, kMaxI) != LACACHE_OK) return 0;
+  const size_t m = static_cast<size_t>(M);
+  return align256(m * static_cast<size_t>(H > I ? H : I) * 4) + align256(m * H) + align256((H / 128) * m * 4) +
+         align256(m * I) + align256((I / 128) * m * 4) + align256(m * 4) + align256(tiled_down_ws_bytes(M, H, I));
+}
+
+int lacache_ffn_fp8_g(void* stream, const uint16_t* x, const uint16_t* norm_w, const uint8_t* wgu_q,
+                      const float* wgu_s, const float* wgu_row_s, const uint8_t* wd_q, const float* wd_s,
+                      const float* wd_row_s, uint16_t* out, int64_t M, int64_t H, int64_t I, int granularity) {
+  if (granularity == LACACHE_GRAN_GROUP) return lacache_ffn_fp8(stream, x, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, M, H, I, 128);
+  if (granularity != LACACHE_GRAN_TOKEN && granularity != LACACHE_GRAN_TENSOR) return LACACHE_ERR_INVALID_ARG;
+  RETURN_IF(validate_ffn(x, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, M, H, I, 128));
+  if (M == 0) return LACACHE_OK;
+  if (!ptrs_ok({wgu_row_s, wd_row_s}) ||
+      !disjoint({rng(out, M * H * 2)}, {rng(wgu_row_s, 2 * I * 4), rng(wd_row_s, H * 4)}))
+    return LACACHE_ERR_INVALID_ARG;
+  void* base = nullptr;
+  RETURN_IF(get_workspace(lacache_ffn_g_workspace_bytes(M, H, I), &base));
+  // [fp32 y, then h][xq][xs][hq][hs][row scales][split-K partials]
+  char* b = static_cast<char*>(base);
+  const size_t m = static_cast<size_t>(M);
+  float* f = reinterpret_cast<float*>(b);
+  b += align256(m * static_cast<size_t>(H > I ? H : I) * 4);
+  uint8_t* xq = reinterpret_cast<uint8_t*>(b);
+  b += align256(m * H);
+  float* xs = reinterpret_cast<float*>(b);
+  b += align256((H / 128) * m * 4);
+  uint8_t* hq = reinterpret_cast<uint8_t*>(b);
+  b += align256(m * I);
+  float* hs = reinterpret_cast<float*>(b);
+  b += align256((I / 128) * m * 4);
+  float* rows = reinterpret_cast<float*>(b);
+  b += align256(m * 4);
+  void* part = b;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const bool tensor = granularity == LACACHE_GRAN_TENSOR;
+  RETURN_IF(hip_status(launch_rmsnorm_f32(st, x, norm_w, f, M, H)));
+  RETURN_IF(hip_status(launch_quant_rows_f32(st, f, xq, xs, rows, M, H, tensor)));
+  RETURN_IF(hip_status(launch_gateup_tiled(st, xq, xs, wgu_q, wgu_s, nullptr, nullptr, f, M, H, I, wgu_row_s)));
+  RETURN_IF(hip_status(launch_quant_rows_f32(st, f, hq, hs, rows, M, I, tensor)));
+  return hip_status(launch_down_tiled(st, hq, hs, wd_q, wd_s, out, nullptr, M, H, I, part, wd_row_s));
+}
+
 int lacache_add_bf16(void* stream, uint16_t* x_inout, const uint16_t* y, int64_t n) {
   if (n < 0) return LACACHE_ERR_INVALID_ARG;
   if (n == 0) return LACACHE_OK;

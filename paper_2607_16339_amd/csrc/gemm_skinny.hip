@@ -485,6 +485,13 @@ hipError_t launch_gateup_skinny(hipStream_t st, const uint8_t* xq, const float* 
   return hipGetLastError();
 }
 
+hipError_t launch_quant_groups_f32(hipStream_t st, const float* v, uint8_t* codes, float* scales, int64_t M, int64_t K) {
+  const int64_t groups = M * (K / 128);
+  hipLaunchKernelGGL(skinny_hquant_kernel, dim3(static_cast<unsigned>((groups + 15) / 16)), dim3(256), 0, st, v, codes,
+                     scales, M, K);
+  return hipGetLastError();
+}
+
 hipError_t launch_down_skinny(hipStream_t st, const uint8_t* hq, const float* hs, const uint8_t* wq, const float* ws,
                               uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I) {
   const dim3 grid(static_cast<unsigned>(H / 16)), block(kDnSplit * 64);

@@ -107,8 +107,8 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
     const uint8_t* __restrict__ aq, const float* __restrict__ as,  // [M x K] codes, [K/128 x M] scales
     const uint8_t* __restrict__ bq, const float* __restrict__ bs,  // [N x K] codes, [N/128 x K/128] scales
     uint8_t* __restrict__ hq, float* __restrict__ hs, float* __restrict__ h_tap,
-    uint16_t* __restrict__ out, float* __restrict__ out_tap, float* __restrict__ part, int64_t M, int64_t K,
-    int64_t N, int64_t I, int KS, int W) {
+    uint16_t* __restrict__ out, float* __restrict__ out_tap, float* __restrict__ part,
+    const float* __restrict__ col_s, int64_t M, int64_t K, int64_t N, int64_t I, int KS, int W) {
   static_assert(BM == 128 || BM == 256, "BM must be 128 or 256");
   constexpr int NW = kTileWaves;
   constexpr int WC = BM == 256 ? 128 : 64;  // weight rows (output columns) per wavefront
@@ -300,6 +300,23 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
       cur = cur + 1 == S ? 0 : cur + 1;
     }
 
+    if (col_s != nullptr) {
+      // per-channel weight scales: output column n times col_s[n]
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const int64_t n = kGateUp ? (j < NJ / 2 ? 0 : I) + static_cast<int64_t>(it.col) * 128 + (WC / 2) * wn +
+                                        16 * (j < NJ / 2 ? j : j - NJ / 2) + 4 * q
+                                  : static_cast<int64_t>(it.col) * BNR + WC * wn + 16 * j + 4 * q;
+        const float4 cs = (kGateUp || n < N) ? *reinterpret_cast<const float4*>(col_s + n) : make_float4(0, 0, 0, 0);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          acc[i][j][0] *= cs.x;
+          acc[i][j][1] *= cs.y;
+          acc[i][j][2] *= cs.z;
+          acc[i][j][3] *= cs.w;
+        }
+      }
+    }
     if (kGateUp) {
       // ---- SwiGLU: h = SiLU(g) * u; lanes hold matching gate (j) and up
       // (j + NJ/2) values; h replaces g in acc
@@ -326,9 +343,20 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
       }
       wait_lds();
       bar();  // the row amax of every wavefront of the band is in LDS
-      // ---- 1x128 quantization of each row's h-group
+      // ---- 1x128 quantization of each row's h-group (without hq: h only)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
+        if (hq == nullptr) {
+          const int64_t grow = static_cast<int64_t>(it.m0) + 64 * wm + 16 * i + lr;
+          if (grow < M) {
+#pragma unroll
+            for (int j = 0; j < NJ / 2; ++j)
+              *reinterpret_cast<float4*>(h_tap + grow * I + static_cast<int64_t>(it.col) * 128 + (WC / 2) * wn +
+                                         16 * j + 4 * q) =
+                  make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+          }
+          continue;
+        }
         const int row = 64 * wm + 16 * i + lr;
         const int64_t grow = static_cast<int64_t>(it.m0) + row;
         float amax = sRed[0][row];
@@ -388,16 +416,16 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
 }
 
 template __global__ void gemm_tiled_kernel<true, 256>(const uint8_t*, const float*, const uint8_t*, const float*,
-                                                     uint8_t*, float*, float*, uint16_t*, float*, float*, int64_t,
+                                                     uint8_t*, float*, float*, uint16_t*, float*, float*, const float*, int64_t,
                                                      int64_t, int64_t, int64_t, int, int);
 template __global__ void gemm_tiled_kernel<true, 128>(const uint8_t*, const float*, const uint8_t*, const float*,
-                                                     uint8_t*, float*, float*, uint16_t*, float*, float*, int64_t,
+                                                     uint8_t*, float*, float*, uint16_t*, float*, float*, const float*, int64_t,
                                                      int64_t, int64_t, int64_t, int, int);
 template __global__ void gemm_tiled_kernel<false, 256>(const uint8_t*, const float*, const uint8_t*, const float*,
-                                                      uint8_t*, float*, float*, uint16_t*, float*, float*, int64_t,
+                                                      uint8_t*, float*, float*, uint16_t*, float*, float*, const float*, int64_t,
                                                       int64_t, int64_t, int64_t, int, int);
 template __global__ void gemm_tiled_kernel<false, 128>(const uint8_t*, const float*, const uint8_t*, const float*,
-                                                      uint8_t*, float*, float*, uint16_t*, float*, float*, int64_t,
+                                                      uint8_t*, float*, float*, uint16_t*, float*, float*, const float*, int64_t,
                                                       int64_t, int64_t, int64_t, int, int);
 
 namespace {
@@ -433,13 +461,13 @@ int cu_count() {
 template <bool kGateUp, int BM>
 hipError_t launch_tiled(hipStream_t st, const uint8_t* aq, const float* as, const uint8_t* bq, const float* bs,
                         uint8_t* hq, float* hs, float* h_tap, uint16_t* out, float* out_tap, float* part, int64_t M,
-                        int64_t K, int64_t N, int64_t I, int KS) {
+                        int64_t K, int64_t N, int64_t I, int KS, const float* col_s) {
   const int64_t ny = kGateUp ? I / 128 : (N + BNR - 1) / BNR;
   const int W = static_cast<int>(((M + BM - 1) / BM) * ny * KS);  // work items (< 2^31 by the size limits)
   // one workgroup per CU (the LDS ring allows no more)
   const int G = W < cu_count() ? W : cu_count();
   hipLaunchKernelGGL((gemm_tiled_kernel<kGateUp, BM>), dim3(static_cast<unsigned>(G)), dim3(kTileWaves * 64), 0, st,
-                     aq, as, bq, bs, hq, hs, h_tap, out, out_tap, part, M, K, N, I, KS, W);
+                     aq, as, bq, bs, hq, hs, h_tap, out, out_tap, part, col_s, M, K, N, I, KS, W);
   return hipGetLastError();
 }
 
@@ -476,21 +504,24 @@ bool gateup_bm256(int64_t M, int64_t I) {
 
 hipError_t launch_gateup_tiled(hipStream_t st, const uint8_t* xq, const float* xs, const uint8_t* wq,
                                const float* ws, uint8_t* hq, float* hs, float* h_tap, int64_t M, int64_t H,
-                               int64_t I) {
+                               int64_t I, const float* col_s) {
   if (gateup_bm256(M, I))
-    return launch_tiled<true, 256>(st, xq, xs, wq, ws, hq, hs, h_tap, nullptr, nullptr, nullptr, M, H, 2 * I, I, 1);
-  return launch_tiled<true, 128>(st, xq, xs, wq, ws, hq, hs, h_tap, nullptr, nullptr, nullptr, M, H, 2 * I, I, 1);
+    return launch_tiled<true, 256>(st, xq, xs, wq, ws, hq, hs, h_tap, nullptr, nullptr, nullptr, M, H, 2 * I, I, 1,
+                                   col_s);
+  return launch_tiled<true, 128>(st, xq, xs, wq, ws, hq, hs, h_tap, nullptr, nullptr, nullptr, M, H, 2 * I, I, 1,
+                                 col_s);
 }
 
 hipError_t launch_down_tiled(hipStream_t st, const uint8_t* hq, const float* hs, const uint8_t* wq, const float* ws,
-                             uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I, void* ws_buf) {
+                             uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I, void* ws_buf,
+                             const float* col_s) {
   if (use_bm256(M, (H + BNR - 1) / BNR))
     return launch_tiled<false, 256>(st, hq, hs, wq, ws, nullptr, nullptr, nullptr, out, out_tap, nullptr, M, I, H, I,
-                                    1);
+                                    1, col_s);
   const int ks = down_splits(M, H, I);
   float* part = static_cast<float*>(ws_buf);
   hipError_t e = launch_tiled<false, 128>(st, hq, hs, wq, ws, nullptr, nullptr, nullptr, out, out_tap, part, M, I, H,
-                                          I, ks);
+                                          I, ks, col_s);
   if (e != hipSuccess || ks == 1) return e;
   const int64_t mn = M * H;
   hipLaunchKernelGGL(split_reduce_kernel, dim3(static_cast<unsigned>((mn / 4 + 255) / 256)), dim3(256), 0, st, part,

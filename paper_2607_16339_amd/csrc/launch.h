@@ -12,7 +12,22 @@ hipError_t launch_quant_weights(hipStream_t st, const uint16_t* w, uint8_t* wq, 
 // With y non-null: x = RNE_bf16(x + y) in place first (the fused AddNorm).
 hipError_t launch_rmsnorm_quant(hipStream_t st, uint16_t* x, const uint16_t* nw, uint8_t* xq, float* xs, int64_t M,
                                 int64_t H, const uint16_t* y = nullptr);
+// The RMSNorm alone, y = RN32(RN32(x * w) * r) in fp32 [M x H] (same
+// arithmetic as the fused quantizer).
+hipError_t launch_rmsnorm_f32(hipStream_t st, const uint16_t* x, const uint16_t* nw, float* y, int64_t M, int64_t H);
 hipError_t launch_add_bf16(hipStream_t st, uint16_t* x, const uint16_t* y, int64_t n);
+
+// Coarse granularities: per-row (or, with per_tensor, one) scales of fp32
+// rows [M x K] into s_rows [M], the codes, and (kgm non-null) the scales in
+// the K-group-major [K/128 x M] layout of the GEMMs.
+hipError_t launch_quant_rows_f32(hipStream_t st, const float* v, uint8_t* codes, float* kgm, float* s_rows, int64_t M,
+                                 int64_t K, bool per_tensor);
+// The same for a bf16 weight [N x K]: row scales w_rows [N], block scales
+// w_blocks [N/128 x K/128] set to 1 (the row scales act in the GEMM epilogue).
+hipError_t launch_quant_weights_rows(hipStream_t st, const uint16_t* w, uint8_t* wq, float* w_blocks, float* w_rows,
+                                     int64_t N, int64_t K, bool per_tensor);
+// The 1x128 group quantizer of fp32 rows [M x K] (codes, scales [K/128 x M]).
+hipError_t launch_quant_groups_f32(hipStream_t st, const float* v, uint8_t* codes, float* scales, int64_t M, int64_t K);
 hipError_t launch_encode_e4m3(hipStream_t st, const float* v, uint8_t* codes, int64_t n);
 
 // Tile (row r, column c) of workgroup `bid` in an R x C grid of output tiles.
@@ -37,16 +52,19 @@ __host__ __device__ inline void xcd_grouped_tile(int64_t bid, int64_t R, int64_t
   c = w / rows;
 }
 
-// Tiled MFMA GEMMs (any M).
+// Tiled MFMA GEMMs (any M). col_s (nullable): a scale per weight row that
+// multiplies that output column after the K sum (per-channel weights); with
+// hq == nullptr the gate/up writes only the fp32 h to h_tap (no quantization).
 hipError_t launch_gateup_tiled(hipStream_t st, const uint8_t* xq, const float* xs, const uint8_t* wq,
                                const float* ws, uint8_t* hq, float* hs, float* h_tap, int64_t M, int64_t H,
-                               int64_t I);
+                               int64_t I, const float* col_s = nullptr);
 // The down GEMM splits K over several workgroups when there are too few
 // output tiles to fill the chip; it then needs an fp32 scratch buffer of
 // tiled_down_ws_bytes() (0 when it does not split).
 size_t tiled_down_ws_bytes(int64_t M, int64_t H, int64_t I);
 hipError_t launch_down_tiled(hipStream_t st, const uint8_t* hq, const float* hs, const uint8_t* wq, const float* ws,
-                             uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I, void* ws_buf);
+                             uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I, void* ws_buf,
+                             const float* col_s = nullptr);
 
 // Skinny weight-streaming GEMMs (M <= kSkinnyMaxM, H <= 8192, I <= 16384).
 // The gate/up stage needs an fp32 scratch buffer of skinny_gateup_ws_bytes()

@@ -71,13 +71,14 @@ hipError_t launch_quant_weights(hipStream_t st, const uint16_t* w, uint8_t* wq, 
 // row (several wavefronts per row shorten the path of a small-M call).
 // With y (the fused AddNorm), the row is first x = RNE_bf16(float(x) +
 // float(y)), written back in place; a row then has one wavefront, which reads
-// all of it before writing any of it.
+// all of it before writing any of it. With kF32Out the normalized row goes to
+// yf (fp32) instead of being quantized (the coarse-granularity paths).
 // ---------------------------------------------------------------------------
-template <int T>
+template <int T, bool kF32Out = false>
 __global__ __launch_bounds__(256) void rmsnorm_quant_kernel(uint16_t* x, const uint16_t* __restrict__ y,
                                                             const uint16_t* __restrict__ nw,
                                                             uint8_t* __restrict__ xq, float* __restrict__ xs,
-                                                            int64_t M, int H, int wpr_log2) {
+                                                            int64_t M, int H, int wpr_log2, float* __restrict__ yf) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int part = wave & ((1 << wpr_log2) - 1);
@@ -139,6 +140,14 @@ __global__ __launch_bounds__(256) void rmsnorm_quant_kernel(uint16_t* x, const u
       y[2 * e] = (bf16lo(q[e]) * bf16lo(g[e])) * r;  // x*w is exact in fp32; one rounding for *r
       y[2 * e + 1] = (bf16hi(q[e]) * bf16hi(g[e])) * r;
     }
+    if (kF32Out) {
+      if (valid) {
+        float4* d = reinterpret_cast<float4*>(yf + row * H + 8 * c);
+        d[0] = make_float4(y[0], y[1], y[2], y[3]);
+        d[1] = make_float4(y[4], y[5], y[6], y[7]);
+      }
+      continue;
+    }
     float amax = 0.0f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) amax = __builtin_fmaxf(amax, __builtin_fabsf(y[e]));
@@ -167,7 +176,7 @@ hipError_t launch_rmsnorm_quant(hipStream_t st, uint16_t* x, const uint16_t* nw,
   const int per_block = wl > 0 ? (1 << wl) : 4;
   dim3 grid(static_cast<unsigned>((waves + per_block - 1) / per_block)), block(64 * per_block);
   const int h = static_cast<int>(H);
-#define NQ(T_) hipLaunchKernelGGL(rmsnorm_quant_kernel<T_>, grid, block, 0, st, x, y, nw, xq, xs, M, h, wl)
+#define NQ(T_) hipLaunchKernelGGL(rmsnorm_quant_kernel<T_>, grid, block, 0, st, x, y, nw, xq, xs, M, h, wl, nullptr)
   if (T <= 1) NQ(1);
   else if (T <= 2) NQ(2);
   else if (T <= 4) NQ(4);
@@ -175,6 +184,24 @@ hipError_t launch_rmsnorm_quant(hipStream_t st, uint16_t* x, const uint16_t* nw,
   else if (T <= 16) NQ(16);
   else NQ(32);
 #undef NQ
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm_f32(hipStream_t st, const uint16_t* x, const uint16_t* nw, float* yf, int64_t M, int64_t H) {
+  const int T = static_cast<int>((H + 511) / 512);
+  const dim3 grid(static_cast<unsigned>((M + 3) / 4)), block(256);  // one wavefront per row
+  uint16_t* xr = const_cast<uint16_t*>(x);                            // only read (no residual)
+  const int h = static_cast<int>(H);
+#define NF(T_)                                                                                                  \
+  hipLaunchKernelGGL((rmsnorm_quant_kernel<T_, true>), grid, block, 0, st, xr, nullptr, nw, nullptr, nullptr, M, h, \
+                     0, yf)
+  if (T <= 1) NF(1);
+  else if (T <= 2) NF(2);
+  else if (T <= 4) NF(4);
+  else if (T <= 8) NF(8);
+  else if (T <= 16) NF(16);
+  else NF(32);
+#undef NF
   return hipGetLastError();
 }
 

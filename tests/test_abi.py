@@ -214,3 +214,46 @@ def test_binding_refuses_host_tensors():
 def test_ctypes_signatures_cover_header():
     assert set(_declared_symbols()) == set(_lib.SIGNATURES)
     assert ctypes.sizeof(ctypes.c_void_p) == 8
+
+
+def test_granularity_validation(L):
+    f = Fake()
+    w, wq, ws, wr = f(), f(), f(), f()
+    # unknown granularity; null row scales; misaligned pointers; overlap
+    assert L.lacache_quant_weights_g(None, w, wq, ws, wr, 256, 256, 3) == INVALID
+    assert L.lacache_quant_weights_g(None, w, wq, ws, None, 256, 256, 1) == INVALID
+    assert L.lacache_quant_weights_g(None, w, wq, ws, wr + 4, 256, 256, 2) == INVALID
+    assert L.lacache_quant_weights_g(None, w, w, ws, wr, 256, 256, 1) == INVALID
+    assert L.lacache_quant_weights_g(None, w, wq, ws, wr, 200, 256, 1) == INVALID
+    # the group granularity is lacache_quant_weights (its own checks)
+    assert L.lacache_quant_weights_g(None, w, wq, ws, None, 256, 200, 0) == INVALID
+    # fp32 row quantization
+    v, q, sk, sr = f(), f(), f(), f()
+    assert L.lacache_quant_rows_g(None, v, q, sk, sr, 4, 256, -1) == INVALID
+    assert L.lacache_quant_rows_g(None, v, q, sk, None, 4, 256, 2) == INVALID
+    assert L.lacache_quant_rows_g(None, v, q, sk, sr, 4, 100, 1) == INVALID
+    assert L.lacache_quant_rows_g(None, v, v, sk, sr, 4, 256, 1) == INVALID
+    assert L.lacache_quant_rows_g(None, v, q, sk, sr, 0, 256, 1) == OK
+    # the norm alone
+    x, nw, y = f(), f(), f()
+    assert L.lacache_rmsnorm_f32(None, x, nw, x, 4, 256) == INVALID
+    assert L.lacache_rmsnorm_f32(None, x, nw, y, 4, 200) == INVALID
+    assert L.lacache_rmsnorm_f32(None, x, nw, y, 0, 256) == OK
+    # gate/up without re-quantization and down with row scales
+    xq, xs, gq, gs, gr, h = f(), f(), f(), f(), f(), f()
+    assert L.lacache_gateup_swiglu_f32(None, xq, xs, gq, gs, gr, h, 4, 256, 384, 64) == UNSUP
+    assert L.lacache_gateup_swiglu_f32(None, xq, xs, gq, gs, gr, xq, 4, 256, 384, 128) == INVALID
+    assert L.lacache_gateup_swiglu_f32(None, xq, xs, gq, gs, gr + 4, h, 4, 256, 384, 128) == INVALID
+    assert L.lacache_gateup_swiglu_f32(None, xq, xs, gq, gs, None, h, 0, 256, 384, 128) == OK
+    hq, hs, dq, ds, dr, out = f(), f(), f(), f(), f(), f()
+    assert L.lacache_down_proj_g(None, hq, hs, dq, ds, dr, hq, None, 4, 256, 384, 128) == INVALID
+    assert L.lacache_down_proj_g(None, hq, hs, dq, ds, dr + 8, out, None, 4, 256, 384, 128) == INVALID
+    assert L.lacache_down_proj_g(None, hq, hs, dq, ds, None, out, None, 0, 256, 384, 128) == OK
+    # the whole FFN at a granularity
+    a = [f() for _ in range(10)]
+    assert L.lacache_ffn_fp8_g(None, *a, 32, 256, 384, 5) == INVALID
+    assert L.lacache_ffn_fp8_g(None, a[0], a[1], a[2], a[3], None, a[5], a[6], a[7], a[8], 32, 256, 384, 1) == INVALID
+    assert L.lacache_ffn_fp8_g(None, a[0], a[1], a[2], a[3], a[4], a[5], a[6], a[7], a[0], 32, 256, 384, 2) == INVALID
+    assert L.lacache_ffn_fp8_g(None, *a[:9], 0, 256, 384, 1) == OK
+    assert L.lacache_ffn_g_workspace_bytes(32, 256, 384) > 0
+    assert L.lacache_ffn_g_workspace_bytes(32, 200, 384) == 0
