@@ -54,6 +54,9 @@ def parse():
     p.add_argument("--workload", default="block32_h4096_i12288",
                    help="an FFN workload, or an attention workload (attn_*): the first-layer FACache attention")
     p.add_argument("--weight-sets", type=int, default=4)
+    p.add_argument("--granularity", action="store_true",
+                   help="time the FFN at the three quantization granularities (per group, per token, per tensor) "
+                        "and report each one's error against the unquantized bf16 FFN")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--eager", action="store_true",
                    help="time the eager host loop instead of the HIP-graph replay of the K steps")
@@ -176,6 +179,9 @@ def main():
 
     if args.workload.startswith("attn_"):
         attention_main(args)
+        return
+    if args.granularity:
+        granularity_main(args)
         return
     w = synth.WORKLOADS[args.workload]
     M, H, I = w.M, w.H, w.I
@@ -417,6 +423,124 @@ def cpu_baseline(w, sets, out, dev):
             "sample": "%d calls of %d of %d rows (one layer each; the FFN is row-independent): %.2f s"
                       % (calls, rows, w.M, t),
             "tokens_per_s": round(rows * calls / t, 3)}
+
+
+def granularity_main(args):
+    """One line for the quantization granularities of the FFN (the paper's
+    per-group scheme against per-token and per-tensor, Table
+    fp8-granularities): a step is one whole FFN call at the headline
+    granularity (per token), timed as a HIP graph of back-to-back calls beside
+    the other two; each granularity's error against the unquantized bf16 FFN
+    (bf16 operands, fp64 arithmetic) on the first rows of the workload."""
+    import numpy as np
+    import torch
+
+    import oracle.ffn as O
+    import paper_2607_16339_amd as lc
+    import synth
+    from oracle.bf16 import bf16_to_f32
+
+    w = synth.WORKLOADS[args.workload]
+    M, H, I = w.M, w.H, w.I
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    lc.lib()
+
+    def dev_bf16(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16).copy()).view(torch.bfloat16).to(dev)
+
+    grans = {"group": lc.LACACHE_GRAN_GROUP, "token": lc.LACACHE_GRAN_TOKEN, "tensor": lc.LACACHE_GRAN_TENSOR}
+    # the weights of several layers per granularity, more bytes than the
+    # Infinity Cache holds, so that every call streams its weights from HBM
+    S = args.weight_sets
+    sets = {name: [] for name in grans}
+    for layer in range(1, S + 1):
+        b = synth.make_weights(w, layer)
+        wgu = dev_bf16(np.concatenate([b["w_gate"], b["w_up"]], axis=0))
+        wd = dev_bf16(b["w_down"])
+        for name, g in grans.items():
+            sets[name].append(lc.quantize_weights_g(wgu, g) + lc.quantize_weights_g(wd, g))
+        del wgu, wd
+    b = synth.make_weights(w, 1)
+    x = dev_bf16(synth.make_x(w, layer=1, step=0))
+    norm_w = dev_bf16(b["norm_w"])
+    out = torch.empty((M, H), dtype=torch.bfloat16, device=dev)
+
+    def call(name, i=0):
+        gq, gs, gr, dq, ds, dr = sets[name][i % S]
+        lc.lacache_ffn_fp8_g(x, norm_w, gq, gs, gr, dq, ds, dr, out, grans[name])
+
+    stream = torch.cuda.current_stream()
+    reps = max(min(args.steps, 64), 8)
+    ms, gate_ms, errs = {}, {}, {}
+    rows = min(M, 8)
+    ref = O.ffn_bf16_reference(synth.make_x(w, layer=1, step=0)[:rows], b["norm_w"], b["w_gate"], b["w_up"],
+                               b["w_down"])
+    for name in grans:
+        for _ in range(args.warmup):
+            call(name)
+        torch.cuda.synchronize()
+        got = bf16_to_f32(out[:rows].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)).astype(np.float64)
+        errs[name] = {"rms_err_rel_to_rms": float(np.sqrt(((got - ref) ** 2).mean() / (ref ** 2).mean())),
+                      "max_err_rel_to_max": float(np.abs(got - ref).max() / np.abs(ref).max())}
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for i in range(reps):
+                call(name, i)
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(3):
+            g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms[name] = e0.elapsed_time(e1) / (3 * reps)
+        del g
+    # the dominant kernel of the coarse path: gate/up + SwiGLU writing fp32 h
+    gq, gs, gr = sets["token"][0][:3]
+    xq = torch.empty((M, H), dtype=torch.uint8, device=dev)
+    xs = torch.empty((H // 128, M), dtype=torch.float32, device=dev)
+    xr = torch.empty((M,), dtype=torch.float32, device=dev)
+    y = torch.empty((M, H), dtype=torch.float32, device=dev)
+    h = torch.empty((M, I), dtype=torch.float32, device=dev)
+    lc.lacache_rmsnorm_f32(x, norm_w, y)
+    lc.lacache_quant_rows_g(y, xq, xs, xr, lc.LACACHE_GRAN_TOKEN)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(reps):
+            gq, gs, gr = sets["token"][i % S][:3]
+            lc.lacache_gateup_swiglu_f32(xq, xs, gq, gs, gr, h)
+    g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(3):
+        g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    k_ms = e0.elapsed_time(e1) / (3 * reps)
+    del g
+    flop = 6.0 * M * H * I
+    ach = 4.0 * M * H * I / (k_ms * 1e-3) / 1e12
+    line = {
+        "metric": "FP8 FFN TFLOP/s per layer at a quantization granularity (per token; per group and per tensor "
+                  "beside it)",
+        "value": round(flop / (ms["token"] * 1e-3) / 1e12, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": reps,
+        "warmup": args.warmup, "ms_per_step": round(ms["token"], 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "fp8_e4m3 (fp32 accumulate)", "data": "synthetic",
+        "config": {"workload": args.workload, "M": M, "H": H, "I": I, "granularity": "token", "weight_sets": S},
+        "ms_per_step_by_granularity": {k: round(v, 5) for k, v in ms.items()},
+        "tflops_by_granularity": {k: round(flop / (v * 1e-3) / 1e12, 1) for k, v in ms.items()},
+        "error_vs_bf16_ffn": errs, "error_rows": rows,
+        "timing": "HIP graph of %d back-to-back calls per granularity, 3 replays" % reps,
+        "roofline": {"bound": "mfma", "achieved": round(ach, 1), "peak": PEAK_FP8_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(ach / PEAK_FP8_TFLOPS, 4), "traffic": None,
+                     "kernel": "gateup_tiled (h-only, per-column scales)", "kernel_ms": round(k_ms, 5),
+                     "algorithmic_flop": 4 * M * H * I},
+    }
+    print(json.dumps(line), flush=True)
 
 
 PEAK_BF16_TFLOPS = 2500.0  # dense bf16 MFMA
