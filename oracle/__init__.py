@@ -25,6 +25,10 @@ csweep  ctypes wrapper of ``e4m3_sweep.c``: the same e4m3 encoder in plain C,
 attention  the first-layer attention and the FACache schedule (Sec. 3.3,
         Eqs. 2-6): plain softmax attention, the online-softmax update and
         the populate / resume steps of the cached state.
+granularity  the per-token and per-tensor quantization granularities
+        compared with the per-group scheme (Sec. 4, Table fp8-granularities).
+first_layer  the token-wise first-layer operators with EmbedCache and
+        RoPECache (Sec. 3.3): embedding, attention norm, QKV projection, RoPE.
 """
 
-from . import attention, bf16, e4m3, ffn  # noqa: F401
+from . import attention, bf16, e4m3, ffn, first_layer, granularity  # noqa: F401
