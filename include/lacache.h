@@ -297,6 +297,57 @@ int lacache_ffn_fp8_g(void* stream, const uint16_t* x, const uint16_t* norm_w, c
 size_t lacache_ffn_g_workspace_bytes(int64_t M, int64_t H, int64_t I);
 
 /*
+ * Token-wise first layer with EmbedCache and RoPECache (Sec. 3.3). Inside a
+ * SAR block only the tokens of the current block C change, so embedding, the
+ * attention RMSNorm, the QKV projection and RoPE run on C's rows only and
+ * write into cached tensors that hold every row of the sequence: the
+ * embedding cache [N x H] and Q, K, V [heads x N x 128] (the attention layout
+ * of lacache_facache_attention). The first layer keeps 16-bit precision
+ * (Sec. 3.4): bf16 values, fp32 arithmetic. A call with rows = 0..N-1 fills
+ * the caches (the block's first step); a call with C's rows updates them, and
+ * the result equals the full call on the new tokens bit for bit. Row indices
+ * must be distinct within a call. Token ids outside [0, vocab) and row indices
+ * outside [0, N) are device data the host cannot check: the kernels skip such
+ * entries (nothing is read or written for them).
+ *
+ * lacache_embed_rmsnorm: x_r = embed[token_ids[r]] ([vocab x H] bf16) is
+ *   written to embed_cache[rows[r]], and y[r] = RNE_bf16(RMSNorm(x_r)) with the
+ *   arithmetic of lacache_rmsnorm_quant (eps 1e-5, fp64 sum of squares in its
+ *   fixed order, y = RN32(RN32(x w) r)). token_ids, rows: [R] int32.
+ */
+int lacache_embed_rmsnorm(void* stream, const int32_t* token_ids, const int32_t* rows, int64_t R,
+                          const uint16_t* embed, int64_t vocab, const uint16_t* norm_w, uint16_t* embed_cache,
+                          int64_t N, uint16_t* y, int64_t H);
+
+/* out [M x N] bf16 = RNE_bf16(a [M x K] W[N x K]^T), bf16 inputs, fp32
+ * accumulation (bf16 MFMAs; the K range is split over four partial sums added
+ * in a fixed order); out_tap (nullable) receives the fp32 result. Streams W
+ * from HBM once per 64 rows of a: meant for the few rows of a block. */
+int lacache_linear_bf16(void* stream, const uint16_t* a, const uint16_t* w, uint16_t* out, float* out_tap, int64_t M,
+                        int64_t N, int64_t K);
+
+/*
+ * RoPE and scatter: row r of qkv ([R x 3 heads 128] bf16, columns = Q heads,
+ * then K heads, then V heads, 128 each) goes to row rows[r] of q, k, v
+ * ([heads x N x 128] bf16). Q and K are rotated (rotate-half form): for the
+ * pair (i, i + 64) of a head, i < 64, with c = rope_cos[p*64 + i] and
+ * s = rope_sin[p*64 + i] (p = rows[r]; fp32 tables [N x 64]),
+ *   out_i = RNE_bf16(RN32(x_i c) - RN32(x_{i+64} s)),
+ *   out_{i+64} = RNE_bf16(RN32(x_{i+64} c) + RN32(x_i s)); V is copied.
+ */
+int lacache_rope_scatter(void* stream, const uint16_t* qkv, const int32_t* rows, int64_t R, const float* rope_cos,
+                         const float* rope_sin, uint16_t* q, uint16_t* k, uint16_t* v, int64_t heads, int64_t N);
+
+/* The three steps above in one call (embedding + norm, the QKV projection
+ * with w_qkv [3 heads 128 x H] bf16, RoPE + scatter), with a library-owned
+ * workspace of lacache_first_layer_workspace_bytes(R, heads, H) bytes. */
+int lacache_first_layer_tokens(void* stream, const int32_t* token_ids, const int32_t* rows, int64_t R,
+                               const uint16_t* embed, int64_t vocab, const uint16_t* norm_w, const uint16_t* w_qkv,
+                               const float* rope_cos, const float* rope_sin, uint16_t* embed_cache, uint16_t* q,
+                               uint16_t* k, uint16_t* v, int64_t heads, int64_t N, int64_t H);
+size_t lacache_first_layer_workspace_bytes(int64_t R, int64_t heads, int64_t H);
+
+/*
  * Kernel-path policy for the GEMM stages, process-wide:
  *   0 = automatic (the skinny weight-streaming kernels for M <= 64,
  *       H <= 8192 and I <= 16384, the tiled MFMA kernels otherwise), 1 = always skinny

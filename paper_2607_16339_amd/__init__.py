@@ -231,6 +231,57 @@ def quantize_weights_g(w, granularity, stream=None):
     return w_q, w_s, w_row_s
 
 
+# ---- token-wise first layer (EmbedCache, RoPECache) -------------------------
+
+_I32 = (torch.int32,)
+
+
+def lacache_embed_rmsnorm(token_ids, rows, embed, norm_w, embed_cache, y, stream=None):
+    """token_ids, rows [R] int32; embed [vocab, H] bf16 -> embed_cache rows, y [R, H] bf16."""
+    R = token_ids.shape[0]
+    vocab, H = embed.shape
+    N = embed_cache.shape[0]
+    check(lib().lacache_embed_rmsnorm(
+        _stream(stream, embed), _ptr(token_ids, _I32, "token_ids", (R,)), _ptr(rows, _I32, "rows", (R,)), R,
+        _ptr(embed, _BF16, "embed"), vocab, _ptr(norm_w, _BF16, "norm_w", (H,)),
+        _ptr(embed_cache, _BF16, "embed_cache", (N, H)), N, _ptr(y, _BF16, "y", (R, H)), H), "lacache_embed_rmsnorm")
+
+
+def lacache_linear_bf16(a, w, out, out_tap=None, stream=None):
+    """out [M, N] bf16 = a [M, K] w[N, K]^T (fp32 accumulation)."""
+    M, K = a.shape
+    N = w.shape[0]
+    check(lib().lacache_linear_bf16(
+        _stream(stream, a), _ptr(a, _BF16, "a"), _ptr(w, _BF16, "w", (N, K)), _ptr(out, _BF16, "out", (M, N)),
+        _ptr(out_tap, _F32, "out_tap", (M, N), optional=True), M, N, K), "lacache_linear_bf16")
+
+
+def lacache_rope_scatter(qkv, rows, rope_cos, rope_sin, q, k, v, stream=None):
+    """qkv [R, 3 heads 128] bf16 -> RoPE(Q, K) and V scattered to rows of q, k, v [heads, N, 128]."""
+    R = qkv.shape[0]
+    heads, N, d = q.shape
+    check(lib().lacache_rope_scatter(
+        _stream(stream, qkv), _ptr(qkv, _BF16, "qkv", (R, 3 * heads * d)), _ptr(rows, _I32, "rows", (R,)), R,
+        _ptr(rope_cos, _F32, "rope_cos", (N, 64)), _ptr(rope_sin, _F32, "rope_sin", (N, 64)),
+        _ptr(q, _BF16, "q"), _ptr(k, _BF16, "k", (heads, N, d)), _ptr(v, _BF16, "v", (heads, N, d)), heads, N),
+        "lacache_rope_scatter")
+
+
+def lacache_first_layer_tokens(token_ids, rows, embed, norm_w, w_qkv, rope_cos, rope_sin, embed_cache, q, k, v,
+                               stream=None):
+    """The token-wise first layer for the given rows: embedding + norm, QKV projection, RoPE + scatter."""
+    R = token_ids.shape[0]
+    vocab, H = embed.shape
+    heads, N, d = q.shape
+    check(lib().lacache_first_layer_tokens(
+        _stream(stream, embed), _ptr(token_ids, _I32, "token_ids", (R,)), _ptr(rows, _I32, "rows", (R,)), R,
+        _ptr(embed, _BF16, "embed"), vocab, _ptr(norm_w, _BF16, "norm_w", (H,)),
+        _ptr(w_qkv, _BF16, "w_qkv", (3 * heads * d, H)), _ptr(rope_cos, _F32, "rope_cos", (N, 64)),
+        _ptr(rope_sin, _F32, "rope_sin", (N, 64)), _ptr(embed_cache, _BF16, "embed_cache", (N, H)),
+        _ptr(q, _BF16, "q"), _ptr(k, _BF16, "k", (heads, N, d)), _ptr(v, _BF16, "v", (heads, N, d)), heads, N, H),
+        "lacache_first_layer_tokens")
+
+
 def lacache_set_path_policy(policy):
     """0 = automatic, 1 = skinny kernels (M <= 64), 2 = tiled kernels. Returns the previous policy."""
     r = lib().lacache_set_path_policy(int(policy))

@@ -40,6 +40,12 @@ SIGNATURES = {
     "lacache_down_proj_g": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I]),
     "lacache_ffn_fp8_g": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I]),
     "lacache_ffn_g_workspace_bytes": (ctypes.c_size_t, [_I64, _I64, _I64]),
+    "lacache_embed_rmsnorm": (_I, [_P, _P, _P, _I64, _P, _I64, _P, _P, _I64, _P, _I64]),
+    "lacache_linear_bf16": (_I, [_P, _P, _P, _P, _P, _I64, _I64, _I64]),
+    "lacache_rope_scatter": (_I, [_P, _P, _P, _I64, _P, _P, _P, _P, _P, _I64, _I64]),
+    "lacache_first_layer_tokens": (_I, [_P, _P, _P, _I64, _P, _I64, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64,
+                                        _I64]),
+    "lacache_first_layer_workspace_bytes": (ctypes.c_size_t, [_I64, _I64, _I64]),
     "lacache_set_path_policy": (_I, [_I]),
     "lacache_status_string": (ctypes.c_char_p, [_I]),
     "lacache_release_workspace": (None, []),

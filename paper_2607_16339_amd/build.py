@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "liblacache.so")
-SOURCES = ["quant.hip", "gemm_tiled.hip", "gemm_skinny.hip", "granularity.hip", "attention.hip", "api.hip"]
+SOURCES = ["quant.hip", "gemm_tiled.hip", "gemm_skinny.hip", "granularity.hip", "first_layer.hip", "attention.hip", "api.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

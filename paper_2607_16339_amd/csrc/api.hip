@@ -475,6 +475,83 @@ int lacache_ffn_fp8_g(void* stream, const uint16_t* x, const uint16_t* norm_w, c
   return hip_status(launch_down_tiled(st, hq, hs, wd_q, wd_s, out, nullptr, M, H, I, part, wd_row_s));
 }
 
+// ---------------------------------------------------------------------------
+// Token-wise first layer (EmbedCache, RoPECache)
+// ---------------------------------------------------------------------------
+
+int lacache_embed_rmsnorm(void* stream, const int32_t* token_ids, const int32_t* rows, int64_t R,
+                          const uint16_t* embed, int64_t vocab, const uint16_t* norm_w, uint16_t* embed_cache,
+                          int64_t N, uint16_t* y, int64_t H) {
+  if (R < 0 || vocab <= 0 || N <= 0) return LACACHE_ERR_INVALID_ARG;
+  RETURN_IF(check_dim(H, kMaxH));
+  if (R > kMaxM || N > kMaxM) return LACACHE_ERR_UNSUPPORTED;
+  if (R == 0) return LACACHE_OK;
+  if (!ptrs_ok({token_ids, rows, embed, norm_w, embed_cache, y})) return LACACHE_ERR_INVALID_ARG;
+  const size_t hb = static_cast<size_t>(H) * 2;
+  if (!disjoint({rng(embed_cache, N * hb), rng(y, R * hb)},
+                {rng(token_ids, R * 4), rng(rows, R * 4), rng(embed, vocab * hb), rng(norm_w, hb)}))
+    return LACACHE_ERR_INVALID_ARG;
+  return hip_status(launch_embed_rmsnorm(static_cast<hipStream_t>(stream), token_ids, rows, R, embed, vocab, norm_w,
+                                         embed_cache, N, y, H));
+}
+
+int lacache_linear_bf16(void* stream, const uint16_t* a, const uint16_t* w, uint16_t* out, float* out_tap, int64_t M,
+                        int64_t N, int64_t K) {
+  RETURN_IF(check_m(M));
+  RETURN_IF(check_dim(N, kMaxN));
+  RETURN_IF(check_dim(K, kMaxN));
+  if (M == 0) return LACACHE_OK;
+  if (!ptrs_ok({a, w, out}) || !opt_ptr_ok(out_tap)) return LACACHE_ERR_INVALID_ARG;
+  if (!disjoint({rng(out, M * N * 2), rng(out_tap, out_tap ? M * N * 4 : 0)}, {rng(a, M * K * 2), rng(w, N * K * 2)}))
+    return LACACHE_ERR_INVALID_ARG;
+  return hip_status(launch_linear_bf16(static_cast<hipStream_t>(stream), a, w, out, out_tap, M, N, K));
+}
+
+int lacache_rope_scatter(void* stream, const uint16_t* qkv, const int32_t* rows, int64_t R, const float* rope_cos,
+                         const float* rope_sin, uint16_t* q, uint16_t* k, uint16_t* v, int64_t heads, int64_t N) {
+  if (R < 0 || heads <= 0 || N <= 0) return LACACHE_ERR_INVALID_ARG;
+  if (heads > kAttnMaxHeads || N > kAttnMaxN || R > kMaxM) return LACACHE_ERR_UNSUPPORTED;
+  if (R == 0) return LACACHE_OK;
+  if (!ptrs_ok({qkv, rows, rope_cos, rope_sin, q, k, v})) return LACACHE_ERR_INVALID_ARG;
+  const size_t cache = static_cast<size_t>(heads * N) * 128 * 2, tab = static_cast<size_t>(N) * 64 * 4;
+  if (!disjoint({rng(q, cache), rng(k, cache), rng(v, cache)},
+                {rng(qkv, R * 3 * heads * 128 * 2), rng(rows, R * 4), rng(rope_cos, tab), rng(rope_sin, tab)}))
+    return LACACHE_ERR_INVALID_ARG;
+  return hip_status(launch_rope_scatter(static_cast<hipStream_t>(stream), qkv, rows, R, rope_cos, rope_sin, q, k, v,
+                                        heads, N));
+}
+
+size_t lacache_first_layer_workspace_bytes(int64_t R, int64_t heads, int64_t H) {
+  if (R < 0 || heads <= 0 || check_dim(H, kMaxH) != LACACHE_OK) return 0;
+  return align256(static_cast<size_t>(R * H) * 2) + align256(static_cast<size_t>(R * 3 * heads * 128) * 2);
+}
+
+int lacache_first_layer_tokens(void* stream, const int32_t* token_ids, const int32_t* rows, int64_t R,
+                               const uint16_t* embed, int64_t vocab, const uint16_t* norm_w, const uint16_t* w_qkv,
+                               const float* rope_cos, const float* rope_sin, uint16_t* embed_cache, uint16_t* q,
+                               uint16_t* k, uint16_t* v, int64_t heads, int64_t N, int64_t H) {
+  if (R < 0 || vocab <= 0 || N <= 0 || heads <= 0) return LACACHE_ERR_INVALID_ARG;
+  RETURN_IF(check_dim(H, kMaxH));
+  if (heads > kAttnMaxHeads || N > kAttnMaxN || R > kMaxM || 3 * heads * 128 > kMaxN) return LACACHE_ERR_UNSUPPORTED;
+  if (R == 0) return LACACHE_OK;
+  if (!ptrs_ok({token_ids, rows, embed, norm_w, w_qkv, rope_cos, rope_sin, embed_cache, q, k, v}))
+    return LACACHE_ERR_INVALID_ARG;
+  const size_t hb = static_cast<size_t>(H) * 2, cache = static_cast<size_t>(heads * N) * 128 * 2;
+  const size_t tab = static_cast<size_t>(N) * 64 * 4, nq = static_cast<size_t>(3 * heads * 128);
+  if (!disjoint({rng(embed_cache, N * hb), rng(q, cache), rng(k, cache), rng(v, cache)},
+                {rng(token_ids, R * 4), rng(rows, R * 4), rng(embed, vocab * hb), rng(norm_w, hb),
+                 rng(w_qkv, nq * hb), rng(rope_cos, tab), rng(rope_sin, tab)}))
+    return LACACHE_ERR_INVALID_ARG;
+  void* base = nullptr;
+  RETURN_IF(get_workspace(lacache_first_layer_workspace_bytes(R, heads, H), &base));
+  uint16_t* y = static_cast<uint16_t*>(base);
+  uint16_t* qkv = reinterpret_cast<uint16_t*>(static_cast<char*>(base) + align256(static_cast<size_t>(R * H) * 2));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  RETURN_IF(hip_status(launch_embed_rmsnorm(st, token_ids, rows, R, embed, vocab, norm_w, embed_cache, N, y, H)));
+  RETURN_IF(hip_status(launch_linear_bf16(st, y, w_qkv, qkv, nullptr, R, static_cast<int64_t>(nq), H)));
+  return hip_status(launch_rope_scatter(st, qkv, rows, R, rope_cos, rope_sin, q, k, v, heads, N));
+}
+
 int lacache_add_bf16(void* stream, uint16_t* x_inout, const uint16_t* y, int64_t n) {
   if (n < 0) return LACACHE_ERR_INVALID_ARG;
   if (n == 0) return LACACHE_OK;

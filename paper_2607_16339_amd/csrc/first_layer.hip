@@ -1,0 +1,276 @@
+// Token-wise first-layer operators with EmbedCache and RoPECache (Sec. 3.3):
+// inside a SAR block only the rows of the current block C change, so the
+// embedding, the attention RMSNorm, the QKV projection and RoPE run on those
+// rows only and write their results into the cached tensors (the embedding
+// cache [N x H] and Q, K, V [heads x N x 128] in the attention layout). The
+// first layer keeps 16-bit precision (Sec. 3.4): bf16 storage, fp32
+// arithmetic.
+//
+//   embed_rmsnorm_kernel  one wavefront per row: gather the token's embedding
+//                         row, write it to the embedding cache, RMSNorm (the
+//                         fused FFN quantizer's arithmetic: fp64 sum of squares
+//                         in the same fixed order) rounded to bf16;
+//   linear_bf16_kernel    out = a W^T for a few rows: 16 weight rows per
+//                         workgroup streamed from HBM once per 64 activation
+//                         rows, K split over the 4 wavefronts (private
+//                         direct-to-LDS rings), bf16 MFMAs into fp32, the four
+//                         partials added in wavefront order, bf16 out;
+//   rope_scatter_kernel   rotate-half RoPE of the Q and K heads from fp32 cos /
+//                         sin tables, V unrotated, scattered to each row's
+//                         position in Q, K, V.
+// Token ids outside [0, vocab) and row indices outside [0, N) are skipped on
+// the device (no access is made for them).
+#include "device.h"
+#include "launch.h"
+
+namespace lacache {
+namespace {
+
+typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
+
+template <int T>
+__global__ __launch_bounds__(256) void embed_rmsnorm_kernel(const int32_t* __restrict__ ids,
+                                                            const int32_t* __restrict__ rows, int64_t R,
+                                                            const uint16_t* __restrict__ embed, int64_t vocab,
+                                                            const uint16_t* __restrict__ nw,
+                                                            uint16_t* __restrict__ cache, int64_t N,
+                                                            uint16_t* __restrict__ y, int H) {
+  const int lane = threadIdx.x & 63;
+  const int64_t r = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (r >= R) return;  // uniform per wavefront
+  const int64_t id = ids[r], pos = rows[r];
+  if (id < 0 || id >= vocab || pos < 0 || pos >= N) return;
+  const int nchunk = H >> 3;
+  const uint4* xr = reinterpret_cast<const uint4*>(embed + id * H);
+  const uint4* wr = reinterpret_cast<const uint4*>(nw);
+  uint4 xv[T], wv[T];
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    const int c = t * 64 + lane;
+    const int cc = c < nchunk ? c : nchunk - 1;
+    xv[t] = xr[cc];
+    wv[t] = wr[cc];
+  }
+  uint4* cw = reinterpret_cast<uint4*>(cache + pos * H);  // EmbedCache row
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    if (t * 64 + lane < nchunk)
+      cw[t * 64 + lane] = xv[t];
+    else
+      xv[t] = make_uint4(0u, 0u, 0u, 0u);
+  }
+  // fp64 sum of squares: per-lane partials in increasing element index, then
+  // a xor butterfly over offsets 32..1 (every lane ends with the same bits)
+  double p = 0.0;
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    const uint32_t q[4] = {xv[t].x, xv[t].y, xv[t].z, xv[t].w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const double a = bf16lo(q[e]), b = bf16hi(q[e]);
+      p = p + a * a;
+      p = p + b * b;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) p = p + __shfl_xor(p, o, 64);
+  const float rs = static_cast<float>(1.0 / __builtin_sqrt(p / static_cast<double>(H) + 1e-5));
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    const int c = t * 64 + lane;
+    if (c >= nchunk) continue;
+    const uint32_t q[4] = {xv[t].x, xv[t].y, xv[t].z, xv[t].w};
+    const uint32_t g[4] = {wv[t].x, wv[t].y, wv[t].z, wv[t].w};
+    uint32_t o[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      o[e] = pack_bf16x2((bf16lo(q[e]) * bf16lo(g[e])) * rs, (bf16hi(q[e]) * bf16hi(g[e])) * rs);
+    reinterpret_cast<uint4*>(y + r * H)[c] = make_uint4(o[0], o[1], o[2], o[3]);
+  }
+}
+
+// out [M x N] = a [M x K] W[N x K]^T, bf16 in and out, fp32 accumulation.
+// Workgroup (blockIdx.x, blockIdx.y): weight rows 16 x .. + 15, activation
+// rows 64 y .. + 63 (MT slabs of 16 rows). Its 4 wavefronts take a quarter of
+// the K range each; a K-step is 64 elements (128 bytes of a row), staged
+// global -> LDS as [rows][128 B] with the 16-byte chunk c of row r at
+// c ^ (r mod 8); each 16x16 tile gets two 16x16x32 bf16 MFMAs per K-step (the
+// lanes' chunks q and 4 + q).
+constexpr int kLinSplit = 4;
+
+template <int MT>
+struct LinCfg {
+  static constexpr int RA = MT * 16;
+  static constexpr int kA = RA * 128;
+  static constexpr int kSlot = kA + 16 * 128;
+  static constexpr int AI = RA / 8;  // 1 KB copies of activations per slot
+  static constexpr int PER = AI + 2;
+  static constexpr int D = MT == 1 ? 8 : (MT == 2 ? 5 : (MT == 3 ? 4 : 3));
+};
+
+__device__ __forceinline__ void lin_frag(const uint8_t* rows, int lr, int q, bf8& lo, bf8& hi) {
+  const uint8_t* row = rows + lr * 128;
+  lo = *reinterpret_cast<const bf8*>(row + ((q ^ (lr & 7)) << 4));
+  hi = *reinterpret_cast<const bf8*>(row + (((4 + q) ^ (lr & 7)) << 4));
+}
+
+template <int MT>
+__global__ __launch_bounds__(kLinSplit * 64) void linear_bf16_kernel(const uint16_t* __restrict__ a,
+                                                                     const uint16_t* __restrict__ w,
+                                                                     uint16_t* __restrict__ out,
+                                                                     float* __restrict__ out_tap, int64_t M,
+                                                                     int64_t N, int64_t K) {
+  using C = LinCfg<MT>;
+  constexpr int D = C::D, RA = C::RA;
+  __shared__ __align__(16) uint8_t ring[kLinSplit][D * C::kSlot];
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = wave_uniform(t >> 6);
+  const int q = lane >> 4, lr = lane & 15;
+  const int64_t n0 = static_cast<int64_t>(blockIdx.x) * 16;
+  const int64_t m0 = static_cast<int64_t>(blockIdx.y) * 64;
+  const int64_t KS = K / 64;  // K-steps
+  const int64_t ks0 = wave * KS / kLinSplit, ks1 = (wave + 1) * KS / kLinSplit;
+  const int nks = static_cast<int>(ks1 - ks0);
+  uint8_t* my = ring[wave];
+  const uint8_t* ab = reinterpret_cast<const uint8_t*>(a);
+  const uint8_t* wb = reinterpret_cast<const uint8_t*>(w);
+
+  // copy plan: instruction u fills slot rows 8u..8u+7; lane l fills row
+  // 8u + l/8, physical chunk l%8 (logical chunk (l%8) ^ (row & 7))
+  const int crow = lane >> 3, pch = lane & 7;
+  int64_t a_off[C::AI];
+#pragma unroll
+  for (int u = 0; u < C::AI; ++u) {
+    const int row = 8 * u + crow;
+    const int64_t gr = m0 + row < M ? m0 + row : M - 1;
+    a_off[u] = gr * K * 2 + ((pch ^ (row & 7)) << 4);
+  }
+  int64_t w_off[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int row = 8 * u + crow;
+    w_off[u] = (n0 + row) * K * 2 + ((pch ^ (row & 7)) << 4);
+  }
+  auto issue = [&](int s, int slot) {
+    const int64_t kb = (ks0 + (s < nks ? s : nks - 1)) * 128;  // byte offset of the K-step
+    const uint32_t base = lds_u32(my + slot * C::kSlot);
+#pragma unroll
+    for (int u = 0; u < C::AI; ++u) dma16(ab + a_off[u] + kb, wave_uniform(static_cast<int>(base) + u * 1024));
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+      dma16(wb + w_off[u] + kb, wave_uniform(static_cast<int>(base) + C::kA + u * 1024));
+  };
+  if (nks > 0) {
+#pragma unroll
+    for (int s = 0; s < D - 1; ++s) issue(s, s);
+  }
+  v4f acc[MT];
+#pragma unroll
+  for (int i = 0; i < MT; ++i) acc[i] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+  for (int s = 0; s < nks; ++s) {
+    wait_vm_lds<(D - 2) * C::PER>();  // step s has landed; slot (s-1) % D is read
+    issue(s + D - 1, (s + D - 1) % D);
+    const uint8_t* slot = my + (s % D) * C::kSlot;
+    bf8 blo, bhi;
+    lin_frag(slot + C::kA, lr, q, blo, bhi);
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      bf8 alo, ahi;
+      lin_frag(slot + i * 16 * 128, lr, q, alo, ahi);
+      acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, blo, acc[i], 0, 0, 0);
+      acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, bhi, acc[i], 0, 0, 0);
+    }
+  }
+  wait_vm<0>();
+  __syncthreads();  // every ring is idle: reuse it for the partials
+  float* red = reinterpret_cast<float*>(&ring[0][0]);
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) red[(wave * RA + 16 * i + 4 * q + r) * 16 + lr] = acc[i][r];
+  __syncthreads();
+  for (int e = t; e < RA * 16; e += kLinSplit * 64) {
+    const int row = e >> 4, col = e & 15;
+    if (m0 + row >= M) continue;
+    float sum = red[row * 16 + col];
+#pragma unroll
+    for (int wv = 1; wv < kLinSplit; ++wv) sum += red[(wv * RA + row) * 16 + col];
+    out[(m0 + row) * N + n0 + col] = static_cast<uint16_t>(f32_to_bf16(sum));
+    if (out_tap != nullptr) out_tap[(m0 + row) * N + n0 + col] = sum;
+  }
+}
+
+// One thread per (row r, Q/K/V part, head, pair i < 64): the pair (i, i + 64)
+// of the head's 128 values; Q and K rotated by the angle of the row's position.
+__global__ __launch_bounds__(256) void rope_scatter_kernel(const uint16_t* __restrict__ qkv,
+                                                           const int32_t* __restrict__ rows, int64_t R,
+                                                           const float* __restrict__ cs, const float* __restrict__ sn,
+                                                           uint16_t* __restrict__ q, uint16_t* __restrict__ k,
+                                                           uint16_t* __restrict__ v, int64_t heads, int64_t N) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t per_row = 3 * heads * 64;
+  if (e >= R * per_row) return;
+  const int64_t r = e / per_row;
+  const int64_t rem = e - r * per_row;
+  const int part = static_cast<int>(rem / (heads * 64));
+  const int64_t h = (rem / 64) % heads;
+  const int i = static_cast<int>(rem & 63);
+  const int64_t pos = rows[r];
+  if (pos < 0 || pos >= N) return;
+  const uint16_t* src = qkv + r * 3 * heads * 128 + (part * heads + h) * 128;
+  uint16_t* dst = (part == 0 ? q : (part == 1 ? k : v)) + (h * N + pos) * 128;
+  const uint16_t x1 = src[i], x2 = src[64 + i];
+  if (part == 2) {
+    dst[i] = x1;
+    dst[64 + i] = x2;
+    return;
+  }
+  const float a = bf16lo(x1), b = bf16lo(x2), c = cs[pos * 64 + i], s = sn[pos * 64 + i];
+  dst[i] = static_cast<uint16_t>(f32_to_bf16(a * c - b * s));
+  dst[64 + i] = static_cast<uint16_t>(f32_to_bf16(b * c + a * s));
+}
+
+}  // namespace
+
+hipError_t launch_embed_rmsnorm(hipStream_t st, const int32_t* ids, const int32_t* rows, int64_t R,
+                                const uint16_t* embed, int64_t vocab, const uint16_t* nw, uint16_t* cache, int64_t N,
+                                uint16_t* y, int64_t H) {
+  const int T = static_cast<int>((H + 511) / 512);
+  const dim3 grid(static_cast<unsigned>((R + 3) / 4)), block(256);
+  const int h = static_cast<int>(H);
+#define ER(T_) \
+  hipLaunchKernelGGL(embed_rmsnorm_kernel<T_>, grid, block, 0, st, ids, rows, R, embed, vocab, nw, cache, N, y, h)
+  if (T <= 1) ER(1);
+  else if (T <= 2) ER(2);
+  else if (T <= 4) ER(4);
+  else if (T <= 8) ER(8);
+  else if (T <= 16) ER(16);
+  else ER(32);
+#undef ER
+  return hipGetLastError();
+}
+
+hipError_t launch_linear_bf16(hipStream_t st, const uint16_t* a, const uint16_t* w, uint16_t* out, float* out_tap,
+                              int64_t M, int64_t N, int64_t K) {
+  // up to 64 rows per pass; the last pass may hold fewer slabs
+  const unsigned passes = static_cast<unsigned>((M + 63) / 64);
+  const dim3 grid(static_cast<unsigned>(N / 16), passes), block(kLinSplit * 64);
+  const int mt = static_cast<int>(M >= 64 ? 4 : (M + 15) / 16);
+#define LB(MT_) hipLaunchKernelGGL(linear_bf16_kernel<MT_>, grid, block, 0, st, a, w, out, out_tap, M, N, K)
+  if (mt <= 1) LB(1);
+  else if (mt == 2) LB(2);
+  else if (mt == 3) LB(3);
+  else LB(4);
+#undef LB
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_scatter(hipStream_t st, const uint16_t* qkv, const int32_t* rows, int64_t R, const float* cs,
+                               const float* sn, uint16_t* q, uint16_t* k, uint16_t* v, int64_t heads, int64_t N) {
+  const int64_t threads = R * 3 * heads * 64;
+  hipLaunchKernelGGL(rope_scatter_kernel, dim3(static_cast<unsigned>((threads + 255) / 256)), dim3(256), 0, st, qkv,
+                     rows, R, cs, sn, q, k, v, heads, N);
+  return hipGetLastError();
+}
+
+}  // namespace lacache

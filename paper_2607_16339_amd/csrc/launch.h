@@ -78,6 +78,16 @@ hipError_t launch_gateup_skinny(hipStream_t st, const uint8_t* xq, const float* 
 hipError_t launch_down_skinny(hipStream_t st, const uint8_t* hq, const float* hs, const uint8_t* wq, const float* ws,
                               uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I);
 
+// Token-wise first layer (EmbedCache / RoPECache). Ids outside [0, vocab)
+// and rows outside [0, N) are skipped on the device.
+hipError_t launch_embed_rmsnorm(hipStream_t st, const int32_t* ids, const int32_t* rows, int64_t R,
+                                const uint16_t* embed, int64_t vocab, const uint16_t* nw, uint16_t* cache, int64_t N,
+                                uint16_t* y, int64_t H);
+hipError_t launch_linear_bf16(hipStream_t st, const uint16_t* a, const uint16_t* w, uint16_t* out, float* out_tap,
+                              int64_t M, int64_t N, int64_t K);
+hipError_t launch_rope_scatter(hipStream_t st, const uint16_t* qkv, const int32_t* rows, int64_t R, const float* cs,
+                               const float* sn, uint16_t* q, uint16_t* k, uint16_t* v, int64_t heads, int64_t N);
+
 // First-layer attention with FACache: heads x N x 128 bf16, N % 64 == 0;
 // mode 0 populate, 1 resume, 2 plain (cache pointers unused).
 hipError_t launch_facache_attention(hipStream_t st, const uint16_t* q, const uint16_t* k, const uint16_t* v,

@@ -257,3 +257,31 @@ def test_granularity_validation(L):
     assert L.lacache_ffn_fp8_g(None, *a[:9], 0, 256, 384, 1) == OK
     assert L.lacache_ffn_g_workspace_bytes(32, 256, 384) > 0
     assert L.lacache_ffn_g_workspace_bytes(32, 200, 384) == 0
+
+
+def test_first_layer_validation(L):
+    f = Fake()
+    ids, rows, emb, nw, cache, y = f(), f(), f(), f(), f(), f()
+    assert L.lacache_embed_rmsnorm(None, ids, rows, -1, emb, 100, nw, cache, 64, y, 256) == INVALID
+    assert L.lacache_embed_rmsnorm(None, ids, rows, 4, emb, 0, nw, cache, 64, y, 256) == INVALID
+    assert L.lacache_embed_rmsnorm(None, ids, rows, 4, emb, 100, nw, cache, 64, y, 200) == INVALID
+    assert L.lacache_embed_rmsnorm(None, ids, rows, 4, emb, 100, nw, emb, 64, y, 256) == INVALID
+    assert L.lacache_embed_rmsnorm(None, ids + 4, rows, 4, emb, 100, nw, cache, 64, y, 256) == INVALID
+    assert L.lacache_embed_rmsnorm(None, ids, rows, 0, emb, 100, nw, cache, 64, y, 256) == OK
+    a, w, out = f(), f(), f()
+    assert L.lacache_linear_bf16(None, a, w, out, None, 4, 384, 200) == INVALID
+    assert L.lacache_linear_bf16(None, a, w, a, None, 4, 384, 256) == INVALID
+    assert L.lacache_linear_bf16(None, a, w, out, out + 4, 4, 384, 256) == INVALID
+    assert L.lacache_linear_bf16(None, a, w, out, None, 0, 384, 256) == OK
+    qkv, cs, sn, q, k, v = f(), f(), f(), f(), f(), f()
+    assert L.lacache_rope_scatter(None, qkv, rows, 4, cs, sn, q, k, v, 0, 64) == INVALID
+    assert L.lacache_rope_scatter(None, qkv, rows, 4, cs, sn, q, q, v, 2, 64) == INVALID
+    assert L.lacache_rope_scatter(None, qkv, rows, 4, cs, sn, q, k, v, 5000, 64) == UNSUP
+    assert L.lacache_rope_scatter(None, qkv, rows, 0, cs, sn, q, k, v, 2, 64) == OK
+    wq = f()
+    assert L.lacache_first_layer_tokens(None, ids, rows, 4, emb, 100, nw, wq, cs, sn, cache, q, k, v, 2, 64, 200) \
+        == INVALID
+    assert L.lacache_first_layer_tokens(None, ids, rows, 4, emb, 100, nw, wq, cs, sn, q, q, k, v, 2, 64, 256) \
+        == INVALID
+    assert L.lacache_first_layer_tokens(None, ids, rows, 0, emb, 100, nw, wq, cs, sn, cache, q, k, v, 2, 64, 256) == OK
+    assert L.lacache_first_layer_workspace_bytes(32, 32, 4096) > 0
