@@ -52,7 +52,8 @@ def parse():
     p.add_argument("--steps", type=int, default=50)
     p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--workload", default="block32_h4096_i12288",
-                   help="an FFN workload, or an attention workload (attn_*): the first-layer FACache attention")
+                   help="an FFN workload, an attention workload (attn_*: the first-layer FACache attention), or "
+                        "first_layer_n512 (the token-wise first layer with EmbedCache / RoPECache)")
     p.add_argument("--weight-sets", type=int, default=4)
     p.add_argument("--granularity", action="store_true",
                    help="time the FFN at the three quantization granularities (per group, per token, per tensor) "
@@ -182,6 +183,9 @@ def main():
         return
     if args.granularity:
         granularity_main(args)
+        return
+    if args.workload.startswith("first_layer"):
+        first_layer_main(args)
         return
     w = synth.WORKLOADS[args.workload]
     M, H, I = w.M, w.H, w.I
@@ -540,6 +544,113 @@ def granularity_main(args):
                      "kernel": "gateup_tiled (h-only, per-column scales)", "kernel_ms": round(k_ms, 5),
                      "algorithmic_flop": 4 * M * H * I},
     }
+    print(json.dumps(line), flush=True)
+
+
+def first_layer_main(args):
+    """One line for the token-wise first layer (EmbedCache / RoPECache,
+    Sec. 3.3) at the LLaDA-8B shape (H = 4096, 32 heads of 128, vocabulary
+    126464): a step is the update of one 32-token block of a 512-token
+    sequence (embedding + norm, QKV projection, RoPE + scatter of those rows);
+    the full recompute of all 512 rows (the block's first step) is timed
+    beside it. Inputs are seeded synthetic (token ids, embedding table,
+    weights); 4 rotating QKV weight sets keep the projection streaming from
+    HBM."""
+    import numpy as np
+    import torch
+
+    import paper_2607_16339_amd as lc
+
+    H, heads, N, vocab, Cn, D = 4096, 32, 512, 126464, 32, 128
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    lc.lib()
+    g = torch.Generator(device="cpu").manual_seed(260716339)
+    S = args.weight_sets
+
+    def bf16_randn(shape, std):
+        return (torch.randn(shape, generator=g) * std).to(torch.bfloat16).to(dev)
+
+    embed = bf16_randn((vocab, H), 1.0)
+    norm_w = (1.0 + torch.randn((H,), generator=g) * 0.02).to(torch.bfloat16).to(dev)
+    wqkv = [bf16_randn((3 * heads * D, H), 0.02) for _ in range(S)]
+    i = torch.arange(D // 2, dtype=torch.float64)
+    ang = torch.arange(N, dtype=torch.float64)[:, None] * torch.pow(torch.tensor(500000.0, dtype=torch.float64),
+                                                                     -2.0 * i / D)[None, :]
+    rc, rs = torch.cos(ang).float().to(dev), torch.sin(ang).float().to(dev)
+    caches = [torch.empty((N, H), dtype=torch.bfloat16, device=dev)] + [
+        torch.empty((heads, N, D), dtype=torch.bfloat16, device=dev) for _ in range(3)]
+    ids = torch.randint(0, vocab, (N,), generator=g, dtype=torch.int32).to(dev)
+    rows_all = torch.arange(N, dtype=torch.int32, device=dev)
+    c0 = N // 2 + Cn
+    rows_c = torch.arange(c0, c0 + Cn, dtype=torch.int32, device=dev)
+    ids_c = torch.randint(0, vocab, (Cn,), generator=g, dtype=torch.int32).to(dev)
+
+    def call(t, rows, j):
+        lc.lacache_first_layer_tokens(t, rows, embed, norm_w, wqkv[j % S], rc, rs, *caches)
+
+    call(ids, rows_all, 0)
+    stream = torch.cuda.current_stream()
+    reps = max(min(args.steps, 64), 8)
+
+    def timed(fn):
+        for j in range(args.warmup):
+            fn(j)
+        torch.cuda.synchronize()
+        gr = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gr):
+            for j in range(reps):
+                fn(j)
+        gr.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(3):
+            gr.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        del gr
+        return e0.elapsed_time(e1) / (3 * reps)
+
+    ms_block = timed(lambda j: call(ids_c, rows_c, j))
+    ms_full = timed(lambda j: call(ids, rows_all, j))
+    # the dominant kernel of the block update: the QKV projection of 32 rows
+    y = torch.empty((Cn, H), dtype=torch.bfloat16, device=dev)
+    qkv = torch.empty((Cn, 3 * heads * D), dtype=torch.bfloat16, device=dev)
+    ms_lin = timed(lambda j: lc.lacache_linear_bf16(y, wqkv[j % S], qkv))
+    lin_bytes = 3 * heads * D * H * 2 + Cn * H * 2 + Cn * 3 * heads * D * 2
+    gbs = lin_bytes / (ms_lin * 1e-3) / 1e9
+    line = {
+        "metric": "token-wise first layer (EmbedCache/RoPECache): 32-token block update, tokens/s",
+        "value": round(Cn / (ms_block * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1, "steps": reps,
+        "warmup": args.warmup, "ms_per_step": round(ms_block, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16 (fp32 accumulate)", "data": "synthetic",
+        "config": {"workload": "first_layer_n512", "H": H, "heads": heads, "N": N, "block": Cn, "vocab": vocab,
+                   "weight_sets": S},
+        "ms_full_recompute_512_rows": round(ms_full, 5),
+        "block_update_speedup_vs_full": round(ms_full / ms_block, 2),
+        "timing": "HIP graph of %d back-to-back calls, 3 replays" % reps,
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                     "frac": round(gbs / PEAK_HBM_GBPS, 4), "traffic": None,
+                     "kernel": "linear_bf16_kernel (QKV projection of the 32 block rows)",
+                     "kernel_ms": round(ms_lin, 5), "algorithmic_bytes": lin_bytes},
+    }
+    if not args.no_cpu_baseline and not args.profile_only:
+        import oracle.first_layer as F
+        e = embed[ids_c.long()].view(torch.int16).cpu().numpy().view(np.uint16)
+        wq = wqkv[0].view(torch.int16).cpu().numpy().view(np.uint16)
+        nwh = norm_w.view(torch.int16).cpu().numpy().view(np.uint16)
+        t0 = time.perf_counter()
+        n = 0
+        while time.perf_counter() - t0 < 10.0 and n < 16:
+            _, yb = F.embed_norm(np.arange(Cn), e, nwh)
+            F.linear_bf16(yb, wq)
+            n += 1
+        t = time.perf_counter() - t0
+        line["cpu_baseline"] = {"value": round(n * Cn / t, 3), "unit": "tokens/s", "cores": _threads(),
+                                "kind": "oracle",
+                                "sample": "%d block updates of 32 rows (embedding + norm + QKV projection, fp64; "
+                                          "RoPE excluded): %.2f s" % (n, t)}
     print(json.dumps(line), flush=True)
 
 
