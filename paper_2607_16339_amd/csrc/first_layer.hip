@@ -10,7 +10,7 @@
 //                         row, write it to the embedding cache, RMSNorm (the
 //                         fused FFN quantizer's arithmetic: fp64 sum of squares
 //                         in the same fixed order) rounded to bf16;
-//   linear_bf16_kernel    out = a W^T for a few rows: 16 weight rows per
+//   linear_bf16_kernel    out = a W^T for a few rows: 16 or 48 weight rows per
 //                         workgroup streamed from HBM once per 64 activation
 //                         rows, K split over the 4 wavefronts (private
 //                         direct-to-LDS rings), bf16 MFMAs into fp32, the four
@@ -90,22 +90,26 @@ __global__ __launch_bounds__(256) void embed_rmsnorm_kernel(const int32_t* __res
 }
 
 // out [M x N] = a [M x K] W[N x K]^T, bf16 in and out, fp32 accumulation.
-// Workgroup (blockIdx.x, blockIdx.y): weight rows 16 x .. + 15, activation
-// rows 64 y .. + 63 (MT slabs of 16 rows). Its 4 wavefronts take a quarter of
-// the K range each; a K-step is 64 elements (128 bytes of a row), staged
-// global -> LDS as [rows][128 B] with the 16-byte chunk c of row r at
-// c ^ (r mod 8); each 16x16 tile gets two 16x16x32 bf16 MFMAs per K-step (the
-// lanes' chunks q and 4 + q).
+// Workgroup (blockIdx.x, blockIdx.y): weight rows 16 NJ x .. (NJ slabs of
+// 16), activation rows 64 y .. + 63 (MT slabs of 16 rows). Its 4 wavefronts
+// take a quarter of the K range each; a K-step is 64 elements (128 bytes of a
+// row), staged global -> LDS as [rows][128 B] with the 16-byte chunk c of
+// row r at c ^ (r mod 8); each 16x16 tile gets two 16x16x32 bf16 MFMAs per
+// K-step (the lanes' chunks q and 4 + q). Several weight slabs per workgroup
+// share each staged activation row, so the activations (re-read from L2 by
+// every workgroup) cost less of the CU's copy bandwidth than the weights.
 constexpr int kLinSplit = 4;
 
-template <int MT>
+template <int MT, int NJ>
 struct LinCfg {
   static constexpr int RA = MT * 16;
   static constexpr int kA = RA * 128;
-  static constexpr int kSlot = kA + 16 * 128;
+  static constexpr int kSlot = kA + NJ * 16 * 128;
   static constexpr int AI = RA / 8;  // 1 KB copies of activations per slot
-  static constexpr int PER = AI + 2;
-  static constexpr int D = MT == 1 ? 8 : (MT == 2 ? 5 : (MT == 3 ? 4 : 3));
+  static constexpr int PER = AI + 2 * NJ;
+  static constexpr int D0 = 160000 / (kLinSplit * kSlot);  // ring depth that fits the LDS
+  static constexpr int D = D0 > 8 ? 8 : D0;
+  static_assert(D >= 2, "ring depth");
 };
 
 __device__ __forceinline__ void lin_frag(const uint8_t* rows, int lr, int q, bf8& lo, bf8& hi) {
@@ -114,19 +118,19 @@ __device__ __forceinline__ void lin_frag(const uint8_t* rows, int lr, int q, bf8
   hi = *reinterpret_cast<const bf8*>(row + (((4 + q) ^ (lr & 7)) << 4));
 }
 
-template <int MT>
+template <int MT, int NJ>
 __global__ __launch_bounds__(kLinSplit * 64) void linear_bf16_kernel(const uint16_t* __restrict__ a,
                                                                      const uint16_t* __restrict__ w,
                                                                      uint16_t* __restrict__ out,
                                                                      float* __restrict__ out_tap, int64_t M,
                                                                      int64_t N, int64_t K) {
-  using C = LinCfg<MT>;
-  constexpr int D = C::D, RA = C::RA;
+  using C = LinCfg<MT, NJ>;
+  constexpr int D = C::D, RA = C::RA, NC = 16 * NJ;
   __shared__ __align__(16) uint8_t ring[kLinSplit][D * C::kSlot];
   const int t = threadIdx.x, lane = t & 63;
   const int wave = wave_uniform(t >> 6);
   const int q = lane >> 4, lr = lane & 15;
-  const int64_t n0 = static_cast<int64_t>(blockIdx.x) * 16;
+  const int64_t n0 = static_cast<int64_t>(blockIdx.x) * NC;
   const int64_t m0 = static_cast<int64_t>(blockIdx.y) * 64;
   const int64_t KS = K / 64;  // K-steps
   const int64_t ks0 = wave * KS / kLinSplit, ks1 = (wave + 1) * KS / kLinSplit;
@@ -145,9 +149,9 @@ __global__ __launch_bounds__(kLinSplit * 64) void linear_bf16_kernel(const uint1
     const int64_t gr = m0 + row < M ? m0 + row : M - 1;
     a_off[u] = gr * K * 2 + ((pch ^ (row & 7)) << 4);
   }
-  int64_t w_off[2];
+  int64_t w_off[2 * NJ];
 #pragma unroll
-  for (int u = 0; u < 2; ++u) {
+  for (int u = 0; u < 2 * NJ; ++u) {
     const int row = 8 * u + crow;
     w_off[u] = (n0 + row) * K * 2 + ((pch ^ (row & 7)) << 4);
   }
@@ -157,28 +161,34 @@ __global__ __launch_bounds__(kLinSplit * 64) void linear_bf16_kernel(const uint1
 #pragma unroll
     for (int u = 0; u < C::AI; ++u) dma16(ab + a_off[u] + kb, wave_uniform(static_cast<int>(base) + u * 1024));
 #pragma unroll
-    for (int u = 0; u < 2; ++u)
+    for (int u = 0; u < 2 * NJ; ++u)
       dma16(wb + w_off[u] + kb, wave_uniform(static_cast<int>(base) + C::kA + u * 1024));
   };
   if (nks > 0) {
 #pragma unroll
     for (int s = 0; s < D - 1; ++s) issue(s, s);
   }
-  v4f acc[MT];
+  v4f acc[MT][NJ];
 #pragma unroll
-  for (int i = 0; i < MT; ++i) acc[i] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) acc[i][j] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
   for (int s = 0; s < nks; ++s) {
     wait_vm_lds<(D - 2) * C::PER>();  // step s has landed; slot (s-1) % D is read
     issue(s + D - 1, (s + D - 1) % D);
     const uint8_t* slot = my + (s % D) * C::kSlot;
-    bf8 blo, bhi;
-    lin_frag(slot + C::kA, lr, q, blo, bhi);
+    bf8 alo[MT], ahi[MT];
 #pragma unroll
-    for (int i = 0; i < MT; ++i) {
-      bf8 alo, ahi;
-      lin_frag(slot + i * 16 * 128, lr, q, alo, ahi);
-      acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, blo, acc[i], 0, 0, 0);
-      acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, bhi, acc[i], 0, 0, 0);
+    for (int i = 0; i < MT; ++i) lin_frag(slot + i * 16 * 128, lr, q, alo[i], ahi[i]);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      bf8 blo, bhi;
+      lin_frag(slot + C::kA + j * 16 * 128, lr, q, blo, bhi);
+#pragma unroll
+      for (int i = 0; i < MT; ++i) {
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo[i], blo, acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi[i], bhi, acc[i][j], 0, 0, 0);
+      }
     }
   }
   wait_vm<0>();
@@ -187,14 +197,16 @@ __global__ __launch_bounds__(kLinSplit * 64) void linear_bf16_kernel(const uint1
 #pragma unroll
   for (int i = 0; i < MT; ++i)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) red[(wave * RA + 16 * i + 4 * q + r) * 16 + lr] = acc[i][r];
-  __syncthreads();
-  for (int e = t; e < RA * 16; e += kLinSplit * 64) {
-    const int row = e >> 4, col = e & 15;
-    if (m0 + row >= M) continue;
-    float sum = red[row * 16 + col];
+    for (int j = 0; j < NJ; ++j)
 #pragma unroll
-    for (int wv = 1; wv < kLinSplit; ++wv) sum += red[(wv * RA + row) * 16 + col];
+      for (int r = 0; r < 4; ++r) red[(wave * RA + 16 * i + 4 * q + r) * NC + 16 * j + lr] = acc[i][j][r];
+  __syncthreads();
+  for (int e = t; e < RA * NC; e += kLinSplit * 64) {
+    const int row = e / NC, col = e - row * NC;
+    if (m0 + row >= M) continue;
+    float sum = red[row * NC + col];
+#pragma unroll
+    for (int wv = 1; wv < kLinSplit; ++wv) sum += red[(wv * RA + row) * NC + col];
     out[(m0 + row) * N + n0 + col] = static_cast<uint16_t>(f32_to_bf16(sum));
     if (out_tap != nullptr) out_tap[(m0 + row) * N + n0 + col] = sum;
   }
@@ -252,15 +264,21 @@ hipError_t launch_embed_rmsnorm(hipStream_t st, const int32_t* ids, const int32_
 
 hipError_t launch_linear_bf16(hipStream_t st, const uint16_t* a, const uint16_t* w, uint16_t* out, float* out_tap,
                               int64_t M, int64_t N, int64_t K) {
-  // up to 64 rows per pass; the last pass may hold fewer slabs
+  // up to 64 rows per pass; the last pass may hold fewer slabs. Three weight
+  // slabs per workgroup when that still gives a workgroup per CU (few rows),
+  // else one.
   const unsigned passes = static_cast<unsigned>((M + 63) / 64);
-  const dim3 grid(static_cast<unsigned>(N / 16), passes), block(kLinSplit * 64);
   const int mt = static_cast<int>(M >= 64 ? 4 : (M + 15) / 16);
-#define LB(MT_) hipLaunchKernelGGL(linear_bf16_kernel<MT_>, grid, block, 0, st, a, w, out, out_tap, M, N, K)
-  if (mt <= 1) LB(1);
-  else if (mt == 2) LB(2);
-  else if (mt == 3) LB(3);
-  else LB(4);
+  const bool wide = mt <= 2 && N % 48 == 0 && N / 48 >= 256;
+  const dim3 grid(static_cast<unsigned>(N / (wide ? 48 : 16)), passes), block(kLinSplit * 64);
+#define LB(MT_, NJ_) hipLaunchKernelGGL((linear_bf16_kernel<MT_, NJ_>), grid, block, 0, st, a, w, out, out_tap, M, N, K)
+  if (wide) {
+    if (mt <= 1) LB(1, 3);
+    else LB(2, 3);
+  } else if (mt <= 1) LB(1, 1);
+  else if (mt == 2) LB(2, 1);
+  else if (mt == 3) LB(3, 1);
+  else LB(4, 1);
 #undef LB
   return hipGetLastError();
 }

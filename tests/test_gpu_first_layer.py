@@ -93,7 +93,7 @@ def _linear_check(a, w, out, tap):
 
 
 @pytest.mark.parametrize("M,N,K", [(1, 384, 256), (17, 768, 1024), (64, 384, 4096), (100, 384, 512),
-                                   (200, 256, 256)])
+                                   (200, 256, 256), (32, 12288, 256), (9, 12288, 512)])
 def test_linear_bf16(M, N, K):
     rng = np.random.default_rng(M * 7 + K)
     a = to_bf16_bits(rng.standard_normal((M, K)).astype(np.float32))
