@@ -287,7 +287,7 @@ def main():
     # weight sets) are captured in a HIP graph, so that the host's per-call
     # cost does not leave the GPU idle between them; the graph is replayed
     # between HIP events on the stream it runs on.
-    skinny = M <= 64
+    skinny = M <= 32
     xq = torch.empty((M, H), dtype=torch.uint8, device=dev)
     xs = torch.empty((H // 128, M), dtype=torch.float32, device=dev)
     hq = torch.empty((M, I), dtype=torch.uint8, device=dev)
@@ -401,6 +401,7 @@ def cpu_baseline(w, sets, out, dev):
     """The oracle, as it stands, on a bounded sample of the same workload."""
     import numpy as np
     import oracle.ffn as O
+    import paper_2607_16339_amd as lc
     import synth
 
     try:
@@ -416,7 +417,8 @@ def cpu_baseline(w, sets, out, dev):
     while t < 10.0 and calls < 64:
         s = sets[calls % len(sets)]
         xb = synth.make_x(w, layer=calls % len(sets) + 1, step=calls % len(sets))[:rows]
-        host = [a.cpu().numpy() for a in (s["wgu_q"], s["wgu_s"], s["wd_q"], s["wd_s"])]
+        host = [lc.weight_codes_rowmajor(s["wgu_q"]), s["wgu_s"].cpu().numpy(), lc.weight_codes_rowmajor(s["wd_q"]),
+                s["wd_s"].cpu().numpy()]
         norm_w = s["norm_w"].view(torch.int16).cpu().numpy().view(np.uint16)
         t0 = time.perf_counter()
         O.ffn(xb, norm_w, host[0], host[1], host[2], host[3], w.I)

@@ -35,7 +35,7 @@
  *   Outputs must not overlap inputs.
  * - The caller owns every buffer it passes. The library owns only its
  *   workspace: the intermediates of lacache_ffn_fp8 and the fp32 h of the
- *   skinny (M <= 64) gate/up stage call (see lacache_ffn_fp8).
+ *   skinny (M <= 32) gate/up stage call (see lacache_ffn_fp8).
  * - Results are deterministic: the same inputs give the same output bytes
  *   (no floating-point atomics).
  * - A failed HIP launch or allocation returns LACACHE_ERR_HIP or
@@ -62,11 +62,21 @@ typedef enum {
 /*
  * 128x128 block quantization of a bf16 weight (Sec. 3.4, Eqs. 7-8).
  *   w   [N x K] bf16               (input)
- *   w_q [N x K] e4m3 codes         (output)
+ *   w_q N*K e4m3 codes             (output) in the weight tile layout below
  *   w_s [N/128 x K/128] fp32       (output) block (nb, kb) covers rows
  *                                  nb*128.. and columns kb*128..
  * For the FFN, the gate/up weight is the row concatenation [W_gate; W_up]
  * ([2I x H], gate rows first) and the down weight is W_down [H x I].
+ *
+ * Weight tile layout (every e4m3 weight argument of this library): the code
+ * of W[n, k] sits at byte
+ *   ((n/16) (K/128) + k/128) 2048 + ((k/64) mod 2) 1024 + (n mod 16) 64 + k mod 64,
+ * i.e. 16-row x 128-column tiles of 2 KB, a 16-row slab's tiles in K order
+ * (the slab starts at byte 16 (n/16) K, as in a row-major matrix), and in a
+ * tile first columns 0..63 of its 16 rows (64 bytes per row), then columns
+ * 64..127. The MFMA operand of a slab and K-group is then two contiguous
+ * 1 KB runs, so the weight-streaming kernels load 1 KB per instruction.
+ * The codes themselves are those of the row-major statement of Eqs. 7-8.
  */
 int lacache_quant_weights(void* stream, const uint16_t* w, uint8_t* w_q, float* w_s,
                           int64_t N, int64_t K, int group);
@@ -103,13 +113,15 @@ int lacache_add_rmsnorm_quant(void* stream, uint16_t* resid, const uint16_t* y, 
  * re-quantization (Sec. 3.4: quantization fused with the SwiGLU before the
  * ffout linear).
  *   xq, xs  as produced by lacache_rmsnorm_quant                   (input)
- *   wgu_q   [2I x H] e4m3, wgu_s [2I/128 x H/128] fp32             (input)
+ *   wgu_q   [2I x H] e4m3 (tile layout), wgu_s [2I/128 x H/128] fp32 (input)
  *   hq      [M x I] e4m3, hs [I/128 x M] fp32                      (output)
  *   h_tap   [M x I] fp32 or NULL: if non-NULL, also receives the fp32 h that
  *           was quantized (a test hook; same kernel, one more store)
  * acc[m,n] = sum_kb (xs[kb,m] * wgu_s[n/128,kb]) * dot_kb(xq[m,:], wgu_q[n,:])
  * accumulated in fp32; h = SiLU(acc[:, j]) * acc[:, I + j].
- * On the skinny path h passes through the library workspace (M x I fp32).
+ * On the skinny path h passes through the library workspace (M x I fp32),
+ * and the K range is split into four parts whose fp32 partial sums are
+ * added in part order.
  */
 int lacache_gateup_swiglu_quant(void* stream, const uint8_t* xq, const float* xs, const uint8_t* wgu_q,
                                 const float* wgu_s, uint8_t* hq, float* hs, float* h_tap,
@@ -118,12 +130,12 @@ int lacache_gateup_swiglu_quant(void* stream, const uint8_t* xq, const float* xs
 /*
  * FP8 down (ffout) GEMM with per-group dequantization to bf16 (Sec. 3.4).
  *   hq, hs  as produced by lacache_gateup_swiglu_quant             (input)
- *   wd_q    [H x I] e4m3, wd_s [H/128 x I/128] fp32                (input)
+ *   wd_q    [H x I] e4m3 (tile layout), wd_s [H/128 x I/128] fp32  (input)
  *   out     [M x H] bf16, rounded to nearest-even from fp32         (output)
  *   out_tap [M x H] fp32 or NULL: if non-NULL, also receives the fp32 value
  *           that was rounded (test hook)
- * On the skinny path (M <= 64) the K range is split over the four wavefronts
- * of a workgroup, whose fp32 partial sums are added in a fixed order.
+ * On the skinny path (M <= 32) the K range is split over eight wavefronts
+ * of a workgroup, whose fp32 partial sums are added in wavefront order.
  */
 int lacache_down_proj(void* stream, const uint8_t* hq, const float* hs, const uint8_t* wd_q, const float* wd_s,
                       uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I, int group);
@@ -239,7 +251,7 @@ enum { LACACHE_GRAN_GROUP = 0, LACACHE_GRAN_TOKEN = 1, LACACHE_GRAN_TENSOR = 2 }
  * Weight quantization at a granularity. GROUP: lacache_quant_weights (w_row_s
  * unused, may be NULL). TOKEN / TENSOR:
  *   w       [N x K] bf16                     (input)
- *   w_q     [N x K] e4m3                     (output)
+ *   w_q     [N x K] e4m3 (tile layout)       (output)
  *   w_s     [N/128 x K/128] fp32             (output) all 1.0
  *   w_row_s [N] fp32                         (output) RN32(max|w[n, :]| / 448)
  *                                            per row, or the whole matrix's
@@ -349,9 +361,10 @@ size_t lacache_first_layer_workspace_bytes(int64_t R, int64_t heads, int64_t H);
 
 /*
  * Kernel-path policy for the GEMM stages, process-wide:
- *   0 = automatic (the skinny weight-streaming kernels for M <= 64,
- *       H <= 8192 and I <= 16384, the tiled MFMA kernels otherwise), 1 = always skinny
- *       (other shapes return LACACHE_ERR_UNSUPPORTED), 2 = always tiled.
+ *   0 = automatic (the skinny weight-streaming kernels for M <= 32 with
+ *       ceil(M/16) 16 (H + 16) <= 131584 bytes, H <= 8192 and I <= 16384;
+ *       the tiled MFMA kernels otherwise), 1 = always skinny (other shapes
+ *       return LACACHE_ERR_UNSUPPORTED), 2 = always tiled.
  * Returns the previous policy, or LACACHE_ERR_INVALID_ARG for other values.
  */
 int lacache_set_path_policy(int policy);

@@ -6,6 +6,7 @@ pass raw pointers and the current HIP stream, and raise ``LacacheError`` on a
 non-OK status. Every step of the FFN runs in the library's HIP kernels.
 """
 
+import numpy as np
 import torch
 
 from ._lib import (LACACHE_ERR_ALLOC, LACACHE_ERR_HIP, LACACHE_ERR_INVALID_ARG, LACACHE_ERR_UNSUPPORTED,  # noqa: F401
@@ -222,7 +223,8 @@ def lacache_ffn_g_workspace_bytes(M, H, I):
 
 
 def quantize_weights_g(w, granularity, stream=None):
-    """Returns (w_q, w_s, w_row_s) for a bf16 weight at a granularity (w_row_s None for GROUP)."""
+    """Returns (w_q, w_s, w_row_s) for a bf16 weight at a granularity (w_row_s None for GROUP);
+    w_q is in the tile layout (weight_codes_rowmajor)."""
     N, K = w.shape
     w_q = torch.empty((N, K), dtype=torch.uint8, device=w.device)
     w_s = torch.empty((N // GROUP, K // GROUP), dtype=torch.float32, device=w.device)
@@ -283,7 +285,7 @@ def lacache_first_layer_tokens(token_ids, rows, embed, norm_w, w_qkv, rope_cos, 
 
 
 def lacache_set_path_policy(policy):
-    """0 = automatic, 1 = skinny kernels (M <= 64), 2 = tiled kernels. Returns the previous policy."""
+    """0 = automatic, 1 = skinny kernels (M <= 32), 2 = tiled kernels. Returns the previous policy."""
     r = lib().lacache_set_path_policy(int(policy))
     if r < 0:
         raise LacacheError(r, "lacache_set_path_policy")
@@ -300,8 +302,33 @@ def lacache_release_workspace():
 
 # ---- allocation conveniences (torch allocates; the library computes) -------
 
+def weight_codes_rowmajor(w_q):
+    """Host copy of FP8 weight codes in row-major order: a numpy uint8 [N, K]
+    array whose element (n, k) is the code of W[n, k].
+
+    The library stores the codes of W [N x K] in 16-row x 128-column tiles of
+    2 KB (the layout its kernels stream, described with lacache_quant_weights
+    in include/lacache.h): tile (n/16, k/128) at byte
+    ((n/16)(K/128) + k/128) 2048, columns 0..63 of its 16 rows in the first
+    1 KB (64 bytes per row), columns 64..127 in the second. A host-side
+    reordering for inspection; the kernels never need it.
+    """
+    a = w_q.cpu().numpy() if torch.is_tensor(w_q) else np.asarray(w_q)
+    a = a.view(np.uint8) if a.dtype != np.uint8 else a
+    N, K = a.shape
+    return np.ascontiguousarray(a.reshape(N // 16, K // 128, 2, 16, 64).transpose(0, 3, 1, 2, 4).reshape(N, K))
+
+
+def weight_codes_tiled(codes):
+    """The inverse of weight_codes_rowmajor: row-major codes [N, K] -> the
+    library's tile layout (a numpy uint8 array of the same shape)."""
+    a = np.asarray(codes, dtype=np.uint8)
+    N, K = a.shape
+    return np.ascontiguousarray(a.reshape(N // 16, 16, K // 128, 2, 64).transpose(0, 2, 3, 1, 4).reshape(N, K))
+
+
 def quantize_weights(w, group=GROUP, stream=None):
-    """Returns (w_q uint8 [N, K], w_s fp32 [N/128, K/128]) for a bf16 weight."""
+    """Returns (w_q uint8 [N, K] in the tile layout, w_s fp32 [N/128, K/128]) for a bf16 weight."""
     N, K = w.shape
     w_q = torch.empty((N, K), dtype=torch.uint8, device=w.device)
     w_s = torch.empty((N // group, K // group), dtype=torch.float32, device=w.device)

@@ -99,10 +99,13 @@ int choose_path(int64_t M, int64_t H, int64_t I, Path* p) {
   return LACACHE_OK;
 }
 
-// fp32 scratch of the GEMM stages: the skinny gate/up h (M <= 64), or the
-// split-K partials of the tiled down GEMM.
+// fp32 scratch of the GEMM stages: the skinny gate/up h (M <= kSkinnyMaxM),
+// or the split-K partials of the tiled down GEMM, whichever path runs (both
+// are possible at small M: by shape and by the path policy).
 size_t scratch_bytes(int64_t M, int64_t H, int64_t I) {
-  return M <= kSkinnyMaxM ? skinny_gateup_ws_bytes(M, I) : tiled_down_ws_bytes(M, H, I);
+  const size_t sk = M <= kSkinnyMaxM ? skinny_gateup_ws_bytes(M, I) : 0;
+  const size_t tl = tiled_down_ws_bytes(M, H, I);
+  return sk > tl ? sk : tl;
 }
 
 // ---------------------------------------------------------------------------
@@ -143,7 +146,7 @@ int get_workspace(size_t bytes, void** out) {
 
 // Workspace layout (every region 256-byte aligned):
 //   [scratch: the skinny gate/up h (M <= kSkinnyMaxM) or the split-K partials
-//    of the tiled down GEMM; may be empty]
+//    of the tiled down GEMM, the larger of the two; may be empty]
 //   [xq: M x H][xs: H/128 x M fp32][hq: M x I][hs: I/128 x M fp32]
 struct FfnWs {
   void* scratch;

@@ -14,6 +14,21 @@ constexpr int kGroup = 128;      // quantization group (1x128 activations, 128x1
 constexpr float kE4M3Max = 448.0f;
 
 // ---------------------------------------------------------------------------
+// Layout of FP8 weight codes W [N x K] (N a multiple of 16, K of 128): tiles
+// of 16 rows x 128 columns (one K-group), 2 KB each, tile (n/16, k/128) at
+// byte ((n/16) (K/128) + k/128) 2048, so a 16-row slab's K range is one
+// contiguous run starting at byte 16 (n/16) K, as in a row-major matrix.
+// Inside a tile the first 1 KB holds columns 0..63 of the 16 rows (64 bytes
+// per row, row after row) and the second 1 KB columns 64..127. The 16x16x128
+// MFMA operand of a slab then takes exactly the two 1 KB halves of a tile,
+// one 16-byte load per lane each, so register loads of the weights read 1 KB
+// contiguous per instruction.
+// ---------------------------------------------------------------------------
+__host__ __device__ inline int64_t wtile_off(int64_t n, int64_t k, int64_t K) {
+  return ((n >> 4) * (K >> 7) + (k >> 7)) * 2048 + ((k >> 6) & 1) * 1024 + (n & 15) * 64 + (k & 63);
+}
+
+// ---------------------------------------------------------------------------
 // e4m3fn encoding: clip to [-448, 448] (Eq. 7), then the hardware's
 // round-to-nearest-even conversion. The conversion itself does not saturate
 // (values above 464 become the NaN code), so the clip must come first. The

@@ -175,11 +175,13 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
     const int blim = kGateUp ? BNR : static_cast<int>(N) - 1 - n0;
     b_base = kGateUp ? bq + static_cast<int64_t>(it.col) * 128 * K : bq + static_cast<int64_t>(n0) * K;
     b_base_hi = kGateUp ? bq + (I + static_cast<int64_t>(it.col) * 128 - 128) * K : b_base;
+    // (weights in the tile layout of wtile_off: the slab bases above are the
+    // same as row-major, the offsets within and the K-group step are not)
 #pragma unroll
     for (int u = 0; u < kBInst; ++u) {
       const int row = (wave * kBInst + u) * 8 + (lane >> 3);
       const int r = row < blim ? row : blim;
-      b_off[u] = static_cast<uint32_t>(r) * static_cast<uint32_t>(K) + ((lane & 7) ^ swz(row)) * 16;
+      b_off[u] = static_cast<uint32_t>(wtile_off(r, ((lane & 7) ^ swz(row)) * 16, K));
     }
     {
       const int row = xband * 64 + lane;
@@ -202,7 +204,7 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
 #pragma unroll
     for (int u = 0; u < kBInst; ++u) {
       const uint8_t* base = (kGateUp && (wave * kBInst + u) * 8 >= 128) ? b_base_hi : b_base;
-      dma16s(base + ko, b_off[u], wave_uniform(lb + (wave * kBInst + u) * 1024));
+      dma16s(base + ko * 16, b_off[u], wave_uniform(lb + (wave * kBInst + u) * 1024));
     }
     const int lx = static_cast<int>(lds_u32(dst->xs));
     dma4s(x_base + static_cast<int64_t>(kb) * M, x_off, wave_uniform(lx + xs_dst * 4));
@@ -223,28 +225,34 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
 
   // Multiplies the K-group in stage cur into acc.
   auto compute = [&](const Stage<BM>* cur) {
+    auto brow = [&](int j) {
+      return kGateUp ? (j < NJ / 2 ? (WC / 2) * wn + 16 * j : 128 + (WC / 2) * wn + 16 * (j - NJ / 2)) : WC * wn + 16 * j;
+    };
+    // Every LDS read the first MFMAs and FMAs need is issued up front, in the
+    // order they are needed (LDS reads complete in order): the first B slab,
+    // the scales, then the four A slabs. MFMA i waits only for its own
+    // operands, and the scale products are formed after MFMA 1, when the
+    // first FMAs need them, instead of holding MFMA 0 back by a round trip.
+    v8i bb[2];
+    bb[0] = load_frag(cur->b, brow(0) + lr, q);
+    __builtin_amdgcn_sched_barrier(0);
+    float xv[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) xv[i] = cur->xs[64 * wm + 16 * i + lr];
     // gate/up: slabs 0..NJ/2-1 are gate rows (block scale in slot BM), the
     // rest the matching up rows (slot BM + 1); down: the wave's columns lie in
     // one block, slot BM + (WC wn) / 128
     const float w0 = cur->xs[BM + (kGateUp ? 0 : (WC * wn) / 128)];
     const float w1 = cur->xs[BM + 1];
+    __builtin_amdgcn_sched_barrier(0);
     v8i af[4];
-    float sc[kGateUp ? 2 : 1][4];  // RN32(x_scale * w_scale) of this lane's row
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      af[i] = load_frag(cur->a, 64 * wm + 16 * i + lr, q);
-      const float xv = cur->xs[64 * wm + 16 * i + lr];
-      sc[0][i] = xv * w0;
-      if (kGateUp) sc[kGateUp ? 1 : 0][i] = xv * w1;
-    }
-    auto brow = [&](int j) {
-      return kGateUp ? (j < NJ / 2 ? (WC / 2) * wn + 16 * j : 128 + (WC / 2) * wn + 16 * (j - NJ / 2)) : WC * wn + 16 * j;
-    };
+    for (int i = 0; i < 4; ++i) af[i] = load_frag(cur->a, 64 * wm + 16 * i + lr, q);
+    __builtin_amdgcn_sched_barrier(0);
+    float sc[kGateUp ? 2 : 1][4];  // RN32(x_scale * w_scale) of this lane's row
     // Software pipeline over the 4 NJ sub-tiles s = 4 j + i: MFMA s, then the
     // scale FMAs of MFMA s - 2; the B operand of slab j + 1 is read while slab
     // j multiplies.
-    v8i bb[2];
-    bb[0] = load_frag(cur->b, brow(0) + lr, q);
     v4f pr[3];
 #pragma unroll
     for (int s = 0; s < 4 * NJ; ++s) {
@@ -255,6 +263,13 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
       // keep MFMA s ahead of the FMAs below: they read a result two MFMAs
       // old, so they neither wait for the matrix core nor delay the next MFMA
       __builtin_amdgcn_sched_barrier(0);
+      if (s == 1) {
+#pragma unroll
+        for (int i2 = 0; i2 < 4; ++i2) {
+          sc[0][i2] = xv[i2] * w0;
+          if (kGateUp) sc[kGateUp ? 1 : 0][i2] = xv[i2] * w1;
+        }
+      }
       if (s >= 2) {
         const int ps = s - 2;
         const int blk = (kGateUp && (ps >> 2) >= NJ / 2) ? 1 : 0;

@@ -77,8 +77,9 @@ __global__ __launch_bounds__(1024) void row_scales_kernel(float* __restrict__ s,
 
 // codes[m, k] = E(RN32(v[m, k] / s[m])) (0x00 for s == 0); eight values per
 // thread; with kgm non-null every K-group's first thread of row m also writes
-// kgm[kb * M + m] = s[m].
-template <typename T>
+// kgm[kb * M + m] = s[m]. kTiled: the codes go to the weight tile layout
+// (wtile_off) instead of row-major.
+template <typename T, bool kTiled>
 __global__ __launch_bounds__(256) void quant_rows_kernel(const T* __restrict__ v, const float* __restrict__ s,
                                                          uint8_t* __restrict__ codes, float* __restrict__ kgm,
                                                          int64_t M, int64_t K) {
@@ -93,7 +94,7 @@ __global__ __launch_bounds__(256) void quant_rows_kernel(const T* __restrict__ v
     lo = enc4_e4m3(qdiv(y[0], sc), qdiv(y[1], sc), qdiv(y[2], sc), qdiv(y[3], sc));
     hi = enc4_e4m3(qdiv(y[4], sc), qdiv(y[5], sc), qdiv(y[6], sc), qdiv(y[7], sc));
   }
-  *reinterpret_cast<uint2*>(codes + e) = make_uint2(lo, hi);
+  *reinterpret_cast<uint2*>(codes + (kTiled ? wtile_off(row, col, K) : e)) = make_uint2(lo, hi);
   if (kgm != nullptr && (col & (kGroup - 1)) == 0) kgm[(col / kGroup) * M + row] = sc;
 }
 
@@ -102,13 +103,13 @@ __global__ __launch_bounds__(256) void fill_kernel(float* __restrict__ p, float 
   if (i < n) p[i] = v;
 }
 
-template <typename T>
+template <typename T, bool kTiled>
 hipError_t quant_rows(hipStream_t st, const T* v, uint8_t* codes, float* kgm, float* s_rows, int64_t M, int64_t K,
                       int per_tensor) {
   hipLaunchKernelGGL(row_amax_kernel<T>, dim3(static_cast<unsigned>(M)), dim3(256), 0, st, v, s_rows, K);
   hipLaunchKernelGGL(row_scales_kernel, dim3(1), dim3(1024), 0, st, s_rows, M, per_tensor);
   const int64_t threads = M * K / 8;
-  hipLaunchKernelGGL(quant_rows_kernel<T>, dim3(static_cast<unsigned>((threads + 255) / 256)), dim3(256), 0, st, v,
+  hipLaunchKernelGGL((quant_rows_kernel<T, kTiled>), dim3(static_cast<unsigned>((threads + 255) / 256)), dim3(256), 0, st, v,
                      s_rows, codes, kgm, M, K);
   return hipGetLastError();
 }
@@ -117,12 +118,12 @@ hipError_t quant_rows(hipStream_t st, const T* v, uint8_t* codes, float* kgm, fl
 
 hipError_t launch_quant_rows_f32(hipStream_t st, const float* v, uint8_t* codes, float* kgm, float* s_rows, int64_t M,
                                  int64_t K, bool per_tensor) {
-  return quant_rows<float>(st, v, codes, kgm, s_rows, M, K, per_tensor ? 1 : 0);
+  return quant_rows<float, false>(st, v, codes, kgm, s_rows, M, K, per_tensor ? 1 : 0);
 }
 
 hipError_t launch_quant_weights_rows(hipStream_t st, const uint16_t* w, uint8_t* wq, float* w_blocks, float* w_rows,
                                      int64_t N, int64_t K, bool per_tensor) {
-  const hipError_t e = quant_rows<uint16_t>(st, w, wq, nullptr, w_rows, N, K, per_tensor ? 1 : 0);
+  const hipError_t e = quant_rows<uint16_t, true>(st, w, wq, nullptr, w_rows, N, K, per_tensor ? 1 : 0);
   if (e != hipSuccess) return e;
   const int64_t nb = (N / kGroup) * (K / kGroup);
   hipLaunchKernelGGL(fill_kernel, dim3(static_cast<unsigned>((nb + 255) / 256)), dim3(256), 0, st, w_blocks, 1.0f, nb);

@@ -66,10 +66,11 @@ hipError_t launch_down_tiled(hipStream_t st, const uint8_t* hq, const float* hs,
                              uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I, void* ws_buf,
                              const float* col_s = nullptr);
 
-// Skinny weight-streaming GEMMs (M <= kSkinnyMaxM, H <= 8192, I <= 16384).
+// Skinny weight-streaming GEMMs (M <= kSkinnyMaxM; skinny_supported() also
+// checks that the activation rows fit the gate/up kernel's LDS).
 // The gate/up stage needs an fp32 scratch buffer of skinny_gateup_ws_bytes()
 // (no initial contents) for h; the down stage needs none.
-constexpr int64_t kSkinnyMaxM = 64;
+constexpr int64_t kSkinnyMaxM = 32;
 bool skinny_supported(int64_t M, int64_t H, int64_t I);
 size_t skinny_gateup_ws_bytes(int64_t M, int64_t I);
 hipError_t launch_gateup_skinny(hipStream_t st, const uint8_t* xq, const float* xs, const uint8_t* wq,

@@ -8,7 +8,8 @@ namespace lacache {
 
 // ---------------------------------------------------------------------------
 // 128x128 block weight quantization. One workgroup (256 threads) per block:
-// thread t owns row t/2 of the block, 64 consecutive elements (128 bytes).
+// thread t owns row t/2 of the block, 64 consecutive elements (128 bytes of
+// bf16); its 64 codes are one row's half of a 16 x 128 tile (wtile_off).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void quant_weights_kernel(const uint16_t* __restrict__ w, uint8_t* __restrict__ wq,
                                                             float* __restrict__ ws, int64_t K) {
@@ -48,7 +49,7 @@ __global__ __launch_bounds__(256) void quant_weights_kernel(const uint16_t* __re
       }
     }
   }
-  uint4* dst = reinterpret_cast<uint4*>(wq + row * K + col);
+  uint4* dst = reinterpret_cast<uint4*>(wq + wtile_off(row, col, K));
 #pragma unroll
   for (int i = 0; i < 4; ++i) dst[i] = make_uint4(out[4 * i], out[4 * i + 1], out[4 * i + 2], out[4 * i + 3]);
   if (t == 0) ws[nb * (K / kGroup) + kb] = s;

@@ -39,7 +39,9 @@ class Layer:
             torch.cuda.synchronize()
 
     def host_weights(self):
-        return host(self.wgu_q), host(self.wgu_s), host(self.wd_q), host(self.wd_s)
+        """Row-major codes and the block scales (the device holds the codes in tiles)."""
+        return (lc.weight_codes_rowmajor(self.wgu_q), host(self.wgu_s), lc.weight_codes_rowmajor(self.wd_q),
+                host(self.wd_s))
 
 
 def run_stages(x, layer, M, H, I, sentinel=True):

@@ -156,9 +156,11 @@ def test_path_policy(L):
     try:
         f = Fake()
         p = [f() for _ in range(8)]
-        # skinny kernels only take M <= 64
-        assert L.lacache_gateup_swiglu_quant(None, p[0], p[1], p[2], p[3], p[4], p[5], None, 65, 256, 768, 128) == UNSUP
-        assert L.lacache_down_proj(None, p[0], p[1], p[2], p[3], p[4], None, 65, 256, 768, 128) == UNSUP
+        # skinny kernels only take M <= 32
+        assert L.lacache_gateup_swiglu_quant(None, p[0], p[1], p[2], p[3], p[4], p[5], None, 33, 256, 768, 128) == UNSUP
+        assert L.lacache_down_proj(None, p[0], p[1], p[2], p[3], p[4], None, 33, 256, 768, 128) == UNSUP
+        # ... whose activation rows fit the gate/up kernel's LDS (16 rows x 8192, 32 rows x 4096) ...
+        assert L.lacache_gateup_swiglu_quant(None, p[0], p[1], p[2], p[3], p[4], p[5], None, 17, 8192, 768, 128) == UNSUP
         # ... and H <= 8192, I <= 16384 (the scales of a K range are staged in LDS)
         assert L.lacache_gateup_swiglu_quant(None, p[0], p[1], p[2], p[3], p[4], p[5], None, 8, 8320, 768, 128) == UNSUP
         assert L.lacache_down_proj(None, p[0], p[1], p[2], p[3], p[4], None, 8, 256, 16512, 128) == UNSUP
@@ -171,9 +173,11 @@ def test_workspace_bytes_and_status_strings(L):
     def a256(b):
         return (b + 255) // 256 * 256
     M, H, I = 32, 4096, 12288
-    # one fp32 scratch buffer for the gate/up h (M x I)
-    skinny = a256(M * I * 4)
-    want = skinny + a256(M * H) + a256(H // 128 * M * 4) + a256(M * I) + a256(I // 128 * M * 4)
+    # one fp32 scratch buffer, big enough for either path of the shape: the
+    # skinny gate/up h (M x I) or the tiled down GEMM's split-K partials
+    # (16 output tiles -> 6 splits of 16 K-groups: 6 x M x H)
+    scratch = max(a256(M * I * 4), a256(6 * M * H * 4))
+    want = scratch + a256(M * H) + a256(H // 128 * M * 4) + a256(M * I) + a256(I // 128 * M * 4)
     assert L.lacache_ffn_workspace_bytes(M, H, I, 128) == want
     M = 512
     # the tiled down GEMM splits K 4 ways at M = 512 (64 output tiles): fp32 partials
@@ -285,3 +289,27 @@ def test_first_layer_validation(L):
         == INVALID
     assert L.lacache_first_layer_tokens(None, ids, rows, 0, emb, 100, nw, wq, cs, sn, cache, q, k, v, 2, 64, 256) == OK
     assert L.lacache_first_layer_workspace_bytes(32, 32, 4096) > 0
+
+
+def test_weight_tile_layout_helpers():
+    """weight_codes_rowmajor / weight_codes_tiled against positions of the
+    tile layout worked out by hand, and as inverses of each other."""
+    import numpy as np
+    import paper_2607_16339_amd as lc
+    N, K = 48, 384  # 3 slabs of 16 rows x 3 K-groups
+    rm = np.arange(N * K, dtype=np.int64).reshape(N, K)
+    codes = (rm % 251).astype(np.uint8)
+    t = lc.weight_codes_tiled(codes).reshape(-1)
+    # W[0, 0..63] is the first 64 bytes; W[1, 0] follows them; W[0, 64] opens
+    # the tile's second kilobyte; W[0, 128] opens the next tile (same slab)
+    assert np.array_equal(t[:64], codes[0, :64])
+    assert t[64] == codes[1, 0] and t[15 * 64 + 63] == codes[15, 63]
+    assert t[1024] == codes[0, 64] and t[1024 + 64 * 3 + 5] == codes[3, 69]
+    assert t[2048] == codes[0, 128] and t[2 * 2048 + 1024 + 7] == codes[0, 256 + 64 + 7]
+    # the second slab starts at byte 16 K, as in a row-major matrix
+    assert t[16 * K] == codes[16, 0] and t[16 * K + 64 * 15 + 1] == codes[31, 1]
+    # every position: the formula of include/lacache.h
+    n, k = np.meshgrid(np.arange(N), np.arange(K), indexing="ij")
+    off = ((n // 16) * (K // 128) + k // 128) * 2048 + ((k // 64) % 2) * 1024 + (n % 16) * 64 + k % 64
+    assert np.array_equal(t[off], codes)
+    assert np.array_equal(lc.weight_codes_rowmajor(t.reshape(N, K)), codes)

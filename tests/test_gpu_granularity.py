@@ -54,7 +54,8 @@ def test_weight_codes_and_row_scales_bit_exact(gran, ogran):
     for bits in (wgu, wd):
         w_q, w_s, w_rs = _weights(bits, gran)
         rq, rrs = G.quant_weights_g(bits, ogran)
-        assert np.array_equal(host(w_q), rq), "codes differ in %d places" % int((host(w_q) != rq).sum())
+        gq = lc.weight_codes_rowmajor(w_q)  # the device holds the codes in tiles
+        assert np.array_equal(gq, rq), "codes differ in %d places" % int((gq != rq).sum())
         assert np.array_equal(host(w_rs).view(np.uint32), rrs.view(np.uint32))
         assert np.all(host(w_s) == 1.0)
 
@@ -127,7 +128,7 @@ def test_gemms_against_the_oracle(gran, ogran, M, H, I):
     lc.lacache_gateup_swiglu_f32(xq, xs, wgu_q, wgu_s, wgu_rs, h)
     torch.cuda.synchronize()
     # gate/up + SwiGLU against the exact fp64 result of the GPU's own codes
-    aq, ar, bq, br = host(xq), host(xr), host(wgu_q), host(wgu_rs)
+    aq, ar, bq, br = host(xq), host(xr), lc.weight_codes_rowmajor(wgu_q), host(wgu_rs)
     acc = G.scaled_gemm(aq, ar, bq, br)
     dacc = _row_gemm_bound(aq, ar, bq, br, np.abs(acc))
     g, u, dg, du = acc[:, :I], acc[:, I:], dacc[:, :I], dacc[:, I:]
@@ -151,7 +152,7 @@ def test_gemms_against_the_oracle(gran, ogran, M, H, I):
     rq, rr = G.quantize_rows(host(h), ogran)
     assert np.array_equal(host(hq), rq) and np.array_equal(host(hr).view(np.uint32), rr.view(np.uint32))
     # down on the same operands: fp32 within 2e-3 of the row max, bf16 = RNE(fp32)
-    out64 = G.scaled_gemm(host(hq), host(hr), host(wd_q), host(wd_rs))
+    out64 = G.scaled_gemm(host(hq), host(hr), lc.weight_codes_rowmajor(wd_q), host(wd_rs))
     o32 = host(tap).astype(np.float64)
     e = float((np.abs(o32 - out64) / np.maximum(np.abs(out64).max(axis=1, keepdims=True), 1e-300)).max())
     _say("  out: err %.2e" % e)

@@ -95,8 +95,10 @@ def _unit_scale_dot(A, B):
     lc.lacache_set_path_policy(2)
     out = torch.empty((M, N), dtype=torch.bfloat16, device=DEV)
     tap = torch.empty((M, N), dtype=torch.float32, device=DEV)
-    lc.lacache_down_proj(torch.from_numpy(A).to(DEV), torch.ones((1, M), device=DEV), torch.from_numpy(B).to(DEV),
-                         torch.ones((N // 128, 1), device=DEV), out, tap)
+    # B is the weight argument: its codes go in the weight tile layout
+    lc.lacache_down_proj(torch.from_numpy(A).to(DEV), torch.ones((1, M), device=DEV),
+                         torch.from_numpy(lc.weight_codes_tiled(B)).to(DEV), torch.ones((N // 128, 1), device=DEV),
+                         out, tap)
     torch.cuda.synchronize()
     return host(tap).astype(np.float64)
 
@@ -132,9 +134,9 @@ def test_mfma_error_model_holds():
 def test_quant_weights_tiny_and_special_blocks():
     lay = Layer(TINY, layer=1)
     wq, ws = O.quant_weights(lay.wgu_bits)
-    assert np.array_equal(host(lay.wgu_q), wq) and np.array_equal(host(lay.wgu_s).view(np.uint32), ws.view(np.uint32))
+    assert np.array_equal(lc.weight_codes_rowmajor(lay.wgu_q), wq) and np.array_equal(host(lay.wgu_s).view(np.uint32), ws.view(np.uint32))
     wq, ws = O.quant_weights(lay.bits["w_down"])
-    assert np.array_equal(host(lay.wd_q), wq) and np.array_equal(host(lay.wd_s).view(np.uint32), ws.view(np.uint32))
+    assert np.array_equal(lc.weight_codes_rowmajor(lay.wd_q), wq) and np.array_equal(host(lay.wd_s).view(np.uint32), ws.view(np.uint32))
     # special blocks: zeros, negative zeros, bf16 subnormals, huge values, a single spike
     rng = np.random.default_rng(0)
     w = (rng.standard_normal((256, 384)) * 0.02).astype(np.float32)
@@ -147,14 +149,14 @@ def test_quant_weights_tiny_and_special_blocks():
     bits = torch.from_numpy(w).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
     gq, gs = lc.quantize_weights(dev_bf16(bits))
     wq, ws = O.quant_weights(bits)
-    assert np.array_equal(host(gq), wq) and np.array_equal(host(gs).view(np.uint32), ws.view(np.uint32))
+    assert np.array_equal(lc.weight_codes_rowmajor(gq), wq) and np.array_equal(host(gs).view(np.uint32), ws.view(np.uint32))
 
 
 def test_quant_weights_full_size_sampled_blocks(big_layer):
     rng = np.random.default_rng(1)
-    gq = host(big_layer.wgu_q)
+    gq = lc.weight_codes_rowmajor(big_layer.wgu_q)
     gs = host(big_layer.wgu_s)
-    dq = host(big_layer.wd_q)
+    dq = lc.weight_codes_rowmajor(big_layer.wd_q)
     ds = host(big_layer.wd_s)
     for (bits, q, s) in ((big_layer.wgu_bits, gq, gs), (big_layer.bits["w_down"], dq, ds)):
         NB, KB = s.shape
@@ -233,6 +235,26 @@ def test_stages_ragged_shapes(M, policy):
     check_norm_exact(xb, lay.bits["norm_w"], host(t["xq"]), host(t["xs"]))
     check_requant_exact(host(t["h_tap"]), host(t["hq"]), host(t["hs"]))
     check_gateup_explained(host(t["xq"]), host(t["xs"]), wgu_q, wgu_s, w.I, host(t["hq"]), host(t["hs"]))
+    check_down_same_operands(host(t["hq"]), host(t["hs"]), wd_q, wd_s, host(t["out_tap"]), host_bf16(t["out"]))
+
+
+@pytest.mark.parametrize("M,H,I", [(5, 256, 384), (32, 640, 1152), (16, 8192, 256), (32, 4096, 384),
+                                   (17, 1152, 2304)])
+def test_skinny_k_parts(M, H, I):
+    """Skinny kernels at K ranges that split unevenly over their K parts: fewer
+    K-groups than parts (H = 256, I = 384), a part one group longer than the
+    others (H = 640), and the longest K the gate/up kernel's LDS holds
+    (H = 8192 at M = 16; 4096 at M = 32)."""
+    _say("skinny M=%d H=%d I=%d" % (M, H, I))
+    lc.lacache_set_path_policy(1)
+    w = synth.Workload(91, "kparts", M, H, I, act="outlier", outlier_ratio=0.02)
+    lay = Layer(w, layer=1)
+    xb = synth.make_x(w, layer=1)
+    t = run_stages(dev_bf16(xb), lay, M, H, I)
+    wgu_q, wgu_s, wd_q, wd_s = lay.host_weights()
+    check_norm_exact(xb, lay.bits["norm_w"], host(t["xq"]), host(t["xs"]))
+    check_requant_exact(host(t["h_tap"]), host(t["hq"]), host(t["hs"]))
+    check_gateup_explained(host(t["xq"]), host(t["xs"]), wgu_q, wgu_s, I, host(t["hq"]), host(t["hs"]))
     check_down_same_operands(host(t["hq"]), host(t["hs"]), wd_q, wd_s, host(t["out_tap"]), host_bf16(t["out"]))
 
 
