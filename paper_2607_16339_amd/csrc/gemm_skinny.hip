@@ -56,7 +56,7 @@ __device__ __forceinline__ v8i cat_frag(u4v lo, u4v hi) {
 
 // gate/up: a workgroup owns kVuPairs (gate, up) slab pairs; each pair's K
 // range is split into kVuKq parts, one wavefront each. The workgroup first
-// copies all M activation rows (codes) into LDS, rows padded by 16 bytes so
+// loads all M activation rows (codes) into LDS, rows padded by 16 bytes so
 // that the 16 rows of an operand read fall on 16 different bank groups; then
 // every wavefront streams its 32 weight rows over its K part. The kVuKq fp32
 // partials meet in LDS and are added in part order before SwiGLU.
@@ -73,7 +73,7 @@ __global__ __launch_bounds__(kVuWaves * 64) void skinny_gateup_kernel(
     const uint8_t* __restrict__ wq, const float* __restrict__ ws,  // weights [2I x K], scales [2I/128 x K/128]
     float* __restrict__ h_tap, float* __restrict__ hbuf, int64_t M, int64_t K, int64_t I) {
   constexpr int R = MT * 16;  // activation rows (padded)
-  __shared__ __align__(16) uint8_t sX[kVuXBytes + 1024];  // codes [R][K + 16]; later the partials
+  __shared__ __align__(16) uint8_t sX[kVuXBytes];  // codes [R][K + 16]; later the partials
   __shared__ __align__(16) float sXs[kVuMaxNkb * R];      // activation scales [K/128][R]
   __shared__ float sWs[kVuWaves][2][kVuMaxNkw];           // each wavefront's (gate, up) block scales
 
@@ -89,21 +89,23 @@ __global__ __launch_bounds__(kVuWaves * 64) void skinny_gateup_kernel(
   const int kb0 = kq * KB / kVuKq, kb1 = (kq + 1) * KB / kVuKq;
   const int nkw = kb1 - kb0;
 
-  // ---- 1. activation codes -> LDS. 16-byte slot s holds row s / cpr, chunk
-  // s % cpr; chunk cpr - 1 is the row's padding (filled with chunk 0).
-  {
-    const int cpr = static_cast<int>(K / 16) + 1;
-    const int ninst = (R * cpr + 63) / 64;
-    for (int u = wave; u < ninst; u += kVuWaves) {
-      const int s = u * 64 + lane;
-      const int row = s / cpr, c = s - (s / cpr) * cpr;
-      const int64_t gr = row < M ? row : M - 1;
-      const int64_t cc = c < cpr - 1 ? c : 0;
-      dma16(aq + gr * K + cc * 16, wave_uniform(static_cast<int>(lds_u32(sX)) + u * 1024));
-    }
+  // ---- 1. activation codes -> registers: the M rows are contiguous, so
+  // 16-byte chunk c = t + 768 j of them is bytes 16c.. of aq; it goes to LDS
+  // byte 16 (c + c / cpr) (rows padded by one chunk). Register loads take
+  // these L2-resident bytes at about twice the per-CU rate of direct-to-LDS
+  // copies, and this copy is the kernel's start-up. Rows M..R-1 of the LDS
+  // stay unwritten: they only feed output rows that are never stored (an
+  // MFMA output row depends on its own activation row alone).
+  constexpr int XCH = (32 * 4096 / 16 + kVuWaves * 64 - 1) / (kVuWaves * 64);  // chunks per thread, at most
+  const int cpr = static_cast<int>(K / 16);  // chunks per row
+  const int nch = static_cast<int>(M) * cpr;
+  u4v xc[XCH];
+#pragma unroll
+  for (int j = 0; j < XCH; ++j) {
+    const int c = t + j * kVuWaves * 64;
+    if (c < nch) xc[j] = *reinterpret_cast<const u4v*>(aq + 16 * static_cast<uint32_t>(c));
   }
-  // ---- 2. scales into registers (after the copies, so waiting for them also
-  // waits for the copies: loads retire in issue order)
+  // ---- 2. scales into registers
   constexpr int XPT = (kVuMaxNkb * R + kVuWaves * 64 - 1) / (kVuWaves * 64);
   float xv[XPT];
 #pragma unroll
@@ -144,14 +146,25 @@ __global__ __launch_bounds__(kVuWaves * 64) void skinny_gateup_kernel(
   for (int u = 0; u < DR; ++u) issue(u, u);
   __builtin_amdgcn_sched_barrier(0);
 
+  {
+    // c / cpr for c < 2^13: the float estimate is off by at most one
+    const float rcpr = 1.0f / static_cast<float>(cpr);
+#pragma unroll
+    for (int j = 0; j < XCH; ++j) {
+      const int c = t + j * kVuWaves * 64;
+      int row = static_cast<int>(static_cast<float>(c) * rcpr);
+      row -= row * cpr > c ? 1 : 0;
+      row += (row + 1) * cpr <= c ? 1 : 0;
+      if (c < nch) *reinterpret_cast<u4v*>(sX + 16 * (c + row)) = xc[j];
+    }
+  }
 #pragma unroll
   for (int j = 0; j < XPT; ++j) {
     const int i = t + j * kVuWaves * 64;
     if (i < KB * R) sXs[i] = xv[j];
   }
   if (sj < kVuMaxNkw) sWs[wave][sn][sj] = wv;
-  wait_vm<4 * DR>();  // this wavefront's copies (issued before the ring) have landed
-  __syncthreads();      // ... and everyone's, and the scales are in LDS
+  __syncthreads();  // the activation codes and the scales are in LDS
 
   float acc[MT][2][4];
 #pragma unroll
