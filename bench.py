@@ -15,9 +15,11 @@ reported either way).
 
 Prints one JSON line. The default workload is the 32-token decode block
 (M=32); --workload selects another. Besides the whole-step throughput the
-line carries the dominant stage's roofline figures (timed live with HIP
-events around graph-captured back-to-back calls of that stage alone) and the
-CPU oracle's throughput on a bounded sample of the same workload.
+line carries the dominant kernel's roofline figures (timed live with HIP
+events around graph-captured back-to-back calls of its stage alone; at
+M <= 32 the gate/up stage minus its small h-quantization kernel, which is
+timed alone the same way) and the CPU oracle's throughput on a bounded sample
+of the same workload.
 
   python bench.py [--gpus 1] [--steps 50] [--warmup 10] [--workload block32_h4096_i12288]
 """
@@ -87,6 +89,9 @@ def stage_bytes(M, H, I):
         "norm": 2 * M * H + 2 * H + M * H + 4 * M * H // g,
         "gateup": 2 * I * H + 4 * (2 * I // g) * (H // g) + M * H + 4 * M * H // g + M * I + 4 * M * I // g,
         "down": H * I + 4 * (H // g) * (I // g) + M * I + 4 * M * I // g + 2 * M * H,
+        # the skinny gate/up's weight-streaming kernel alone: its inputs and
+        # its fp32 h (which the h-quantization kernel then reads)
+        "gateup_stream": 2 * I * H + 4 * (2 * I // g) * (H // g) + M * H + 4 * M * H // g + 4 * M * I,
     }
 
 
@@ -298,9 +303,21 @@ def main():
         "gateup": lambda s: lc.lacache_gateup_swiglu_quant(xq, xs, s["wgu_q"], s["wgu_s"], hq, hs),
         "down": lambda s: lc.lacache_down_proj(hq, hs, s["wd_q"], s["wd_s"], out),
     }
+    names = ["norm", "gateup", "down"]
+    if skinny:
+        # the h-quantization kernel of the skinny gate/up stage, timed alone:
+        # the same kernel on the same sizes (lacache_quant_rows_g at group
+        # granularity) over the real h of the workload
+        hbuf = torch.empty((M, I), dtype=torch.float32, device=dev)
+        lc.lacache_rmsnorm_quant(sets[0]["x"], sets[0]["norm_w"], xq, xs)
+        lc.lacache_gateup_swiglu_quant(xq, xs, sets[0]["wgu_q"], sets[0]["wgu_s"], hq, hs, hbuf)
+        hq2 = torch.empty((M, I), dtype=torch.uint8, device=dev)
+        hs2 = torch.empty((I // 128, M), dtype=torch.float32, device=dev)
+        stage_fn["hquant"] = lambda s: lc.lacache_quant_rows_g(hbuf, hq2, hs2, None, lc.LACACHE_GRAN_GROUP)
+        names.append("hquant")
     reps = max(min(args.steps, 64), 8)
     k_ms = {}
-    for name in ("norm", "gateup", "down"):
+    for name in names:
         fn = stage_fn[name]
         for i in range(S):  # inputs of every stage valid, workspace allocated
             for n2 in ("norm", "gateup", "down"):
@@ -313,7 +330,7 @@ def main():
         g.replay()
         torch.cuda.synchronize()
         # the replay must reproduce the eager result of its last call
-        probe = {"norm": xq, "gateup": hq, "down": out}[name]
+        probe = {"norm": xq, "gateup": hq, "down": out, "hquant": hq2 if skinny else None}[name]
         got = probe.clone()
         fn(sets[(reps - 1) % S])
         torch.cuda.synchronize()
@@ -329,21 +346,32 @@ def main():
         k_ms[name] = e0.elapsed_time(e1) / (nrep * reps)
         del g
     dom = "gateup"
-    kname = dom + ("_skinny" if skinny else "_tiled")
-    # the skinny gate/up stage is the weight-streaming kernel followed by the
-    # small h-quantization kernel; both are inside the timed stage
-    kparts = ["gateup_skinny", "hquant_skinny"] if skinny else ["gateup_tiled"]
     if skinny:
-        achieved = sb[dom] / (k_ms[dom] * 1e-3) / 1e9
+        # The skinny gate/up stage is the weight-streaming kernel followed by
+        # the small h-quantization kernel. The dominant kernel is the first:
+        # its time is the stage's minus the h-quantization kernel's, both timed
+        # live above; the stage's own figure is reported beside it.
+        kparts = ["gateup_skinny"]
+        k_stream = k_ms[dom] - k_ms["hquant"]
+        achieved = sb["gateup_stream"] / (k_stream * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM_GBPS, 4)}
+        roof["kernel"] = "gateup_skinny (the weight stream)"
+        roof["kernel_ms"] = round(k_stream, 5)
+        roof["kernel_ms_from"] = "gate/up stage minus the h-quantization kernel timed alone"
+        roof["algorithmic_bytes"] = sb["gateup_stream"]
+        st_ach = sb[dom] / (k_ms[dom] * 1e-3) / 1e9
+        roof["stage"] = {"kernels": "gateup_skinny + hquant_skinny", "ms": round(k_ms[dom], 5),
+                         "algorithmic_bytes": sb[dom], "achieved": round(st_ach, 1),
+                         "frac": round(st_ach / PEAK_HBM_GBPS, 4)}
     else:
+        kparts = ["gateup_tiled"]
         achieved = 4.0 * M * H * I / (k_ms[dom] * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_FP8_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_FP8_TFLOPS, 4)}
-    roof["kernel"] = " + ".join(kparts)
-    roof["kernel_ms"] = round(k_ms[dom], 5)
-    roof["algorithmic_bytes" if skinny else "algorithmic_flop"] = sb[dom] if skinny else 4 * M * H * I
+        roof["kernel"] = "gateup_tiled"
+        roof["kernel_ms"] = round(k_ms[dom], 5)
+        roof["algorithmic_flop"] = 4 * M * H * I
     roof["traffic"] = None
     try:
         with open(TRAFFIC_FILE) as f:
