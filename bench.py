@@ -292,7 +292,7 @@ def main():
     # weight sets) are captured in a HIP graph, so that the host's per-call
     # cost does not leave the GPU idle between them; the graph is replayed
     # between HIP events on the stream it runs on.
-    skinny = M <= 32
+    skinny = M <= 64
     xq = torch.empty((M, H), dtype=torch.uint8, device=dev)
     xs = torch.empty((H // 128, M), dtype=torch.float32, device=dev)
     hq = torch.empty((M, I), dtype=torch.uint8, device=dev)

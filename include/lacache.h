@@ -35,7 +35,7 @@
  *   Outputs must not overlap inputs.
  * - The caller owns every buffer it passes. The library owns only its
  *   workspace: the intermediates of lacache_ffn_fp8 and the fp32 h of the
- *   skinny (M <= 32) gate/up stage call (see lacache_ffn_fp8).
+ *   skinny (M <= 64) gate/up stage call (see lacache_ffn_fp8).
  * - Results are deterministic: the same inputs give the same output bytes
  *   (no floating-point atomics).
  * - A failed HIP launch or allocation returns LACACHE_ERR_HIP or
@@ -121,7 +121,9 @@ int lacache_add_rmsnorm_quant(void* stream, uint16_t* resid, const uint16_t* y, 
  * accumulated in fp32; h = SiLU(acc[:, j]) * acc[:, I + j].
  * On the skinny path h passes through the library workspace (M x I fp32),
  * and the K range is split into four parts whose fp32 partial sums are
- * added in part order.
+ * added in part order; at 33..64 rows the K range is first split into two
+ * halves (separate workgroups) whose gate and up sums pass through the
+ * workspace and are added in half order before SwiGLU.
  */
 int lacache_gateup_swiglu_quant(void* stream, const uint8_t* xq, const float* xs, const uint8_t* wgu_q,
                                 const float* wgu_s, uint8_t* hq, float* hs, float* h_tap,
@@ -134,8 +136,9 @@ int lacache_gateup_swiglu_quant(void* stream, const uint8_t* xq, const float* xs
  *   out     [M x H] bf16, rounded to nearest-even from fp32         (output)
  *   out_tap [M x H] fp32 or NULL: if non-NULL, also receives the fp32 value
  *           that was rounded (test hook)
- * On the skinny path (M <= 32) the K range is split over eight wavefronts
- * of a workgroup, whose fp32 partial sums are added in wavefront order.
+ * On the skinny path (M <= 64) the K range is split over the four
+ * wavefronts of a workgroup, whose fp32 partial sums are added in wavefront
+ * order.
  */
 int lacache_down_proj(void* stream, const uint8_t* hq, const float* hs, const uint8_t* wd_q, const float* wd_s,
                       uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I, int group);
@@ -361,10 +364,12 @@ size_t lacache_first_layer_workspace_bytes(int64_t R, int64_t heads, int64_t H);
 
 /*
  * Kernel-path policy for the GEMM stages, process-wide:
- *   0 = automatic (the skinny weight-streaming kernels for M <= 32 with
- *       ceil(M/16) 16 (H + 16) <= 131584 bytes, H <= 8192 and I <= 16384;
- *       the tiled MFMA kernels otherwise), 1 = always skinny (other shapes
- *       return LACACHE_ERR_UNSUPPORTED), 2 = always tiled.
+ *   0 = automatic (the skinny weight-streaming kernels for M <= 64 whose
+ *       activation rows fit the gate/up kernel's LDS: ceil(M/16) 16 (H + 16)
+ *       <= 132096 bytes for M <= 32, ceil(M/16) 16 (ceil(H/256) 128 + 16)
+ *       <= 132096 for 33..64 rows; H <= 8192, I <= 16384; the tiled MFMA
+ *       kernels otherwise), 1 = always skinny (other shapes return
+ *       LACACHE_ERR_UNSUPPORTED), 2 = always tiled.
  * Returns the previous policy, or LACACHE_ERR_INVALID_ARG for other values.
  */
 int lacache_set_path_policy(int policy);

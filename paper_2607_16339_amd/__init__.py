@@ -285,7 +285,7 @@ def lacache_first_layer_tokens(token_ids, rows, embed, norm_w, w_qkv, rope_cos, 
 
 
 def lacache_set_path_policy(policy):
-    """0 = automatic, 1 = skinny kernels (M <= 32), 2 = tiled kernels. Returns the previous policy."""
+    """0 = automatic, 1 = skinny kernels (M <= 64), 2 = tiled kernels. Returns the previous policy."""
     r = lib().lacache_set_path_policy(int(policy))
     if r < 0:
         raise LacacheError(r, "lacache_set_path_policy")

@@ -56,63 +56,89 @@ __device__ __forceinline__ v8i cat_frag(u4v lo, u4v hi) {
 
 // gate/up: a workgroup owns kVuPairs (gate, up) slab pairs; each pair's K
 // range is split into kVuKq parts, one wavefront each. The workgroup first
-// loads all M activation rows (codes) into LDS, rows padded by 16 bytes so
-// that the 16 rows of an operand read fall on 16 different bank groups; then
-// every wavefront streams its 32 weight rows over its K part. The kVuKq fp32
-// partials meet in LDS and are added in part order before SwiGLU.
+// loads the M activation rows (codes) of its K range into LDS, rows padded by
+// 16 bytes so that the 16 rows of an operand read fall on 16 different bank
+// groups; then every wavefront streams its 32 weight rows over its K part.
+// The kVuKq fp32 partials meet in LDS and are added in part order.
+// NH = 1: the workgroup covers all of K and applies SwiGLU (h to hbuf).
+// NH = 2 (33..64 rows, whose codes over all of K do not fit the LDS): the
+// workgroups of blockIdx.y = 0, 1 cover the two halves of K and store their
+// gate and up sums to part[y] [M][2I]; the h-quantization kernel adds the two
+// halves in that order and applies SwiGLU.
 constexpr int kVuPairs = 3;
 constexpr int kVuKq = 4;
 constexpr int kVuWaves = kVuPairs * kVuKq;
-constexpr int kVuXBytes = 32 * (4096 + 16);  // activation rows x (K + 16) bytes, at most
-constexpr int kVuMaxNkb = 64;
-constexpr int kVuMaxNkw = kVuMaxNkb / kVuKq;
+constexpr int kVuXBytes = 64 * (2048 + 16);  // activation rows x (K range + 16) bytes, at most
+constexpr int kVuMaxNkb = 64;                 // K-groups of the whole K
+constexpr int kVuMaxNkw = kVuMaxNkb / kVuKq;  // K-groups of one part
+constexpr int kVuScales = 2048;               // activation scales of a workgroup's K range, at most
 
-template <int MT, int DR>
+template <int MT, int DR, int NH>
 __global__ __launch_bounds__(kVuWaves * 64) void skinny_gateup_kernel(
     const uint8_t* __restrict__ aq, const float* __restrict__ as,  // activations [M x K], scales [K/128 x M]
     const uint8_t* __restrict__ wq, const float* __restrict__ ws,  // weights [2I x K], scales [2I/128 x K/128]
     float* __restrict__ h_tap, float* __restrict__ hbuf, int64_t M, int64_t K, int64_t I) {
   constexpr int R = MT * 16;  // activation rows (padded)
-  __shared__ __align__(16) uint8_t sX[kVuXBytes];  // codes [R][K + 16]; later the partials
-  __shared__ __align__(16) float sXs[kVuMaxNkb * R];      // activation scales [K/128][R]
-  __shared__ float sWs[kVuWaves][2][kVuMaxNkw];           // each wavefront's (gate, up) block scales
+  static_assert(NH == 1 || NH == 2, "K pieces");
+  __shared__ __align__(16) uint8_t sX[kVuXBytes];  // codes [R][Kw + 16]; later the partials
+  __shared__ __align__(16) float sXs[kVuScales];   // activation scales [Kw/128][R]
+  __shared__ float sWs[kVuWaves][2][kVuMaxNkw];    // each wavefront's (gate, up) block scales
 
   const int t = threadIdx.x, lane = t & 63;
   const int wave = wave_uniform(t >> 6);
   const int q = lane >> 4, lr = lane & 15;
   const int pw = wave % kVuPairs, kq = wave / kVuPairs;
   const int KB = static_cast<int>(K / 128);
-  const int64_t stride = K + 16;
+  // this workgroup's K range [kbw, kbw + KBW) and its parts
+  const int kh = NH == 1 ? 0 : static_cast<int>(blockIdx.y);
+  const int kbw = kh * KB / NH, KBW = (kh + 1) * KB / NH - kbw;
+  const int64_t Kw = static_cast<int64_t>(KBW) * 128;
+  const int64_t stride = Kw + 16;
   const int64_t npair = I / 16;
   const int64_t pair = static_cast<int64_t>(blockIdx.x) * kVuPairs + pw;
   const int64_t p0 = pair < npair ? pair : npair - 1;  // past the end: a valid pair, never stored
-  const int kb0 = kq * KB / kVuKq, kb1 = (kq + 1) * KB / kVuKq;
+  const int kb0 = kbw + kq * KBW / kVuKq, kb1 = kbw + (kq + 1) * KBW / kVuKq;
   const int nkw = kb1 - kb0;
 
-  // ---- 1. activation codes -> registers: the M rows are contiguous, so
-  // 16-byte chunk c = t + 768 j of them is bytes 16c.. of aq; it goes to LDS
-  // byte 16 (c + c / cpr) (rows padded by one chunk). Register loads take
-  // these L2-resident bytes at about twice the per-CU rate of direct-to-LDS
+  // ---- 1. activation codes -> registers: 16-byte chunk c = t + 768 j of
+  // the M rows' K range (row c / cpr, chunk c % cpr) goes to LDS byte
+  // 16 (c + c / cpr) (rows padded by one chunk). Register loads take these
+  // L2-resident bytes at about twice the per-CU rate of direct-to-LDS
   // copies, and this copy is the kernel's start-up. Rows M..R-1 of the LDS
   // stay unwritten: they only feed output rows that are never stored (an
   // MFMA output row depends on its own activation row alone).
-  constexpr int XCH = (32 * 4096 / 16 + kVuWaves * 64 - 1) / (kVuWaves * 64);  // chunks per thread, at most
-  const int cpr = static_cast<int>(K / 16);  // chunks per row
+  constexpr int XCH = (kVuXBytes / 16 + kVuWaves * 64 - 1) / (kVuWaves * 64);  // chunks per thread, at most
+  const int cpr = KBW * 8;  // chunks per row
   const int nch = static_cast<int>(M) * cpr;
+  // c / cpr for c < 2^14: the float estimate is off by at most one
+  const float rcpr = 1.0f / static_cast<float>(cpr > 0 ? cpr : 1);
+  auto row_of = [&](int c) {
+    int r = static_cast<int>(static_cast<float>(c) * rcpr);
+    r -= r * cpr > c ? 1 : 0;
+    r += (r + 1) * cpr <= c ? 1 : 0;
+    return r;
+  };
   u4v xc[XCH];
 #pragma unroll
   for (int j = 0; j < XCH; ++j) {
     const int c = t + j * kVuWaves * 64;
-    if (c < nch) xc[j] = *reinterpret_cast<const u4v*>(aq + 16 * static_cast<uint32_t>(c));
+    if (c < nch) {
+      // NH = 1: the rows are contiguous; NH = 2: row r's range starts at r K + kbw 128
+      const uint32_t off = NH == 1 ? 16u * static_cast<uint32_t>(c)
+                                   : static_cast<uint32_t>(row_of(c)) * static_cast<uint32_t>(K) +
+                                         static_cast<uint32_t>(kbw) * 128u +
+                                         16u * static_cast<uint32_t>(c - row_of(c) * cpr);
+      xc[j] = *reinterpret_cast<const u4v*>(aq + off);
+    }
   }
   // ---- 2. scales into registers
-  constexpr int XPT = (kVuMaxNkb * R + kVuWaves * 64 - 1) / (kVuWaves * 64);
+  constexpr int XPT = (kVuScales + kVuWaves * 64 - 1) / (kVuWaves * 64);
   float xv[XPT];
 #pragma unroll
   for (int j = 0; j < XPT; ++j) {
     const int i = t + j * kVuWaves * 64;
     const int kb = i / R, m = i % R;
-    xv[j] = (kb < KB && m < M) ? as[static_cast<int64_t>(kb) * M + m] : 0.0f;
+    xv[j] = (kb < KBW && m < M) ? as[static_cast<int64_t>(kbw + kb) * M + m] : 0.0f;
   }
   const int64_t wrow[2] = {16 * p0, I + 16 * p0};
   const int sn = lane >> 5, sj = lane & 31;
@@ -124,9 +150,7 @@ __global__ __launch_bounds__(kVuWaves * 64) void skinny_gateup_kernel(
   const uint8_t* wg = wq + wtile_off(wrow[0] + lr, 16 * q, K);
   const uint8_t* wu = wq + wtile_off(wrow[1] + lr, 16 * q, K);
   // K-group of step j: the part is walked from a workgroup-dependent start
-  // (and wraps), so that the chip's loads spread over the memory channels
-  // instead of all reading one K offset of rows a multiple of 4 KB apart;
-  // steps past the end repeat the last K-group walked
+  // (and wraps); steps past the end repeat the last K-group walked
   const int rot = (kRotateK && nkw > 0) ? static_cast<int>(blockIdx.x % static_cast<unsigned>(nkw)) : 0;
   auto kg_at = [&](int j) {
     if (nkw <= 0) return kb0 < KB ? kb0 : KB - 1;
@@ -146,22 +170,15 @@ __global__ __launch_bounds__(kVuWaves * 64) void skinny_gateup_kernel(
   for (int u = 0; u < DR; ++u) issue(u, u);
   __builtin_amdgcn_sched_barrier(0);
 
-  {
-    // c / cpr for c < 2^13: the float estimate is off by at most one
-    const float rcpr = 1.0f / static_cast<float>(cpr);
 #pragma unroll
-    for (int j = 0; j < XCH; ++j) {
-      const int c = t + j * kVuWaves * 64;
-      int row = static_cast<int>(static_cast<float>(c) * rcpr);
-      row -= row * cpr > c ? 1 : 0;
-      row += (row + 1) * cpr <= c ? 1 : 0;
-      if (c < nch) *reinterpret_cast<u4v*>(sX + 16 * (c + row)) = xc[j];
-    }
+  for (int j = 0; j < XCH; ++j) {
+    const int c = t + j * kVuWaves * 64;
+    if (c < nch) *reinterpret_cast<u4v*>(sX + 16 * (c + row_of(c))) = xc[j];
   }
 #pragma unroll
   for (int j = 0; j < XPT; ++j) {
     const int i = t + j * kVuWaves * 64;
-    if (i < KB * R) sXs[i] = xv[j];
+    if (i < KBW * R) sXs[i] = xv[j];
   }
   if (sj < kVuMaxNkw) sWs[wave][sn][sj] = wv;
   __syncthreads();  // the activation codes and the scales are in LDS
@@ -181,13 +198,14 @@ __global__ __launch_bounds__(kVuWaves * 64) void skinny_gateup_kernel(
   auto step = [&](int j, int u) {
     const bool live = j < nkw;
     const int kg = kg_at(j);
+    const int kl = kg - kbw;  // K-group within the workgroup's range
     const float w0 = live ? sWs[wave][0][kg - kb0] : 0.0f, w1 = live ? sWs[wave][1][kg - kb0] : 0.0f;
     const v8i bg = cat_frag(wr[u][0], wr[u][1]), bu = cat_frag(wr[u][2], wr[u][3]);
 #pragma unroll
     for (int i = 0; i < MT; ++i) {
-      const uint8_t* xr = sX + (16 * i + lr) * stride + kg * 128 + 16 * q;
+      const uint8_t* xr = sX + (16 * i + lr) * stride + kl * 128 + 16 * q;
       const v8i af = cat_frag(*reinterpret_cast<const u4v*>(xr), *reinterpret_cast<const u4v*>(xr + 64));
-      const float4 x4 = *reinterpret_cast<const float4*>(sXs + kg * R + 16 * i + 4 * q);
+      const float4 x4 = *reinterpret_cast<const float4*>(sXs + kl * R + 16 * i + 4 * q);
       const v4f zero = {0.0f, 0.0f, 0.0f, 0.0f};
       const v4f pg = mfma_fp8_16x16x128(af, bg, zero);
       const v4f pu = mfma_fp8_16x16x128(af, bu, zero);
@@ -212,7 +230,8 @@ __global__ __launch_bounds__(kVuWaves * 64) void skinny_gateup_kernel(
     for (int u = 0; u < DR; ++u) step((NR - 1) * DR + u, u);
   }
 
-  // ---- 4. partials [kq][pair][R][32] in LDS, added in part order; SwiGLU
+  // ---- 4. partials [kq][pair][R][32] in LDS, added in part order; then
+  // SwiGLU (NH = 1) or the gate and up sums of this K half (NH = 2)
   __syncthreads();  // every wavefront is done with the activation codes
   float* red = reinterpret_cast<float*>(sX);
 #pragma unroll
@@ -234,9 +253,15 @@ __global__ __launch_bounds__(kVuWaves * 64) void skinny_gateup_kernel(
       g += red[((k * kVuPairs + pp) * R + row) * 32 + col];
       u += red[((k * kVuPairs + pp) * R + row) * 32 + 16 + col];
     }
-    const float h = swiglu_fast(g, u);
-    hbuf[row * I + 16 * pr + col] = h;
-    if (h_tap != nullptr) h_tap[row * I + 16 * pr + col] = h;
+    if (NH == 1) {
+      const float h = swiglu_fast(g, u);
+      hbuf[row * I + 16 * pr + col] = h;
+      if (h_tap != nullptr) h_tap[row * I + 16 * pr + col] = h;
+    } else {
+      float* part = hbuf + static_cast<int64_t>(kh) * M * 2 * I + row * 2 * I;
+      part[16 * pr + col] = g;
+      part[I + 16 * pr + col] = u;
+    }
   }
 }
 
@@ -265,7 +290,7 @@ struct DnCfg {
   static constexpr int kSlot = kA + 2048;
   static constexpr int AI = RA / 8;         // 1 KB copies of activations per slot
   static constexpr int PER = AI + 2;        // copies per slot (activations + the two weight halves)
-  static constexpr int D = MT == 1 ? 8 : 5; // ring depth that fits the LDS
+  static constexpr int D = MT == 1 ? 8 : (MT == 2 ? 5 : (MT == 3 ? 4 : 3));  // ring depth that fits the LDS
 };
 
 template <int MT>
@@ -382,14 +407,6 @@ __global__ __launch_bounds__(kDnSplit * 64) void skinny_down_kernel(
   }
 }
 
-// Shapes the kernels cover: M <= 32 activation rows that fit the gate/up
-// kernel's LDS, and K parts that fit the scale tables.
-bool gateup_v_ok(int64_t M, int64_t K) {
-  const int64_t R = ((M + 15) / 16) * 16;
-  return M <= 32 && R * (K + 16) <= kVuXBytes && K / 128 <= kVuMaxNkb;
-}
-bool down_ok(int64_t M, int64_t K) { return M <= 32 && K / 128 <= kDnSplit * kDnMaxNkbW; }
-
 // h [M x I] fp32 -> 1x128 e4m3 groups (Eq. 7): codes [M x I], scales
 // [I/128 x M]. 16 lanes per group, 8 values per lane.
 __global__ __launch_bounds__(256) void skinny_hquant_kernel(const float* __restrict__ h, uint8_t* __restrict__ hq,
@@ -418,6 +435,63 @@ __global__ __launch_bounds__(256) void skinny_hquant_kernel(const float* __restr
   if (part == 0) hs[g * M + row] = s;
 }
 
+// The same quantization after the two K halves of the gate/up sums are
+// combined: g = part[0] + part[1] and u likewise (in that order), h =
+// SiLU(g) u; parts [2][M][2I] fp32 (gate columns, then up). h_tap: the h
+// that was quantized, or null.
+__global__ __launch_bounds__(256) void skinny_hquant2_kernel(const float* __restrict__ part, uint8_t* __restrict__ hq,
+                                                             float* __restrict__ hs, float* __restrict__ h_tap,
+                                                             int64_t M, int64_t I) {
+  const int64_t gi = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) >> 4;  // group index, row-major
+  const int sub = threadIdx.x & 15;
+  const int64_t G = I / 128;
+  const bool ok = gi < M * G;
+  const int64_t row = ok ? gi / G : 0, g = ok ? gi % G : 0;
+  const int64_t c0 = g * 128 + sub * 8;
+  const float* p0 = part + row * 2 * I;
+  const float* p1 = p0 + M * 2 * I;
+  float v[8];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const float4 ga = *reinterpret_cast<const float4*>(p0 + c0 + 4 * h);
+    const float4 gb = *reinterpret_cast<const float4*>(p1 + c0 + 4 * h);
+    const float4 ua = *reinterpret_cast<const float4*>(p0 + I + c0 + 4 * h);
+    const float4 ub = *reinterpret_cast<const float4*>(p1 + I + c0 + 4 * h);
+    v[4 * h + 0] = swiglu_fast(ga.x + gb.x, ua.x + ub.x);
+    v[4 * h + 1] = swiglu_fast(ga.y + gb.y, ua.y + ub.y);
+    v[4 * h + 2] = swiglu_fast(ga.z + gb.z, ua.z + ub.z);
+    v[4 * h + 3] = swiglu_fast(ga.w + gb.w, ua.w + ub.w);
+  }
+  float m = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) m = __builtin_fmaxf(m, __builtin_fabsf(v[e]));
+  m = max_xor<16>(m);
+  const float s = m / kE4M3Max;
+  uint32_t lo = 0u, hi = 0u;
+  if (s != 0.0f && !(scale_is_fast(s) && enc8_div_fast(v, fast_rcp(s), lo, hi))) {
+    lo = enc4_e4m3(qdiv(v[0], s), qdiv(v[1], s), qdiv(v[2], s), qdiv(v[3], s));
+    hi = enc4_e4m3(qdiv(v[4], s), qdiv(v[5], s), qdiv(v[6], s), qdiv(v[7], s));
+  }
+  if (!ok) return;
+  *reinterpret_cast<uint2*>(hq + row * I + c0) = make_uint2(lo, hi);
+  if (sub == 0) hs[g * M + row] = s;
+  if (h_tap != nullptr) {
+    *reinterpret_cast<float4*>(h_tap + row * I + c0) = make_float4(v[0], v[1], v[2], v[3]);
+    *reinterpret_cast<float4*>(h_tap + row * I + c0 + 4) = make_float4(v[4], v[5], v[6], v[7]);
+  }
+}
+
+// Shapes the kernels cover: M <= 32 activation rows over all of K (NH = 1),
+// or 33..64 rows over half of K (NH = 2), that fit the gate/up kernel's LDS
+// and scale tables; down: K parts that fit its scale tables.
+int gateup_halves(int64_t M) { return M <= 32 ? 1 : 2; }
+bool gateup_v_ok(int64_t M, int64_t K) {
+  const int64_t R = ((M + 15) / 16) * 16, KB = K / 128, nh = gateup_halves(M);
+  const int64_t kbw = (KB + nh - 1) / nh;  // K-groups of the larger piece
+  return M <= 64 && KB <= kVuMaxNkb && R * (kbw * 128 + 16) <= kVuXBytes && kbw * R <= kVuScales;
+}
+bool down_ok(int64_t M, int64_t K) { return M <= 64 && K / 128 <= kDnSplit * kDnMaxNkbW; }
+
 }  // namespace
 
 bool skinny_supported(int64_t M, int64_t H, int64_t I) {
@@ -425,8 +499,9 @@ bool skinny_supported(int64_t M, int64_t H, int64_t I) {
 }
 
 size_t skinny_gateup_ws_bytes(int64_t M, int64_t I) {
-  const size_t h = static_cast<size_t>(M) * static_cast<size_t>(I) * sizeof(float);
-  return ((h + 255) / 256) * 256;
+  // h [M x I] fp32, or for 33..64 rows the two K halves' gate and up sums [2][M][2I]
+  const size_t n = static_cast<size_t>(M) * static_cast<size_t>(I) * (gateup_halves(M) == 1 ? 1 : 4);
+  return ((n * sizeof(float) + 255) / 256) * 256;
 }
 
 // ws_buf: an fp32 buffer of skinny_gateup_ws_bytes() for h. The shape must
@@ -435,18 +510,26 @@ hipError_t launch_gateup_skinny(hipStream_t st, const uint8_t* xq, const float* 
                                 const float* ws, uint8_t* hq, float* hs, float* h_tap, int64_t M, int64_t H,
                                 int64_t I, void* ws_buf) {
   float* hbuf = static_cast<float*>(ws_buf);
-  const unsigned grid = static_cast<unsigned>((I / 16 + kVuPairs - 1) / kVuPairs);
+  const unsigned gx = static_cast<unsigned>((I / 16 + kVuPairs - 1) / kVuPairs);
+  const dim3 block(kVuWaves * 64);
+  const int64_t groups = M * (I / 128);
+  const dim3 qgrid(static_cast<unsigned>((groups + 15) / 16)), qblock(256);
   if (M <= 16)
-    hipLaunchKernelGGL((skinny_gateup_kernel<1, kVuDR>), dim3(grid), dim3(kVuWaves * 64), 0, st, xq, xs, wq, ws, h_tap,
-                       hbuf, M, H, I);
+    hipLaunchKernelGGL((skinny_gateup_kernel<1, kVuDR, 1>), dim3(gx), block, 0, st, xq, xs, wq, ws, h_tap, hbuf, M, H, I);
+  else if (M <= 32)
+    hipLaunchKernelGGL((skinny_gateup_kernel<2, kVuDR, 1>), dim3(gx), block, 0, st, xq, xs, wq, ws, h_tap, hbuf, M, H, I);
+  else if (M <= 48)
+    hipLaunchKernelGGL((skinny_gateup_kernel<3, kVuDR, 2>), dim3(gx, 2), block, 0, st, xq, xs, wq, ws, h_tap, hbuf, M, H,
+                       I);
   else
-    hipLaunchKernelGGL((skinny_gateup_kernel<2, kVuDR>), dim3(grid), dim3(kVuWaves * 64), 0, st, xq, xs, wq, ws, h_tap,
-                       hbuf, M, H, I);
+    hipLaunchKernelGGL((skinny_gateup_kernel<4, kVuDR, 2>), dim3(gx, 2), block, 0, st, xq, xs, wq, ws, h_tap, hbuf, M, H,
+                       I);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int64_t groups = M * (I / 128);
-  hipLaunchKernelGGL(skinny_hquant_kernel, dim3(static_cast<unsigned>((groups + 15) / 16)), dim3(256), 0, st, hbuf, hq,
-                     hs, M, I);
+  if (M <= 32)
+    hipLaunchKernelGGL(skinny_hquant_kernel, qgrid, qblock, 0, st, hbuf, hq, hs, M, I);
+  else
+    hipLaunchKernelGGL(skinny_hquant2_kernel, qgrid, qblock, 0, st, hbuf, hq, hs, h_tap, M, I);
   return hipGetLastError();
 }
 
@@ -463,8 +546,12 @@ hipError_t launch_down_skinny(hipStream_t st, const uint8_t* hq, const float* hs
   const dim3 grid(static_cast<unsigned>(H / 16)), block(kDnSplit * 64);
   if (M <= 16)
     hipLaunchKernelGGL(skinny_down_kernel<1>, grid, block, 0, st, hq, hs, wq, ws, out, out_tap, M, I, H);
-  else
+  else if (M <= 32)
     hipLaunchKernelGGL(skinny_down_kernel<2>, grid, block, 0, st, hq, hs, wq, ws, out, out_tap, M, I, H);
+  else if (M <= 48)
+    hipLaunchKernelGGL(skinny_down_kernel<3>, grid, block, 0, st, hq, hs, wq, ws, out, out_tap, M, I, H);
+  else
+    hipLaunchKernelGGL(skinny_down_kernel<4>, grid, block, 0, st, hq, hs, wq, ws, out, out_tap, M, I, H);
   return hipGetLastError();
 }
 

@@ -70,7 +70,7 @@ hipError_t launch_down_tiled(hipStream_t st, const uint8_t* hq, const float* hs,
 // checks that the activation rows fit the gate/up kernel's LDS).
 // The gate/up stage needs an fp32 scratch buffer of skinny_gateup_ws_bytes()
 // (no initial contents) for h; the down stage needs none.
-constexpr int64_t kSkinnyMaxM = 32;
+constexpr int64_t kSkinnyMaxM = 64;
 bool skinny_supported(int64_t M, int64_t H, int64_t I);
 size_t skinny_gateup_ws_bytes(int64_t M, int64_t I);
 hipError_t launch_gateup_skinny(hipStream_t st, const uint8_t* xq, const float* xs, const uint8_t* wq,

@@ -156,11 +156,13 @@ def test_path_policy(L):
     try:
         f = Fake()
         p = [f() for _ in range(8)]
-        # skinny kernels only take M <= 32
-        assert L.lacache_gateup_swiglu_quant(None, p[0], p[1], p[2], p[3], p[4], p[5], None, 33, 256, 768, 128) == UNSUP
-        assert L.lacache_down_proj(None, p[0], p[1], p[2], p[3], p[4], None, 33, 256, 768, 128) == UNSUP
-        # ... whose activation rows fit the gate/up kernel's LDS (16 rows x 8192, 32 rows x 4096) ...
+        # skinny kernels only take M <= 64
+        assert L.lacache_gateup_swiglu_quant(None, p[0], p[1], p[2], p[3], p[4], p[5], None, 65, 256, 768, 128) == UNSUP
+        assert L.lacache_down_proj(None, p[0], p[1], p[2], p[3], p[4], None, 65, 256, 768, 128) == UNSUP
+        # ... whose activation rows fit the gate/up kernel's LDS (16 rows x 8192, 32 rows x 4096; 64 rows x
+        # half of 4096) ...
         assert L.lacache_gateup_swiglu_quant(None, p[0], p[1], p[2], p[3], p[4], p[5], None, 17, 8192, 768, 128) == UNSUP
+        assert L.lacache_gateup_swiglu_quant(None, p[0], p[1], p[2], p[3], p[4], p[5], None, 64, 4224, 768, 128) == UNSUP
         # ... and H <= 8192, I <= 16384 (the scales of a K range are staged in LDS)
         assert L.lacache_gateup_swiglu_quant(None, p[0], p[1], p[2], p[3], p[4], p[5], None, 8, 8320, 768, 128) == UNSUP
         assert L.lacache_down_proj(None, p[0], p[1], p[2], p[3], p[4], None, 8, 256, 16512, 128) == UNSUP
@@ -177,6 +179,10 @@ def test_workspace_bytes_and_status_strings(L):
     # skinny gate/up h (M x I) or the tiled down GEMM's split-K partials
     # (16 output tiles -> 6 splits of 16 K-groups: 6 x M x H)
     scratch = max(a256(M * I * 4), a256(6 * M * H * 4))
+    # (at 33..64 rows the skinny gate/up keeps the two K halves' gate and up sums: 2 x M x 2I)
+    assert L.lacache_ffn_workspace_bytes(64, H, I, 128) == (
+        max(a256(2 * 64 * 2 * I * 4), a256(6 * 64 * H * 4)) + a256(64 * H) + a256(H // 128 * 64 * 4)
+        + a256(64 * I) + a256(I // 128 * 64 * 4))
     want = scratch + a256(M * H) + a256(H // 128 * M * 4) + a256(M * I) + a256(I // 128 * M * 4)
     assert L.lacache_ffn_workspace_bytes(M, H, I, 128) == want
     M = 512

@@ -239,12 +239,15 @@ def test_stages_ragged_shapes(M, policy):
 
 
 @pytest.mark.parametrize("M,H,I", [(5, 256, 384), (32, 640, 1152), (16, 8192, 256), (32, 4096, 384),
-                                   (17, 1152, 2304)])
+                                   (17, 1152, 2304), (3, 128, 256), (2, 256, 128), (33, 512, 384),
+                                   (48, 4096, 384), (64, 1152, 256), (64, 4096, 128)])
 def test_skinny_k_parts(M, H, I):
     """Skinny kernels at K ranges that split unevenly over their K parts: fewer
-    K-groups than parts (H = 256, I = 384), a part one group longer than the
-    others (H = 640), and the longest K the gate/up kernel's LDS holds
-    (H = 8192 at M = 16; 4096 at M = 32)."""
+    K-groups than parts (H = 256, I = 384; a single K-group at H = 128), a part
+    one group longer than the others (H = 640), the longest K the gate/up
+    kernel's LDS holds (H = 8192 at M = 16; 4096 at M = 32), I = 128 (8 slab
+    pairs: the last workgroup has an idle pair), and 33..64 rows, where the
+    gate/up workgroups take one half of K each (odd K-group counts: H = 1152)."""
     _say("skinny M=%d H=%d I=%d" % (M, H, I))
     lc.lacache_set_path_policy(1)
     w = synth.Workload(91, "kparts", M, H, I, act="outlier", outlier_ratio=0.02)
