@@ -18,8 +18,8 @@ Prints one JSON line. The default workload is the 32-token decode block
 line carries the dominant kernel's roofline figures (timed live with HIP
 events around graph-captured back-to-back calls of its stage alone; at
 M <= 32 the gate/up stage minus its small h-quantization kernel, which is
-timed alone the same way) and the CPU oracle's throughput on a bounded sample
-of the same workload.
+timed alone the same way; at 33..64 rows the whole gate/up stage) and the
+CPU oracle's throughput on a bounded sample of the same workload.
 
   python bench.py [--gpus 1] [--steps 50] [--warmup 10] [--workload block32_h4096_i12288]
 """
@@ -304,7 +304,11 @@ def main():
         "down": lambda s: lc.lacache_down_proj(hq, hs, s["wd_q"], s["wd_s"], out),
     }
     names = ["norm", "gateup", "down"]
-    if skinny:
+    # at M <= 32 the skinny gate/up stage ends with the h-quantization kernel
+    # that lacache_quant_rows_g launches alone (33..64 rows: a variant that
+    # also adds the two K halves)
+    split_stage = skinny and M <= 32
+    if split_stage:
         # the h-quantization kernel of the skinny gate/up stage, timed alone:
         # the same kernel on the same sizes (lacache_quant_rows_g at group
         # granularity) over the real h of the workload
@@ -330,7 +334,7 @@ def main():
         g.replay()
         torch.cuda.synchronize()
         # the replay must reproduce the eager result of its last call
-        probe = {"norm": xq, "gateup": hq, "down": out, "hquant": hq2 if skinny else None}[name]
+        probe = {"norm": xq, "gateup": hq, "down": out, "hquant": hq2 if split_stage else None}[name]
         got = probe.clone()
         fn(sets[(reps - 1) % S])
         torch.cuda.synchronize()
@@ -346,7 +350,7 @@ def main():
         k_ms[name] = e0.elapsed_time(e1) / (nrep * reps)
         del g
     dom = "gateup"
-    if skinny:
+    if split_stage:
         # The skinny gate/up stage is the weight-streaming kernel followed by
         # the small h-quantization kernel. The dominant kernel is the first:
         # its time is the stage's minus the h-quantization kernel's, both timed
@@ -364,6 +368,14 @@ def main():
         roof["stage"] = {"kernels": "gateup_skinny + hquant_skinny", "ms": round(k_ms[dom], 5),
                          "algorithmic_bytes": sb[dom], "achieved": round(st_ach, 1),
                          "frac": round(st_ach / PEAK_HBM_GBPS, 4)}
+    elif skinny:
+        kparts = ["gateup_skinny", "hquant_skinny"]
+        achieved = sb[dom] / (k_ms[dom] * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBPS, 4)}
+        roof["kernel"] = "gateup_skinny + hquant_skinny (the stage)"
+        roof["kernel_ms"] = round(k_ms[dom], 5)
+        roof["algorithmic_bytes"] = sb[dom]
     else:
         kparts = ["gateup_tiled"]
         achieved = 4.0 * M * H * I / (k_ms[dom] * 1e-3) / 1e12
