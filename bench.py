@@ -14,7 +14,11 @@ synchronizations; --eager times the plain host loop instead (its figures are
 reported either way).
 
 Prints one JSON line. The default workload is the 32-token decode block
-(M=32); --workload selects another. Besides the whole-step throughput the
+(M=32); --workload selects another. For the 31-layer stack
+(stack31_m512_h4096_i12288) a step is one denoising step through all 31
+layers (all resident in HBM), with the residual adds between them (fused into
+the next layer's norm, the last one a plain add); 32 steps by default, one per
+denoising step, each on its own input. Besides the whole-step throughput the
 line carries the dominant kernel's roofline figures (timed live with HIP
 events around graph-captured back-to-back calls of its stage alone; at
 M <= 32 the gate/up stage minus its small h-quantization kernel, which is
@@ -51,7 +55,8 @@ KERNEL_SOURCES = {
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--steps", type=int, default=None,
+                   help="timed steps (default 50; 32 for the stack, one step per denoising step)")
     p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--workload", default="block32_h4096_i12288",
                    help="an FFN workload, an attention workload (attn_*: the first-layer FACache attention), or "
@@ -171,6 +176,8 @@ def main():
     if args.traffic_from:
         traffic_from(*args.traffic_from)
         return
+    if args.steps is None:
+        args.steps = 32 if args.workload.startswith("stack") else 50
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: the library has no multi-GPU path (the FFN shards by rows with no "
@@ -201,25 +208,54 @@ def main():
     def dev_bf16(bits):
         return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16).copy()).view(torch.bfloat16).to(dev)
 
-    # ---- weights: several layers, quantized on the GPU; bf16 copies freed
-    sets = []
-    for layer in range(1, args.weight_sets + 1):
-        b = synth.make_weights(w, layer)
-        wgu = dev_bf16(np.concatenate([b["w_gate"], b["w_up"]], axis=0))
-        wgu_q, wgu_s = lc.quantize_weights(wgu)
-        del wgu
-        wd = dev_bf16(b["w_down"])
-        wd_q, wd_s = lc.quantize_weights(wd)
-        del wd
-        x = dev_bf16(synth.make_x(w, layer=layer, step=layer - 1))
-        sets.append(dict(norm_w=dev_bf16(b["norm_w"]), wgu_q=wgu_q, wgu_s=wgu_s, wd_q=wd_q, wd_s=wd_s, x=x))
-    torch.cuda.synchronize()
-    out = torch.empty((M, H), dtype=torch.bfloat16, device=dev)
-    S = len(sets)
+    L = w.layers
+    if w.act == "stack":
+        # ---- the stack: one step is one denoising step through all L layers.
+        # Layer 1 runs the plain FFN on the step's input; layers 2..L add the
+        # previous layer's output into the residual stream inside their norm
+        # (AddNorm); the last output is added at the end.
+        layers = stack_weights(w, dev_bf16)
+        xin = [dev_bf16(synth.make_x(w, layer=1, step=t)) for t in range(w.steps)]
+        resid = torch.empty((M, H), dtype=torch.bfloat16, device=dev)
+        outs = [torch.empty((M, H), dtype=torch.bfloat16, device=dev) for _ in range(2)]
 
-    def step(i):
-        s = sets[i % S]
-        lc.lacache_ffn_fp8(s["x"], s["norm_w"], s["wgu_q"], s["wgu_s"], s["wd_q"], s["wd_s"], out)
+        def step(i):
+            resid.copy_(xin[i % len(xin)])
+            a = layers[0]
+            lc.lacache_ffn_fp8(resid, a["norm_w"], a["wgu_q"], a["wgu_s"], a["wd_q"], a["wd_s"], outs[0])
+            for layer in range(1, L):
+                a = layers[layer]
+                lc.lacache_ffn_fp8_addnorm(resid, outs[(layer - 1) % 2], a["norm_w"], a["wgu_q"], a["wgu_s"],
+                                           a["wd_q"], a["wd_s"], outs[layer % 2])
+            lc.lacache_add_bf16(resid, outs[(L - 1) % 2])
+
+        probe = resid
+        out = outs[0]
+        # the stage timings below use the first layers on the first steps' inputs
+        sets = [dict(layers[i], x=xin[i]) for i in range(min(args.weight_sets, L))]
+    else:
+        # ---- weights: several layers, quantized on the GPU; bf16 copies freed
+        sets = []
+        for layer in range(1, args.weight_sets + 1):
+            b = synth.make_weights(w, layer)
+            wgu = dev_bf16(np.concatenate([b["w_gate"], b["w_up"]], axis=0))
+            wgu_q, wgu_s = lc.quantize_weights(wgu)
+            del wgu
+            wd = dev_bf16(b["w_down"])
+            wd_q, wd_s = lc.quantize_weights(wd)
+            del wd
+            x = dev_bf16(synth.make_x(w, layer=layer, step=layer - 1))
+            sets.append(dict(norm_w=dev_bf16(b["norm_w"]), wgu_q=wgu_q, wgu_s=wgu_s, wd_q=wd_q, wd_s=wd_s, x=x))
+        out = torch.empty((M, H), dtype=torch.bfloat16, device=dev)
+        S = len(sets)
+
+        def step(i):
+            s = sets[i % S]
+            lc.lacache_ffn_fp8(s["x"], s["norm_w"], s["wgu_q"], s["wgu_s"], s["wd_q"], s["wd_s"], out)
+
+        probe = out
+    torch.cuda.synchronize()
+    S = len(sets)
 
     stream = torch.cuda.current_stream()
     # eager: one host call per step, per-step events
@@ -249,10 +285,10 @@ def main():
         for _ in range(max(3, args.warmup // args.steps)):
             g.replay()
         torch.cuda.synchronize()
-        got = out.clone()
+        got = probe.clone()
         step(args.steps - 1)
         torch.cuda.synchronize()
-        if not torch.equal(got, out):
+        if not torch.equal(got, probe):
             raise RuntimeError("graph replay of the FFN step differs from the eager call")
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
@@ -281,10 +317,10 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    flop = 6.0 * M * H * I
+    flop = 6.0 * M * H * I * L
     tflops = flop / (ms * 1e-3) / 1e12
     tok_s = M / (ms * 1e-3)
-    bytes_min = 3 * H * I + 4 * (3 * I // 128) * (H // 128) + 2 * H + 4 * M * H
+    bytes_min = (3 * H * I + 4 * (3 * I // 128) * (H // 128) + 2 * H + 4 * M * H) * L
     gbps = bytes_min / (ms * 1e-3) / 1e9
 
     # ---- each stage timed alone: the stage entry points launch the same
@@ -398,8 +434,9 @@ def main():
         "metric": METRIC, "value": round(tflops, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "fp8_e4m3 (fp32 accumulate)", "data": "synthetic",
-        "config": {"workload": args.workload, "M": M, "H": H, "I": I, "group": 128, "weight_sets": S,
-                   "path": "skinny" if skinny else "tiled"},
+        "config": {"workload": args.workload, "M": M, "H": H, "I": I, "group": 128,
+                   "weight_sets": L if w.act == "stack" else S, "path": "skinny" if skinny else "tiled",
+                   "layers": L},
         "tokens_per_s": round(tok_s, 1), "hbm_GBps_min_bytes": round(gbps, 1),
         "frac_hbm_peak": round(gbps / PEAK_HBM_GBPS, 4), "frac_fp8_peak": round(tflops / PEAK_FP8_TFLOPS, 4),
         "step_timing": "HIP graph replay of the K steps" if ms_graph is not None else "eager host loop",
@@ -415,6 +452,34 @@ def main():
     if not args.no_cpu_baseline and not args.profile_only:
         line["cpu_baseline"] = cpu_baseline(w, sets, out, dev)
     print(json.dumps(line), flush=True)
+
+
+def stack_weights(w, dev_bf16):
+    """The FP8 weights of the stack's layers 1..L: each layer's seeded bf16
+    weights drawn on host threads (the generator releases the GIL), then
+    quantized on the GPU; the host and bf16 device copies are freed."""
+    from concurrent.futures import ThreadPoolExecutor, as_completed
+
+    import numpy as np
+
+    import paper_2607_16339_amd as lc
+    import synth
+
+    layers = [None] * w.layers
+    with ThreadPoolExecutor(max_workers=min(8, os.cpu_count() or 1)) as ex:
+        futs = {ex.submit(synth.make_weights, w, layer): layer for layer in range(1, w.layers + 1)}
+        for f in as_completed(futs):
+            b = f.result()
+            wgu = dev_bf16(np.concatenate([b["w_gate"], b["w_up"]], axis=0))
+            wgu_q, wgu_s = lc.quantize_weights(wgu)
+            del wgu
+            wd = dev_bf16(b["w_down"])
+            wd_q, wd_s = lc.quantize_weights(wd)
+            del wd
+            layers[futs[f] - 1] = dict(norm_w=dev_bf16(b["norm_w"]), wgu_q=wgu_q, wgu_s=wgu_s, wd_q=wd_q,
+                                       wd_s=wd_s)
+            del b
+    return layers
 
 
 def error_vs_bf16(w, s, out, dev, rows=8):

@@ -71,8 +71,9 @@ hipError_t launch_quant_weights(hipStream_t st, const uint16_t* w, uint8_t* wq, 
 // quantizes the passes t with t mod (1 << wpr_log2) equal to its index in the
 // row (several wavefronts per row shorten the path of a small-M call).
 // With y (the fused AddNorm), the row is first x = RNE_bf16(float(x) +
-// float(y)), written back in place; a row then has one wavefront, which reads
-// all of it before writing any of it. With kF32Out the normalized row goes to
+// float(y)), written back in place: each wavefront of the row writes its own
+// passes, after a workgroup barrier that follows every wavefront's reads of
+// the old row. With kF32Out the normalized row goes to
 // yf (fp32) instead of being quantized (the coarse-granularity paths).
 // ---------------------------------------------------------------------------
 template <int T, bool kF32Out = false>
@@ -84,7 +85,10 @@ __global__ __launch_bounds__(256) void rmsnorm_quant_kernel(uint16_t* x, const u
   const int wave = threadIdx.x >> 6;
   const int part = wave & ((1 << wpr_log2) - 1);
   const int64_t row = (static_cast<int64_t>(blockIdx.x) * (blockDim.x >> 6) + wave) >> wpr_log2;
-  if (row >= M) return;  // uniform per wavefront; no workgroup barrier below
+  // uniform per wavefront, and per workgroup when a row has several
+  // wavefronts (the workgroup is then that row): the AddNorm barrier below is
+  // reached by every wavefront of the workgroup or by none
+  if (row >= M) return;
   const int nchunk = H >> 3;
   const uint4* xr = reinterpret_cast<const uint4*>(x + row * H);  // (read before any write of the row)
   const uint4* wr = reinterpret_cast<const uint4*>(nw);
@@ -100,15 +104,13 @@ __global__ __launch_bounds__(256) void rmsnorm_quant_kernel(uint16_t* x, const u
     wv[t] = wr[cc];
     if (y != nullptr) yv[t] = reinterpret_cast<const uint4*>(y + row * H)[cc];
   }
-  if (y != nullptr) {  // the residual add, written back in place
-    uint4* xw = reinterpret_cast<uint4*>(x + row * H);
+  if (y != nullptr) {  // the residual add, in registers (written back below)
 #pragma unroll
     for (int t = 0; t < T; ++t) {
       uint32_t* a = reinterpret_cast<uint32_t*>(&xv[t]);
       const uint32_t* b = reinterpret_cast<const uint32_t*>(&yv[t]);
 #pragma unroll
       for (int e = 0; e < 4; ++e) a[e] = pack_bf16x2(bf16lo(a[e]) + bf16lo(b[e]), bf16hi(a[e]) + bf16hi(b[e]));
-      if (t * 64 + lane < nchunk) xw[t * 64 + lane] = xv[t];
     }
   }
 #pragma unroll
@@ -128,6 +130,16 @@ __global__ __launch_bounds__(256) void rmsnorm_quant_kernel(uint16_t* x, const u
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) p = p + __shfl_xor(p, o, 64);
   const float r = static_cast<float>(1.0 / __builtin_sqrt(p / static_cast<double>(H) + 1e-5));
+  if (y != nullptr) {
+    // every wavefront of the row has used all of the old row (the sum above)
+    // before any writes its passes of the new one; the row's wavefronts are
+    // one workgroup (wpr_log2 > 0) or a single wavefront
+    if (wpr_log2 > 0) __syncthreads();
+    uint4* xw = reinterpret_cast<uint4*>(x + row * H);
+#pragma unroll
+    for (int t = 0; t < T; ++t)
+      if ((t & ((1 << wpr_log2) - 1)) == part && t * 64 + lane < nchunk) xw[t * 64 + lane] = xv[t];
+  }
 #pragma unroll
   for (int t = 0; t < T; ++t) {
     if ((t & ((1 << wpr_log2) - 1)) != part) continue;  // uniform
@@ -169,10 +181,10 @@ __global__ __launch_bounds__(256) void rmsnorm_quant_kernel(uint16_t* x, const u
 hipError_t launch_rmsnorm_quant(hipStream_t st, uint16_t* x, const uint16_t* nw, uint8_t* xq, float* xs, int64_t M,
                                 int64_t H, const uint16_t* y) {
   const int T = static_cast<int>((H + 511) / 512);
-  // small M: up to 4 wavefronts per row (one row per workgroup); large M, or
-  // the in-place residual add: one wavefront per row, 4 rows per workgroup
+  // small M: up to 4 wavefronts per row (one row per workgroup); large M:
+  // one wavefront per row, 4 rows per workgroup
   int wl = 0;
-  if (M <= 1024 && y == nullptr) wl = T >= 4 ? 2 : (T >= 2 ? 1 : 0);
+  if (M <= 1024) wl = T >= 4 ? 2 : (T >= 2 ? 1 : 0);
   const int64_t waves = M << wl;
   const int per_block = wl > 0 ? (1 << wl) : 4;
   dim3 grid(static_cast<unsigned>((waves + per_block - 1) / per_block)), block(64 * per_block);

@@ -190,6 +190,30 @@ def test_rmsnorm_quant_bit_exact(M, H):
     check_norm_exact(xb, wb, host(xq), host(xs))
 
 
+@pytest.mark.parametrize("M,H", [(5, 256), (9, 1024), (17, 2176), (64, 16384), (1030, 512)])
+def test_add_rmsnorm_quant_bit_exact(M, H):
+    """The AddNorm kernel at 1, 2 and 4 wavefronts per row (H = 256, 1024,
+    >= 2048 at M <= 1024; 2176 leaves the last pass ragged) and at one
+    wavefront per row (M > 1024): resid = RNE(resid + y) in place, then the
+    norm and quantization of the new resid, all bit-exact."""
+    _say("add_rmsnorm M=%d H=%d" % (M, H))
+    rng = np.random.default_rng(M * 11 + H)
+    x = rng.standard_normal((M, H)).astype(np.float32) * np.exp(rng.uniform(-3, 3, (M, 1))).astype(np.float32)
+    yv = rng.standard_normal((M, H)).astype(np.float32) * 0.5
+    x[:, rng.choice(H, max(1, H // 100), replace=False)] *= 40
+    to_bits = lambda a: torch.from_numpy(a).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    xb, yb = to_bits(x), to_bits(yv)
+    wb = to_bits((1 + 0.02 * rng.standard_normal(H)).astype(np.float32))
+    want = O.residual_add(xb, yb)
+    r = dev_bf16(xb)
+    xq = torch.full((M, H), 0xFF, dtype=torch.uint8, device=DEV)
+    xs = torch.full((H // 128, M), float("nan"), dtype=torch.float32, device=DEV)
+    lc.lacache_add_rmsnorm_quant(r, dev_bf16(yb), dev_bf16(wb), xq, xs)
+    torch.cuda.synchronize()
+    assert np.array_equal(host_bf16(r), want)
+    check_norm_exact(want, wb, host(xq), host(xs))
+
+
 def test_rmsnorm_quant_full_batch_sampled_rows():
     lay = Layer(BATCH8K, layer=1, quantize=False)
     xb = synth.make_x(BATCH8K, layer=1, step=0)
