@@ -32,6 +32,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -79,10 +80,16 @@ def parse():
 
 
 def source_sha(kernel):
+    """Hash of the kernel's sources with comments and blank space removed:
+    counter data stay attached to the code they were taken on, and only a
+    change of code (not of its comments) detaches them."""
     h = hashlib.sha256()
     for f in KERNEL_SOURCES[kernel]:
-        with open(os.path.join(ROOT, "paper_2607_16339_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_2607_16339_amd", "csrc", f), encoding="utf-8") as fh:
+            t = fh.read()
+        t = re.sub(r"/\*.*?\*/", "", t, flags=re.S)
+        t = re.sub(r"//[^\n]*", "", t)
+        h.update("\n".join(ln.strip() for ln in t.splitlines() if ln.strip()).encode())
     return h.hexdigest()[:16]
 
 

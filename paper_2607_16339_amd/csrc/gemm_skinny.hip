@@ -1,4 +1,4 @@
-// Skinny-M (M <= 32) FP8 GEMMs for block-only calls (Sec. 3.4 linears at a
+// Skinny-M (M <= 64) FP8 GEMMs for block-only calls (Sec. 3.4 linears at a
 // decode block's 32 tokens). At this size the FFN is bound by streaming the
 // fp8 weights from HBM once, so the kernels are built around that stream.
 // Each K-group of each 16 x 16 output tile is one 16x16x128 FP8 MFMA, added
@@ -8,15 +8,17 @@
 //
 // gate/up: a workgroup owns 3 (gate, up) slab pairs x 4 K parts (one
 //          wavefront each). The activation codes are copied into LDS once
-//          per workgroup; the weights go global -> VGPRs with non-temporal
+//          per workgroup (up to 32 rows over all of K; 33..64 rows over
+//          one half of K, the halves in two workgroups); the weights go global -> VGPRs with non-temporal
 //          16-byte loads straight into the MFMA operand layout, a ring of
 //          K-groups per wavefront in straight-line code (the compiler waits
 //          for one K-group's registers at a time). The weight tile layout
 //          (wtile_off) makes each load read 1 KB contiguous; on a row-major
 //          matrix the same operand layout reads 16 rows x 64 bytes per load,
 //          which streams about 25 % slower on gfx950. SwiGLU after the
-//          partials are added; h stored as fp32. A second kernel quantizes h
-//          per 1x128 group (a group's columns come from several workgroups,
+//          partials are added; h stored as fp32 (33..64 rows: the gate and
+//          up sums of each K half, added by the second kernel before
+//          SwiGLU). A second kernel quantizes h per 1x128 group (a group's columns come from several workgroups,
 //          and stream order is the cheapest way to make all of them visible:
 //          device-scope fences inside the kernel cost more than the stream).
 // down:    16 output columns per workgroup, 4 K parts, direct-to-LDS copies
