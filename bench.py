@@ -53,7 +53,7 @@ KERNEL_SOURCES = {
 }
 
 
-def parse():
+def parse(argv=None):
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=None,
@@ -76,21 +76,31 @@ def parse():
     p.add_argument("--traffic-from", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "WORKLOAD"),
                    help="turn two rocprofv3 --pmc counter CSVs (FETCH_SIZE, WRITE_SIZE) of a --calibrate-copy "
                         "run into per-launch HBM bytes in profiles/pmc_traffic.json, then exit")
-    return p.parse_args()
+    args = p.parse_args(argv)
+    if args.steps is None:
+        args.steps = 32 if args.workload.startswith("stack") else 50
+    return args
 
 
-def source_sha(kernel):
-    """Hash of the kernel's sources with comments and blank space removed:
-    counter data stay attached to the code they were taken on, and only a
-    change of code (not of its comments) detaches them."""
+def code_hash(texts):
+    """Hash of C++/HIP source texts with comments and blank space removed."""
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES[kernel]:
-        with open(os.path.join(ROOT, "paper_2607_16339_amd", "csrc", f), encoding="utf-8") as fh:
-            t = fh.read()
+    for t in texts:
         t = re.sub(r"/\*.*?\*/", "", t, flags=re.S)
         t = re.sub(r"//[^\n]*", "", t)
         h.update("\n".join(ln.strip() for ln in t.splitlines() if ln.strip()).encode())
     return h.hexdigest()[:16]
+
+
+def source_sha(kernel):
+    """Hash of the kernel's sources without comments: counter data stay
+    attached to the code they were taken on, and only a change of code (not
+    of its comments) detaches them."""
+    texts = []
+    for f in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, "paper_2607_16339_amd", "csrc", f), encoding="utf-8") as fh:
+            texts.append(fh.read())
+    return code_hash(texts)
 
 
 def stage_bytes(M, H, I):
@@ -183,8 +193,6 @@ def main():
     if args.traffic_from:
         traffic_from(*args.traffic_from)
         return
-    if args.steps is None:
-        args.steps = 32 if args.workload.startswith("stack") else 50
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: the library has no multi-GPU path (the FFN shards by rows with no "
