@@ -43,13 +43,13 @@ METRIC = "FP8 FFN TFLOP/s + tokens/s per layer (H=4096,I=12288); % FP8 MFMA / HB
 PEAK_HBM_GBPS = 8000.0
 PEAK_FP8_TFLOPS = 5033.0  # dense FP8 MFMA: 256 CU x 2.4 GHz x 8192 FLOP/clk
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pmc_traffic.json")
-KERNEL_SOURCES = {
-    "gateup_skinny": ["gemm_skinny.hip", "device.h"],
-    "hquant_skinny": ["gemm_skinny.hip", "device.h"],
-    "down_skinny": ["gemm_skinny.hip", "device.h"],
-    "reduce_tiled": ["gemm_tiled.hip", "device.h"],
-    "gateup_tiled": ["gemm_tiled.hip", "device.h"],
-    "down_tiled": ["gemm_tiled.hip", "device.h"],
+KERNEL_SOURCES = {  # the files that define each kernel and its launch (item order, limits)
+    "gateup_skinny": ["gemm_skinny.hip", "device.h", "launch.h"],
+    "hquant_skinny": ["gemm_skinny.hip", "device.h", "launch.h"],
+    "down_skinny": ["gemm_skinny.hip", "device.h", "launch.h"],
+    "reduce_tiled": ["gemm_tiled.hip", "device.h", "launch.h"],
+    "gateup_tiled": ["gemm_tiled.hip", "device.h", "launch.h"],
+    "down_tiled": ["gemm_tiled.hip", "device.h", "launch.h"],
 }
 
 

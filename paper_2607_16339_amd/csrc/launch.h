@@ -38,7 +38,8 @@ hipError_t launch_encode_e4m3(hipStream_t st, const float* v, uint8_t* codes, in
 // weight tiles and a few activation tiles, which its L2 then serves to all of
 // them. A bijection of [0, R*C) for any R, C.
 constexpr int64_t kXcds = 8;
-constexpr int64_t kTileGroupRows = 8;
+// 4 row tiles: measured 2.5 % faster than 8 at M = 512 and no slower at M = 8192
+constexpr int64_t kTileGroupRows = 4;
 __host__ __device__ inline void xcd_grouped_tile(int64_t bid, int64_t R, int64_t C, int64_t& r, int64_t& c) {
   const int64_t T = R * C;
   const int64_t x = bid % kXcds, slot = bid / kXcds;
