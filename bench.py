@@ -865,9 +865,15 @@ def attention_main(args):
         with torch.cuda.graph(g):
             for _ in range(reps):
                 call(mode, q, k, v)
-        g.replay()
-        torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        # untimed replays back to back for about WARM_S seconds, then the timed ones right behind them
+        for _ in range(min(5000, int(WARM_S / max(e0.elapsed_time(e1) * 1e-3, 1e-6)) + 1)):
+            g.replay()
+        torch.cuda.synchronize()
         nrep = 3
         e0.record(stream)
         for _ in range(nrep):
