@@ -8,25 +8,30 @@ Weights rotate over several independently drawn layers, more bytes than the
 256 MB Infinity Cache holds, so every step streams its weights from HBM.
 
 Timing: W warm-up steps, then the K steps are captured once in a HIP graph
-(as a serving loop runs its decode steps; every step is the whole call), the
-graph is replayed untimed for at least half a second (until the clocks have
-settled), and one replay of the graph is the timed region, between HIP events
-and device synchronizations; --eager times the plain host loop instead (its figures are
-reported either way).
+(as a serving loop runs its decode steps; every step is the whole call). The
+graph is replayed untimed for at least half a second; after a device
+synchronization (the barrier) a few more untimed replays are queued and the
+timed replay of exactly K steps follows them between HIP events, then the
+closing synchronization. The replays queued after the barrier keep the GPU
+busy while the host submits the timed one: a replay that starts on a GPU left
+idle by the barrier runs slower while the clocks come back up, which is
+reported as ms_per_step_after_idle. --eager times the plain host loop
+instead (its figures are reported either way).
 
-Prints one JSON line. The default workload is the 32-token decode block
-(M=32); --workload selects another. For the 31-layer stack
-(stack31_m512_h4096_i12288) a step is one denoising step through all 31
+Prints one JSON line. The default workload is the batched long sequence
+(8 x 1024 = 8192 tokens, MFMA-bound), the largest single-GPU configuration;
+the same line nests the 32-token decode block (HBM-bound), measured in the
+same run on its own weights. --workload selects another. For the 31-layer
+stack (stack31_m512_h4096_i12288) a step is one denoising step through all 31
 layers (all resident in HBM), with the residual adds between them (fused into
 the next layer's norm, the last one a plain add); 32 steps by default, one per
 denoising step, each on its own input. Besides the whole-step throughput the
 line carries the dominant kernel's roofline figures (timed live with HIP
-events around graph-captured back-to-back calls of its stage alone; at
-M <= 32 the gate/up stage minus its small h-quantization kernel, which is
-timed alone the same way; at 33..64 rows the whole gate/up stage) and the
-CPU oracle's throughput on a bounded sample of the same workload.
+events around graph-captured back-to-back calls of its stage alone, and
+compared with the same kernel's average in the committed rocprofv3 trace) and
+the CPU oracle's throughput on a bounded sample of the same workload.
 
-  python bench.py [--gpus 1] [--steps 50] [--warmup 10] [--workload block32_h4096_i12288]
+  python bench.py [--gpus 1] [--steps 50] [--warmup 10] [--workload batch8x1024_h4096_i12288]
 """
 
 import argparse
@@ -60,7 +65,7 @@ def parse(argv=None):
     p.add_argument("--steps", type=int, default=None,
                    help="timed steps (default 50; 32 for the stack, one step per denoising step)")
     p.add_argument("--warmup", type=int, default=10)
-    p.add_argument("--workload", default="block32_h4096_i12288",
+    p.add_argument("--workload", default=DEFAULT_WORKLOAD,
                    help="an FFN workload, an attention workload (attn_*: the first-layer FACache attention), or "
                         "first_layer_n512 (the token-wise first layer with EmbedCache / RoPECache)")
     p.add_argument("--weight-sets", type=int, default=4)
@@ -68,6 +73,8 @@ def parse(argv=None):
                    help="time the FFN at the three quantization granularities (per group, per token, per tensor) "
                         "and report each one's error against the unquantized bf16 FFN")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-nested", action="store_true",
+                   help="with the default workload, skip the nested 32-token decode-block measurement")
     p.add_argument("--eager", action="store_true",
                    help="time the eager host loop instead of the HIP-graph replay of the K steps")
     p.add_argument("--profile-only", action="store_true",
@@ -120,6 +127,10 @@ def stage_bytes(M, H, I):
 
 COPY_BYTES = 256 << 20
 WARM_S = 0.5  # seconds of untimed graph replays before the timed one
+DEFAULT_WORKLOAD = "batch8x1024_h4096_i12288"  # MFMA-bound: 8 sequences x 1024 tokens
+NESTED_WORKLOAD = "block32_h4096_i12288"  # HBM-bound: one 32-token decode block
+# the skinny gate/up stage ends with a separate h-quantization kernel
+SKINNY_HQUANT_KERNEL = True
 
 
 def kernel_key(name):
@@ -217,14 +228,137 @@ def main():
         first_layer_main(args)
         return
     w = synth.WORKLOADS[args.workload]
-    M, H, I = w.M, w.H, w.I
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     lc.lib()  # fails loudly when the HIP library is missing
+    line = ffn_line(args, w, dev)
+    if args.workload == DEFAULT_WORKLOAD and not args.no_nested:
+        # the HBM-bound decode block, measured in the same run (its own weights)
+        w2 = synth.WORKLOADS[NESTED_WORKLOAD]
+        nested = ffn_line(args, w2, dev, nested=True)
+        keep = ("value", "unit", "ms_per_step", "tokens_per_s", "hbm_GBps_min_bytes", "frac_hbm_peak",
+                "frac_fp8_peak", "ms_per_step_after_idle", "ms_per_step_graph_replays", "stage_ms", "roofline",
+                "vs_bf16_ffn", "cpu_baseline", "config", "steps")
+        line["nested"] = {NESTED_WORKLOAD: {k: nested[k] for k in keep if k in nested}}
+    print(json.dumps(line), flush=True)
+
+
+def dev_bf16_fn(dev):
+    import numpy as np
+    import torch
 
     def dev_bf16(bits):
         return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16).copy()).view(torch.bfloat16).to(dev)
+    return dev_bf16
 
+
+def ffn_weight_sets(w, n, dev):
+    """n independently drawn layers of the workload's weights, quantized on
+    the GPU (bf16 copies freed), each with its own input x; the seeded bf16
+    draws run on host threads (the generator releases the GIL)."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    import numpy as np
+
+    import paper_2607_16339_amd as lc
+    import synth
+    dev_bf16 = dev_bf16_fn(dev)
+    with ThreadPoolExecutor(max_workers=min(4, n)) as ex:
+        futs = [ex.submit(lambda layer: (synth.make_weights(w, layer), synth.make_x(w, layer=layer, step=layer - 1)),
+                          layer) for layer in range(1, n + 1)]
+        sets = []
+        for f in futs:
+            b, xb = f.result()
+            wgu = dev_bf16(np.concatenate([b["w_gate"], b["w_up"]], axis=0))
+            wgu_q, wgu_s = lc.quantize_weights(wgu)
+            del wgu
+            wd = dev_bf16(b["w_down"])
+            wd_q, wd_s = lc.quantize_weights(wd)
+            del wd
+            sets.append(dict(norm_w=dev_bf16(b["norm_w"]), wgu_q=wgu_q, wgu_s=wgu_s, wd_q=wd_q, wd_s=wd_s,
+                             x=dev_bf16(xb)))
+            del b
+    return sets
+
+
+def time_graph(g, K, stream, warm_s=WARM_S, min_warm=3):
+    """Times one replay of a captured graph of K steps. Untimed replays run
+    back to back for at least warm_s seconds first; after the barrier
+    (device synchronization) a few more untimed replays are queued, then the
+    timed replay between HIP events, then the closing synchronization. The
+    replays queued after the barrier keep the GPU busy while the host submits
+    the timed replay: a timed replay that starts on an idle GPU (measured too,
+    as ms_after_idle) runs slower while the clocks come back up. Returns a
+    dict of per-step milliseconds."""
+    import torch
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    est_s = max(e0.elapsed_time(e1) * 1e-3, 1e-6)
+    n_warm = max(min_warm, min(5000, int(warm_s / est_s) + 1))
+    for _ in range(n_warm):
+        g.replay()
+    torch.cuda.synchronize()
+    # diagnostic: a replay that starts right after the barrier, on an idle GPU
+    e0.record(stream)
+    g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    after_idle = e0.elapsed_time(e1) / K
+    # the timed replay: barrier, untimed replays covering >= 5 ms of GPU time,
+    # then exactly one timed replay of the K steps
+    torch.cuda.synchronize()
+    n_pre = max(2, int(5e-3 / est_s) + 1)
+    t_wall = time.perf_counter()
+    for _ in range(n_pre):
+        g.replay()
+    e0.record(stream)
+    t_sub = time.perf_counter()
+    g.replay()  # the timed region: exactly K steps
+    t_sub = time.perf_counter() - t_sub
+    e1.record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    timed = e0.elapsed_time(e1) / K
+    more = []
+    for _ in range(5):
+        e0.record(stream)
+        g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        more.append(e0.elapsed_time(e1) / K)
+    return {"timed": timed, "after_idle": after_idle, "more": more, "submit_ms": t_sub * 1e3,
+            "n_pre": n_pre, "wall_s": t_wall}
+
+
+def trace_kernel_us(workload, name_prefix):
+    """Average duration (us) of a kernel in the committed rocprofv3 kernel
+    trace summary of the workload (profiles/kernel_trace_ffn_<workload>.txt),
+    or None."""
+    path = os.path.join(ROOT, "profiles", "kernel_trace_ffn_%s.txt" % workload)
+    try:
+        with open(path) as f:
+            for ln in f:
+                if ln.startswith(name_prefix):
+                    cols = ln[74:].split()
+                    return float(cols[1])
+    except (OSError, ValueError, IndexError):
+        return None
+    return None
+
+
+def ffn_line(args, w, dev, nested=False):
+    """The bench line of one FFN workload (see the module docstring)."""
+    import numpy as np
+    import torch
+
+    import paper_2607_16339_amd as lc
+    import synth
+
+    M, H, I = w.M, w.H, w.I
+    dev_bf16 = dev_bf16_fn(dev)
     L = w.layers
     if w.act == "stack":
         # ---- the stack: one step is one denoising step through all L layers.
@@ -251,94 +385,58 @@ def main():
         # the stage timings below use the first layers on the first steps' inputs
         sets = [dict(layers[i], x=xin[i]) for i in range(min(args.weight_sets, L))]
     else:
-        # ---- weights: several layers, quantized on the GPU; bf16 copies freed
-        sets = []
-        for layer in range(1, args.weight_sets + 1):
-            b = synth.make_weights(w, layer)
-            wgu = dev_bf16(np.concatenate([b["w_gate"], b["w_up"]], axis=0))
-            wgu_q, wgu_s = lc.quantize_weights(wgu)
-            del wgu
-            wd = dev_bf16(b["w_down"])
-            wd_q, wd_s = lc.quantize_weights(wd)
-            del wd
-            x = dev_bf16(synth.make_x(w, layer=layer, step=layer - 1))
-            sets.append(dict(norm_w=dev_bf16(b["norm_w"]), wgu_q=wgu_q, wgu_s=wgu_s, wd_q=wd_q, wd_s=wd_s, x=x))
+        sets = ffn_weight_sets(w, args.weight_sets, dev)
         out = torch.empty((M, H), dtype=torch.bfloat16, device=dev)
-        S = len(sets)
 
         def step(i):
-            s = sets[i % S]
+            s = sets[i % len(sets)]
             lc.lacache_ffn_fp8(s["x"], s["norm_w"], s["wgu_q"], s["wgu_s"], s["wd_q"], s["wd_s"], out)
 
         probe = out
     torch.cuda.synchronize()
     S = len(sets)
+    K = args.steps if not (nested and w.act == "stack") else args.steps
 
     stream = torch.cuda.current_stream()
     # eager: one host call per step, per-step events
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
     ev[0].record(stream)
-    for i in range(args.steps):
+    for i in range(K):
         step(i)
         ev[i + 1].record(stream)
     torch.cuda.synchronize()
-    ms_eager = ev[0].elapsed_time(ev[-1]) / args.steps
-    per_step = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)])
+    ms_eager = ev[0].elapsed_time(ev[-1]) / K
+    per_step = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(K)])
     pct = {"p10": float(np.percentile(per_step, 10)), "p50": float(np.percentile(per_step, 50)),
            "p90": float(np.percentile(per_step, 90))}
 
     # graph: the K steps captured once in a HIP graph (as a serving loop runs
     # its decode steps), every step the whole call on its own weight set
-    ms_graph = None
-    replays = []
+    tg = None
     if not args.eager:
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
-            for i in range(args.steps):
+            for i in range(K):
                 step(i)
         # the replay must reproduce the eager result of the same step
         g.replay()
         torch.cuda.synchronize()
         got = probe.clone()
-        step(args.steps - 1)
+        step(K - 1)
         torch.cuda.synchronize()
         if not torch.equal(got, probe):
             raise RuntimeError("graph replay of the FFN step differs from the eager call")
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        g.replay()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        est_s = max(e0.elapsed_time(e1) * 1e-3, 1e-6)
-        # untimed replays queued back to back for at least WARM_S seconds (and
-        # at least max(3, W / K) of them), then the timed replay right behind
-        # them: the first replays after other work run slower (an M = 512
-        # graph about 10 %) until the clocks have settled
-        n_warm = max(max(3, args.warmup // args.steps), min(5000, int(WARM_S / est_s) + 1))
-        for _ in range(n_warm):
-            g.replay()
-        torch.cuda.synchronize()
-        t_wall = time.perf_counter()
-        e0.record(stream)
-        g.replay()  # the timed region: exactly K steps
-        e1.record(stream)
-        torch.cuda.synchronize()
-        t_wall = time.perf_counter() - t_wall
-        ms_graph = e0.elapsed_time(e1) / args.steps
-        for _ in range(5):
-            e0.record(stream)
-            g.replay()
-            e1.record(stream)
-            torch.cuda.synchronize()
-            replays.append(e0.elapsed_time(e1) / args.steps)
+        tg = time_graph(g, K, stream)
         del g
+        ms = tg["timed"]
+        t_wall = tg["wall_s"]
     else:
+        ms = ms_eager
         t_wall = float(per_step.sum()) * 1e-3
-    ms = ms_graph if ms_graph is not None else ms_eager
-    if args.calibrate_copy:
+    if args.calibrate_copy and not nested:
         src = torch.empty(COPY_BYTES, dtype=torch.uint8, device=dev).fill_(1)
         dst = torch.empty_like(src)
         for _ in range(3):
@@ -352,11 +450,52 @@ def main():
     bytes_min = (3 * H * I + 4 * (3 * I // 128) * (H // 128) + 2 * H + 4 * M * H) * L
     gbps = bytes_min / (ms * 1e-3) / 1e9
 
-    # ---- each stage timed alone: the stage entry points launch the same
-    # kernels as the fused call. R back-to-back calls (rotating over the
-    # weight sets) are captured in a HIP graph, so that the host's per-call
-    # cost does not leave the GPU idle between them; the graph is replayed
-    # between HIP events on the stream it runs on.
+    k_ms, roof = stage_timings(args, w, sets, out, dev)
+    roof["step_frac"] = round(tflops / PEAK_FP8_TFLOPS if roof["bound"] == "mfma" else gbps / PEAK_HBM_GBPS, 4)
+
+    line = {
+        "metric": METRIC, "value": round(tflops, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "fp8_e4m3 (fp32 accumulate)", "data": "synthetic",
+        "config": {"workload": w.name, "M": M, "H": H, "I": I, "group": 128,
+                   "weight_sets": L if w.act == "stack" else S, "path": "skinny" if M <= 64 else "tiled",
+                   "layers": L},
+        "tokens_per_s": round(tok_s, 1), "hbm_GBps_min_bytes": round(gbps, 1),
+        "frac_hbm_peak": round(gbps / PEAK_HBM_GBPS, 4), "frac_fp8_peak": round(tflops / PEAK_FP8_TFLOPS, 4),
+        "step_timing": "HIP graph replay of the K steps" if tg is not None else "eager host loop",
+        "ms_per_step_eager": round(ms_eager, 5),
+        "ms_per_step_eager_pct": {k: round(v, 5) for k, v in pct.items()},
+        "stage_ms": {k: round(v, 5) for k, v in k_ms.items()}, "stage_timing": "HIP graph of back-to-back stage calls",
+        "wall_s_timed": round(t_wall, 4),
+        "roofline": roof,
+    }
+    if tg is not None:
+        line["ms_per_step_graph_replays"] = [round(v, 5) for v in tg["more"]]
+        line["ms_per_step_after_idle"] = round(tg["after_idle"], 5)
+        line["replay_submit_ms"] = round(tg["submit_ms"], 4)
+        line["replays_queued_before_timed"] = tg["n_pre"]
+    if not args.profile_only:
+        line["vs_bf16_ffn"] = error_vs_bf16(w, sets[0], out, dev)
+    if not args.no_cpu_baseline and not args.profile_only:
+        line["cpu_baseline"] = cpu_baseline(w, sets, out, dev)
+    del sets
+    torch.cuda.synchronize()
+    return line
+
+
+def stage_timings(args, w, sets, out, dev):
+    """Each stage timed alone: the stage entry points launch the same kernels
+    as the fused call. R back-to-back calls (rotating over the weight sets)
+    are captured in a HIP graph, so that the host's per-call cost does not
+    leave the GPU idle between them; the graph is replayed between HIP events
+    on the stream it runs on. Returns (stage ms, roofline of the dominant
+    kernel)."""
+    import torch
+
+    import paper_2607_16339_amd as lc
+
+    M, H, I = w.M, w.H, w.I
+    S = len(sets)
     skinny = M <= 64
     xq = torch.empty((M, H), dtype=torch.uint8, device=dev)
     xs = torch.empty((H // 128, M), dtype=torch.float32, device=dev)
@@ -372,7 +511,7 @@ def main():
     # at M <= 32 the skinny gate/up stage ends with the h-quantization kernel
     # that lacache_quant_rows_g launches alone (33..64 rows: a variant that
     # also adds the two K halves)
-    split_stage = skinny and M <= 32
+    split_stage = skinny and M <= 32 and SKINNY_HQUANT_KERNEL
     if split_stage:
         # the h-quantization kernel of the skinny gate/up stage, timed alone:
         # the same kernel on the same sizes (lacache_quant_rows_g at group
@@ -405,14 +544,8 @@ def main():
         torch.cuda.synchronize()
         if not torch.equal(got, probe):
             raise RuntimeError("graph replay of the %s stage differs from the eager call" % name)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        nrep = 3
-        e0.record(torch.cuda.current_stream())
-        for _ in range(nrep):
-            g.replay()
-        e1.record(torch.cuda.current_stream())
-        torch.cuda.synchronize()
-        k_ms[name] = e0.elapsed_time(e1) / (nrep * reps)
+        t = time_graph(g, reps, torch.cuda.current_stream(), warm_s=0.1, min_warm=2)
+        k_ms[name] = t["timed"]
         del g
     dom = "gateup"
     if split_stage:
@@ -433,14 +566,18 @@ def main():
         roof["stage"] = {"kernels": "gateup_skinny + hquant_skinny", "ms": round(k_ms[dom], 5),
                          "algorithmic_bytes": sb[dom], "achieved": round(st_ach, 1),
                          "frac": round(st_ach / PEAK_HBM_GBPS, 4)}
+        trace_prefix = "void lacache::(anonymous namespace)::skinny_gateup_kernel"
+        per_byte = sb["gateup_stream"]
     elif skinny:
-        kparts = ["gateup_skinny", "hquant_skinny"]
+        kparts = ["gateup_skinny"] + (["hquant_skinny"] if SKINNY_HQUANT_KERNEL else [])
         achieved = sb[dom] / (k_ms[dom] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM_GBPS, 4)}
-        roof["kernel"] = "gateup_skinny + hquant_skinny (the stage)"
+        roof["kernel"] = "gateup_skinny" + (" + hquant_skinny (the stage)" if SKINNY_HQUANT_KERNEL else "")
         roof["kernel_ms"] = round(k_ms[dom], 5)
         roof["algorithmic_bytes"] = sb[dom]
+        trace_prefix = "void lacache::(anonymous namespace)::skinny_gateup_kernel"
+        per_byte = sb[dom]
     else:
         kparts = ["gateup_tiled"]
         achieved = 4.0 * M * H * I / (k_ms[dom] * 1e-3) / 1e12
@@ -449,38 +586,26 @@ def main():
         roof["kernel"] = "gateup_tiled"
         roof["kernel_ms"] = round(k_ms[dom], 5)
         roof["algorithmic_flop"] = 4 * M * H * I
+        trace_prefix = "void lacache::gemm_tiled_kernel<true"
+        per_byte = None
+    roof["kernel_ms_timing"] = "HIP events around a graph of back-to-back calls of the stage alone"
+    # the same kernel's average duration in the committed rocprofv3 trace
+    us = trace_kernel_us(w.name, trace_prefix)
+    if us is not None:
+        tr = (per_byte / (us * 1e-6) / 1e9 / PEAK_HBM_GBPS) if per_byte else (
+            4.0 * M * H * I / (us * 1e-6) / 1e12 / PEAK_FP8_TFLOPS)
+        roof["trace"] = {"file": "profiles/kernel_trace_ffn_%s.txt" % w.name, "avg_us": us,
+                         "frac": round(tr, 4), "live_vs_trace": round(roof["kernel_ms"] * 1e3 / us - 1, 4)}
     roof["traffic"] = None
     try:
         with open(TRAFFIC_FILE) as f:
             table = json.load(f)
-        parts = [table.get(k + ":" + args.workload) for k in kparts]
+        parts = [table.get(k + ":" + w.name) for k in kparts]
         if all(t and t.get("source_sha") == source_sha(k) for t, k in zip(parts, kparts)):
             roof["traffic"] = sum(t["hbm_bytes_per_launch"] for t in parts)
     except (OSError, ValueError):
         pass
-
-    line = {
-        "metric": METRIC, "value": round(tflops, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "fp8_e4m3 (fp32 accumulate)", "data": "synthetic",
-        "config": {"workload": args.workload, "M": M, "H": H, "I": I, "group": 128,
-                   "weight_sets": L if w.act == "stack" else S, "path": "skinny" if skinny else "tiled",
-                   "layers": L},
-        "tokens_per_s": round(tok_s, 1), "hbm_GBps_min_bytes": round(gbps, 1),
-        "frac_hbm_peak": round(gbps / PEAK_HBM_GBPS, 4), "frac_fp8_peak": round(tflops / PEAK_FP8_TFLOPS, 4),
-        "step_timing": "HIP graph replay of the K steps" if ms_graph is not None else "eager host loop",
-        "ms_per_step_eager": round(ms_eager, 5),
-        "ms_per_step_eager_pct": {k: round(v, 5) for k, v in pct.items()},
-        "ms_per_step_graph_replays": [round(v, 5) for v in replays],
-        "stage_ms": {k: round(v, 5) for k, v in k_ms.items()}, "stage_timing": "HIP graph of back-to-back stage calls",
-        "wall_s_timed": round(t_wall, 4),
-        "roofline": roof,
-    }
-    if not args.profile_only:
-        line["vs_bf16_ffn"] = error_vs_bf16(w, sets[0], out, dev)
-    if not args.no_cpu_baseline and not args.profile_only:
-        line["cpu_baseline"] = cpu_baseline(w, sets, out, dev)
-    print(json.dumps(line), flush=True)
+    return k_ms, roof
 
 
 def stack_weights(w, dev_bf16):
@@ -532,23 +657,24 @@ def error_vs_bf16(w, s, out, dev, rows=8):
 
 
 def cpu_baseline(w, sets, out, dev):
-    """The oracle, as it stands, on a bounded sample of the same workload."""
+    """The oracle, as it stands (NumPy fp64, BLAS-threaded matmuls), on a
+    bounded sample of the same workload: whole-layer calls on up to 512 of
+    its rows (the FFN is row-independent), repeated over the weight sets until
+    about 10 s of CPU work. Larger workloads are extrapolated from the sample
+    and labelled so: M / 512 times the per-call time for the batched
+    workload, and L layers x steps for the stack."""
     import numpy as np
+    import torch
+
     import oracle.ffn as O
     import paper_2607_16339_amd as lc
     import synth
 
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:  # noqa: BLE001
-        threads = os.cpu_count() or 1
-    import torch
-    rows = min(w.M, 32)
-    # repeat whole-layer oracle calls over the weight sets until ~10 s of CPU work
+    blas = _threads()
+    rows = min(w.M, 512)
     t = 0.0
     calls = 0
-    while t < 10.0 and calls < 64:
+    while calls < 1 or (t < 10.0 and calls < 64):
         s = sets[calls % len(sets)]
         xb = synth.make_x(w, layer=calls % len(sets) + 1, step=calls % len(sets))[:rows]
         host = [lc.weight_codes_rowmajor(s["wgu_q"]), s["wgu_s"].cpu().numpy(), lc.weight_codes_rowmajor(s["wd_q"]),
@@ -558,11 +684,25 @@ def cpu_baseline(w, sets, out, dev):
         O.ffn(xb, norm_w, host[0], host[1], host[2], host[3], w.I)
         t += time.perf_counter() - t0
         calls += 1
+    per_call = t / calls
     flop = 6.0 * rows * w.H * w.I * calls
-    return {"value": round(flop / t / 1e12, 6), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
-            "sample": "%d calls of %d of %d rows (one layer each; the FFN is row-independent): %.2f s"
-                      % (calls, rows, w.M, t),
-            "tokens_per_s": round(rows * calls / t, 3)}
+    r = {"value": round(flop / t / 1e12, 6), "unit": "TFLOP/s", "cores": blas, "kind": "oracle",
+         "os_cpu_count": os.cpu_count(), "blas_threads": blas,
+         "sample": "%d whole-layer oracle calls on %d of the %d rows (one layer each; the FFN is row-independent): "
+                   "%.2f s" % (calls, rows, w.M, t),
+         "tokens_per_s_per_layer": round(rows * calls / t, 3), "s_per_sample_call": round(per_call, 4)}
+    if rows < w.M or w.layers > 1:
+        factor = (w.M / rows) * w.layers
+        r["extrapolated"] = {
+            "label": "EXTRAPOLATED, not measured: the sample's per-call time x %g" % factor,
+            "factor": factor,
+            "what": ("one call on all %d rows = %d sample calls of %d rows" % (w.M, w.M // rows, rows))
+            if w.layers == 1 else ("one denoising step = %d layers; the whole run of %d steps = x%d"
+                                   % (w.layers, w.steps, w.layers * w.steps)),
+            "s_per_step": round(per_call * factor, 3)}
+        if w.layers > 1:
+            r["extrapolated"]["s_whole_run"] = round(per_call * w.layers * w.steps, 2)
+    return r
 
 
 def granularity_main(args):

@@ -34,8 +34,19 @@
  *   non-NULL (except the optional *_tap outputs) and 16-byte aligned.
  *   Outputs must not overlap inputs.
  * - The caller owns every buffer it passes. The library owns only its
- *   workspace: the intermediates of lacache_ffn_fp8 and the fp32 h of the
- *   skinny (M <= 64) gate/up stage call (see lacache_ffn_fp8).
+ *   workspace: the intermediates of lacache_ffn_fp8 and the fp32 scratch of
+ *   the GEMM stage calls (see lacache_ffn_fp8). The workspace is one buffer
+ *   per device, allocated on first use and grown (by at least half) when a
+ *   larger call needs it. A superseded buffer is not freed until
+ *   lacache_release_workspace(), so work queued on any stream, and HIP graphs
+ *   captured earlier, keep valid memory; growth never synchronizes.
+ * - Stream capture (HIP graphs): a call whose stream is being captured must
+ *   not need a larger library workspace than earlier calls have made the
+ *   library allocate; it then returns LACACHE_ERR_CAPTURE and enqueues
+ *   nothing (the capture stays valid). Call the largest shape once outside
+ *   capture first, or use lacache_ffn_fp8_ws with a caller-owned workspace.
+ *   Graphs that hold library-workspace calls become invalid at
+ *   lacache_release_workspace().
  * - Results are deterministic: the same inputs give the same output bytes
  *   (no floating-point atomics).
  * - A failed HIP launch or allocation returns LACACHE_ERR_HIP or
@@ -56,7 +67,9 @@ typedef enum {
   LACACHE_ERR_INVALID_ARG = -1, /* null/misaligned pointer, bad shape, overlap */
   LACACHE_ERR_UNSUPPORTED = -2, /* group != 128, or a size above the limits */
   LACACHE_ERR_HIP = -3,         /* a HIP runtime call or kernel launch failed */
-  LACACHE_ERR_ALLOC = -4        /* the library could not allocate its workspace */
+  LACACHE_ERR_ALLOC = -4,       /* the library could not allocate its workspace */
+  LACACHE_ERR_CAPTURE = -5      /* the library workspace would have to grow while the
+                                   stream is being captured (see the conventions) */
 } lacache_status;
 
 /*
@@ -80,6 +93,20 @@ typedef enum {
  */
 int lacache_quant_weights(void* stream, const uint16_t* w, uint8_t* w_q, float* w_s,
                           int64_t N, int64_t K, int group);
+
+/*
+ * Repack of e4m3 weight codes from row-major order into the weight tile
+ * layout above, for weights quantized by another producer (the codes of
+ * Eqs. 7-8 in the row-major [N x K] order of Sec. 3.4's statement; the block
+ * scales [N/128 x K/128] need no repack).
+ *   w_q_rowmajor [N x K] e4m3, row-major   (input)
+ *   w_q          N*K e4m3, tile layout     (output), must not overlap the input
+ * N and K must be positive multiples of 128 (N, K <= 131072). Every weight
+ * code argument of the FFN calls below must be in the tile layout: row-major
+ * codes passed there directly are the same size, so the library cannot tell
+ * them apart, and give wrong results.
+ */
+int lacache_pack_weights(void* stream, const uint8_t* w_q_rowmajor, uint8_t* w_q, int64_t N, int64_t K);
 
 /*
  * Fused RMSNorm + 1x128 activation quantization (Sec. 3.4: quantization fused
@@ -179,7 +206,10 @@ int lacache_ffn_fp8_ws(void* stream, const uint16_t* x, const uint16_t* norm_w, 
                        const float* wgu_s, const uint8_t* wd_q, const float* wd_s, uint16_t* out,
                        int64_t M, int64_t H, int64_t I, int group, void* workspace, size_t ws_bytes);
 
-/* Residual add between stacked layers: x[i] = RNE_bf16(float(x[i]) + float(y[i])), i < n. */
+/* Residual add between stacked layers (the "Add" of the AddNorm that Sec. 3.4
+ * fuses with the quantization; also available fused, see
+ * lacache_add_rmsnorm_quant): x[i] = RNE_bf16(float(x[i]) + float(y[i])), i < n.
+ * x and y must not overlap. */
 int lacache_add_bf16(void* stream, uint16_t* x_inout, const uint16_t* y, int64_t n);
 
 /* Test hook: the device e4m3 encoder applied elementwise, codes[i] = E(v[i]),
@@ -377,7 +407,9 @@ int lacache_set_path_policy(int policy);
 /* Human-readable name of a status code (static string). */
 const char* lacache_status_string(int status);
 
-/* Frees the library-owned workspace of every device (synchronizes each). */
+/* Frees the library-owned workspace of every device, superseded buffers
+ * included (synchronizes each device first). HIP graphs captured with calls
+ * that used the library workspace must not be replayed afterwards. */
 void lacache_release_workspace(void);
 
 #ifdef __cplusplus

@@ -9,9 +9,9 @@ non-OK status. Every step of the FFN runs in the library's HIP kernels.
 import numpy as np
 import torch
 
-from ._lib import (LACACHE_ERR_ALLOC, LACACHE_ERR_HIP, LACACHE_ERR_INVALID_ARG, LACACHE_ERR_UNSUPPORTED,  # noqa: F401
-                   LACACHE_GRAN_GROUP, LACACHE_GRAN_TENSOR, LACACHE_GRAN_TOKEN, LACACHE_OK, LacacheError, check, lib,
-                   status_string)
+from ._lib import (LACACHE_ERR_ALLOC, LACACHE_ERR_CAPTURE, LACACHE_ERR_HIP, LACACHE_ERR_INVALID_ARG,  # noqa: F401
+                   LACACHE_ERR_UNSUPPORTED, LACACHE_GRAN_GROUP, LACACHE_GRAN_TENSOR, LACACHE_GRAN_TOKEN, LACACHE_OK,
+                   LacacheError, check, lib, status_string)
 
 GROUP = 128
 _U8 = (torch.uint8, torch.float8_e4m3fn)
@@ -47,6 +47,13 @@ def lacache_quant_weights(w, w_q, w_s, group=GROUP, stream=None):
     check(lib().lacache_quant_weights(
         _stream(stream, w), _ptr(w, _BF16, "w"), _ptr(w_q, _U8, "w_q", (N, K)),
         _ptr(w_s, (torch.float32,), "w_s", (N // group, K // group)), N, K, group), "lacache_quant_weights")
+
+
+def lacache_pack_weights(w_q_rowmajor, w_q, stream=None):
+    """Row-major e4m3 codes [N, K] -> w_q [N, K] in the library's weight tile layout (on the device)."""
+    N, K = w_q_rowmajor.shape
+    check(lib().lacache_pack_weights(_stream(stream, w_q_rowmajor), _ptr(w_q_rowmajor, _U8, "w_q_rowmajor"),
+                                     _ptr(w_q, _U8, "w_q", (N, K)), N, K), "lacache_pack_weights")
 
 
 def lacache_rmsnorm_quant(x, norm_w, xq, xs, group=GROUP, stream=None):
@@ -325,6 +332,13 @@ def weight_codes_tiled(codes):
     a = np.asarray(codes, dtype=np.uint8)
     N, K = a.shape
     return np.ascontiguousarray(a.reshape(N // 16, 16, K // 128, 2, 64).transpose(0, 2, 3, 1, 4).reshape(N, K))
+
+
+def pack_weights(w_q_rowmajor, stream=None):
+    """Returns the tile-layout copy of row-major e4m3 weight codes [N, K] (a new device tensor)."""
+    w_q = torch.empty(tuple(w_q_rowmajor.shape), dtype=torch.uint8, device=w_q_rowmajor.device)
+    lacache_pack_weights(w_q_rowmajor, w_q, stream)
+    return w_q
 
 
 def quantize_weights(w, group=GROUP, stream=None):

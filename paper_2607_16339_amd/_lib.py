@@ -16,12 +16,14 @@ LACACHE_ERR_INVALID_ARG = -1
 LACACHE_ERR_UNSUPPORTED = -2
 LACACHE_ERR_HIP = -3
 LACACHE_ERR_ALLOC = -4
+LACACHE_ERR_CAPTURE = -5
 LACACHE_GRAN_GROUP, LACACHE_GRAN_TOKEN, LACACHE_GRAN_TENSOR = 0, 1, 2
 
 # name -> (restype, argtypes)
 _P, _I64, _I = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
 SIGNATURES = {
     "lacache_quant_weights": (_I, [_P, _P, _P, _P, _I64, _I64, _I]),
+    "lacache_pack_weights": (_I, [_P, _P, _P, _I64, _I64]),
     "lacache_rmsnorm_quant": (_I, [_P, _P, _P, _P, _P, _I64, _I64, _I]),
     "lacache_add_rmsnorm_quant": (_I, [_P, _P, _P, _P, _P, _P, _I64, _I64, _I]),
     "lacache_ffn_fp8_addnorm": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I]),

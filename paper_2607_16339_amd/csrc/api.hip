@@ -109,36 +109,52 @@ size_t scratch_bytes(int64_t M, int64_t H, int64_t I) {
 }
 
 // ---------------------------------------------------------------------------
-// Library-owned workspace: one grow-only device buffer per device.
+// Library-owned workspace: one grow-only device buffer per device. A buffer
+// that a larger call supersedes is kept (not freed) until
+// lacache_release_workspace: calls queued on any stream, and HIP graphs
+// captured earlier, may still use it. Growth needs hipMalloc, which a stream
+// under capture must not see, so a call that would grow the workspace while
+// its stream is being captured returns LACACHE_ERR_CAPTURE instead.
 // ---------------------------------------------------------------------------
 struct DeviceWs {
   void* ptr = nullptr;
   size_t bytes = 0;
+  std::vector<void*> retired;
 };
 std::mutex g_ws_mu;
 std::vector<DeviceWs> g_ws;
 
 // Returns a workspace of at least `bytes` on the current device.
-int get_workspace(size_t bytes, void** out) {
+int get_workspace(hipStream_t st, size_t bytes, void** out) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return LACACHE_ERR_HIP;
   std::lock_guard<std::mutex> lk(g_ws_mu);
   if (static_cast<size_t>(dev) >= g_ws.size()) g_ws.resize(dev + 1);
   DeviceWs& w = g_ws[dev];
   if (w.bytes < bytes) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(st, &cs) != hipSuccess) return LACACHE_ERR_HIP;
+    if (cs != hipStreamCaptureStatusNone) return LACACHE_ERR_CAPTURE;
     const char* force_fail = std::getenv("LACACHE_TEST_FAIL_ALLOC");
     if (force_fail != nullptr && force_fail[0] == '1') return LACACHE_ERR_ALLOC;
-    if (w.ptr != nullptr) {
-      // earlier calls on any stream may still use the old buffer
-      if (hipDeviceSynchronize() != hipSuccess) return LACACHE_ERR_HIP;
-      if (hipFree(w.ptr) != hipSuccess) return LACACHE_ERR_HIP;
-      w.ptr = nullptr;
-      w.bytes = 0;
-    }
+    // grow by at least half, so that a run of slowly growing calls keeps at
+    // most about twice the largest size alive
+    const size_t want = w.ptr == nullptr ? bytes : (bytes > w.bytes + w.bytes / 2 ? bytes : w.bytes + w.bytes / 2);
     void* p = nullptr;
-    if (hipMalloc(&p, bytes) != hipSuccess) return LACACHE_ERR_ALLOC;
-    w.ptr = p;
-    w.bytes = bytes;
+    if (hipMalloc(&p, want) != hipSuccess) {
+      (void)hipGetLastError();
+      if (want == bytes || hipMalloc(&p, bytes) != hipSuccess) {
+        (void)hipGetLastError();
+        return LACACHE_ERR_ALLOC;
+      }
+      if (w.ptr != nullptr) w.retired.push_back(w.ptr);
+      w.ptr = p;
+      w.bytes = bytes;
+    } else {
+      if (w.ptr != nullptr) w.retired.push_back(w.ptr);
+      w.ptr = p;
+      w.bytes = want;
+    }
   }
   *out = w.ptr;
   return LACACHE_OK;
@@ -228,6 +244,14 @@ int lacache_quant_weights(void* stream, const uint16_t* w, uint8_t* w_q, float* 
   return hip_status(launch_quant_weights(static_cast<hipStream_t>(stream), w, w_q, w_s, N, K));
 }
 
+int lacache_pack_weights(void* stream, const uint8_t* w_q_rowmajor, uint8_t* w_q, int64_t N, int64_t K) {
+  RETURN_IF(check_dim(N, kMaxN));
+  RETURN_IF(check_dim(K, kMaxN));
+  if (!ptrs_ok({w_q_rowmajor, w_q})) return LACACHE_ERR_INVALID_ARG;
+  if (overlap(rng(w_q, N * K), rng(w_q_rowmajor, N * K))) return LACACHE_ERR_INVALID_ARG;
+  return hip_status(launch_pack_weights(static_cast<hipStream_t>(stream), w_q_rowmajor, w_q, N, K));
+}
+
 int lacache_rmsnorm_quant(void* stream, const uint16_t* x, const uint16_t* norm_w, uint8_t* xq, float* xs,
                           int64_t M, int64_t H, int group) {
   RETURN_IF(check_group(group));
@@ -274,7 +298,7 @@ int lacache_gateup_swiglu_quant(void* stream, const uint8_t* xq, const float* xs
     return LACACHE_ERR_INVALID_ARG;
   hipStream_t st = static_cast<hipStream_t>(stream);
   void* skinny = nullptr;
-  if (path == Path::kSkinny) RETURN_IF(get_workspace(skinny_gateup_ws_bytes(M, I), &skinny));
+  if (path == Path::kSkinny) RETURN_IF(get_workspace(st, skinny_gateup_ws_bytes(M, I), &skinny));
   return run_gateup(st, path, xq, xs, wgu_q, wgu_s, hq, hs, h_tap, M, H, I, skinny);
 }
 
@@ -293,7 +317,7 @@ int lacache_down_proj(void* stream, const uint8_t* hq, const float* hs, const ui
     return LACACHE_ERR_INVALID_ARG;
   void* scratch = nullptr;
   if (path == Path::kTiled && tiled_down_ws_bytes(M, H, I) > 0)
-    RETURN_IF(get_workspace(tiled_down_ws_bytes(M, H, I), &scratch));
+    RETURN_IF(get_workspace(static_cast<hipStream_t>(stream), tiled_down_ws_bytes(M, H, I), &scratch));
   return run_down(static_cast<hipStream_t>(stream), path, hq, hs, wd_q, wd_s, out, out_tap, M, H, I, scratch);
 }
 
@@ -313,7 +337,7 @@ int lacache_ffn_fp8(void* stream, const uint16_t* x, const uint16_t* norm_w, con
   if (M == 0) return LACACHE_OK;
   hipStream_t st = static_cast<hipStream_t>(stream);
   void* base = nullptr;
-  RETURN_IF(get_workspace(ffn_layout(nullptr, M, H, I).total, &base));
+  RETURN_IF(get_workspace(st, ffn_layout(nullptr, M, H, I).total, &base));
   return ffn_core(st, x, nullptr, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, M, H, I, path, ffn_layout(base, M, H, I));
 }
 
@@ -332,7 +356,7 @@ int lacache_ffn_fp8_addnorm(void* stream, uint16_t* resid, const uint16_t* y, co
   RETURN_IF(choose_path(M, H, I, &path));
   hipStream_t st = static_cast<hipStream_t>(stream);
   void* base = nullptr;
-  RETURN_IF(get_workspace(ffn_layout(nullptr, M, H, I).total, &base));
+  RETURN_IF(get_workspace(st, ffn_layout(nullptr, M, H, I).total, &base));
   return ffn_core(st, resid, y, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, M, H, I, path, ffn_layout(base, M, H, I));
 }
 
@@ -429,7 +453,8 @@ int lacache_down_proj_g(void* stream, const uint8_t* hq, const float* hs, const 
                  rng(wd_row_s, wd_row_s ? H * 4 : 0)}))
     return LACACHE_ERR_INVALID_ARG;
   void* scratch = nullptr;
-  if (tiled_down_ws_bytes(M, H, I) > 0) RETURN_IF(get_workspace(tiled_down_ws_bytes(M, H, I), &scratch));
+  if (tiled_down_ws_bytes(M, H, I) > 0)
+    RETURN_IF(get_workspace(static_cast<hipStream_t>(stream), tiled_down_ws_bytes(M, H, I), &scratch));
   return hip_status(launch_down_tiled(static_cast<hipStream_t>(stream), hq, hs, wd_q, wd_s, out, out_tap, M, H, I,
                                       scratch, wd_row_s));
 }
@@ -452,7 +477,7 @@ int lacache_ffn_fp8_g(void* stream, const uint16_t* x, const uint16_t* norm_w, c
       !disjoint({rng(out, M * H * 2)}, {rng(wgu_row_s, 2 * I * 4), rng(wd_row_s, H * 4)}))
     return LACACHE_ERR_INVALID_ARG;
   void* base = nullptr;
-  RETURN_IF(get_workspace(lacache_ffn_g_workspace_bytes(M, H, I), &base));
+  RETURN_IF(get_workspace(static_cast<hipStream_t>(stream), lacache_ffn_g_workspace_bytes(M, H, I), &base));
   // [fp32 y, then h][xq][xs][hq][hs][row scales][split-K partials]
   char* b = static_cast<char*>(base);
   const size_t m = static_cast<size_t>(M);
@@ -546,7 +571,7 @@ int lacache_first_layer_tokens(void* stream, const int32_t* token_ids, const int
                  rng(w_qkv, nq * hb), rng(rope_cos, tab), rng(rope_sin, tab)}))
     return LACACHE_ERR_INVALID_ARG;
   void* base = nullptr;
-  RETURN_IF(get_workspace(lacache_first_layer_workspace_bytes(R, heads, H), &base));
+  RETURN_IF(get_workspace(static_cast<hipStream_t>(stream), lacache_first_layer_workspace_bytes(R, heads, H), &base));
   uint16_t* y = static_cast<uint16_t*>(base);
   uint16_t* qkv = reinterpret_cast<uint16_t*>(static_cast<char*>(base) + align256(static_cast<size_t>(R * H) * 2));
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -609,6 +634,7 @@ const char* lacache_status_string(int status) {
     case LACACHE_ERR_UNSUPPORTED: return "LACACHE_ERR_UNSUPPORTED";
     case LACACHE_ERR_HIP: return "LACACHE_ERR_HIP";
     case LACACHE_ERR_ALLOC: return "LACACHE_ERR_ALLOC";
+    case LACACHE_ERR_CAPTURE: return "LACACHE_ERR_CAPTURE";
     default: return "LACACHE_UNKNOWN_STATUS";
   }
 }
@@ -618,10 +644,11 @@ void lacache_release_workspace(void) {
   int cur = 0;
   const bool have_cur = hipGetDevice(&cur) == hipSuccess;
   for (size_t d = 0; d < g_ws.size(); ++d) {
-    if (g_ws[d].ptr == nullptr) continue;
+    if (g_ws[d].ptr == nullptr && g_ws[d].retired.empty()) continue;
     if (hipSetDevice(static_cast<int>(d)) == hipSuccess) {
       (void)hipDeviceSynchronize();
-      (void)hipFree(g_ws[d].ptr);
+      if (g_ws[d].ptr != nullptr) (void)hipFree(g_ws[d].ptr);
+      for (void* p : g_ws[d].retired) (void)hipFree(p);
     }
     g_ws[d] = DeviceWs{};
   }

@@ -9,6 +9,8 @@
 namespace lacache {
 
 hipError_t launch_quant_weights(hipStream_t st, const uint16_t* w, uint8_t* wq, float* ws, int64_t N, int64_t K);
+// Row-major e4m3 codes [N x K] (N % 16 == 0, K % 128 == 0) -> tile layout.
+hipError_t launch_pack_weights(hipStream_t st, const uint8_t* w, uint8_t* wt, int64_t N, int64_t K);
 // With y non-null: x = RNE_bf16(x + y) in place first (the fused AddNorm).
 hipError_t launch_rmsnorm_quant(hipStream_t st, uint16_t* x, const uint16_t* nw, uint8_t* xq, float* xs, int64_t M,
                                 int64_t H, const uint16_t* y = nullptr);

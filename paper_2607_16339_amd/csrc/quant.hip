@@ -62,6 +62,29 @@ hipError_t launch_quant_weights(hipStream_t st, const uint16_t* w, uint8_t* wq, 
 }
 
 // ---------------------------------------------------------------------------
+// Row-major e4m3 codes [N x K] -> the weight tile layout (wtile_off). A
+// 16-byte run of a row (k a multiple of 16) stays contiguous in the tile
+// layout (it lies inside one 64-column half of a tile), so each thread moves
+// one run: loads are contiguous across the wavefront, stores are 64-byte
+// segments.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void pack_weights_kernel(const uint8_t* __restrict__ w, uint8_t* __restrict__ wt,
+                                                           int64_t N, int64_t K) {
+  const int64_t runs = K / 16;
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= N * runs) return;
+  const int64_t n = i / runs, k = (i - n * runs) * 16;
+  *reinterpret_cast<uint4*>(wt + wtile_off(n, k, K)) = *reinterpret_cast<const uint4*>(w + n * K + k);
+}
+
+hipError_t launch_pack_weights(hipStream_t st, const uint8_t* w, uint8_t* wt, int64_t N, int64_t K) {
+  const int64_t threads = N * (K / 16);
+  hipLaunchKernelGGL(pack_weights_kernel, dim3(static_cast<unsigned>((threads + 255) / 256)), dim3(256), 0, st, w, wt,
+                     N, K);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // Fused RMSNorm + 1x128 quantization. A row belongs to 1 << wpr_log2
 // wavefronts; lane l of each holds chunks c = 64 t + l (8 bf16 each) for
 // t < T, so a 128-wide group is the 16 lanes 16g'..16g'+15 of one pass. The

@@ -89,6 +89,13 @@ def test_stage_validation(L):
     assert L.lacache_down_proj(None, p[0], p[1], p[2], p[3], p[4], None, 0, 256, 768, 128) == OK
     assert L.lacache_quant_weights(None, p[0], p[1], p[2], 256, 200, 128) == INVALID
     assert L.lacache_quant_weights(None, p[0], p[0], p[2], 256, 256, 128) == INVALID  # w_q aliases w
+    # row-major -> tile repack of weight codes
+    assert L.lacache_pack_weights(None, p[0], p[1], 256, 200) == INVALID
+    assert L.lacache_pack_weights(None, p[0], p[1], 0, 256) == INVALID
+    assert L.lacache_pack_weights(None, p[0], p[0] + 1024, 256, 256) == INVALID  # overlap
+    assert L.lacache_pack_weights(None, None, p[1], 256, 256) == INVALID
+    assert L.lacache_pack_weights(None, p[0], p[1] + 8, 256, 256) == INVALID  # misaligned
+    assert L.lacache_pack_weights(None, p[0], p[1], 256, 131072 + 128) == UNSUP
     assert L.lacache_add_bf16(None, p[0], p[0], 16) == INVALID
     assert L.lacache_add_bf16(None, p[0], p[1], 0) == OK
     assert L.lacache_add_bf16(None, p[0], p[1], -1) == INVALID
@@ -195,7 +202,7 @@ def test_workspace_bytes_and_status_strings(L):
     assert L.lacache_ffn_workspace_bytes(M, H, I, 64) == 0
     assert L.lacache_ffn_workspace_bytes(-1, H, I, 128) == 0
     for s, name in [(0, "LACACHE_OK"), (-1, "LACACHE_ERR_INVALID_ARG"), (-2, "LACACHE_ERR_UNSUPPORTED"),
-                    (-3, "LACACHE_ERR_HIP"), (-4, "LACACHE_ERR_ALLOC")]:
+                    (-3, "LACACHE_ERR_HIP"), (-4, "LACACHE_ERR_ALLOC"), (-5, "LACACHE_ERR_CAPTURE")]:
         assert L.lacache_status_string(s).decode() == name
 
 

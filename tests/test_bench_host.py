@@ -23,7 +23,17 @@ def test_steps_default_by_workload():
     assert bench.parse([]).steps == 50
     assert bench.parse(["--workload", "stack31_m512_h4096_i12288"]).steps == 32
     assert bench.parse(["--workload", "stack31_m512_h4096_i12288", "--steps", "3"]).steps == 3
-    assert bench.parse([]).workload == "block32_h4096_i12288"
+    # the largest single-GPU configuration is the default line; the decode block is nested in it
+    assert bench.parse([]).workload == "batch8x1024_h4096_i12288" == bench.DEFAULT_WORKLOAD
+    assert bench.NESTED_WORKLOAD == "block32_h4096_i12288"
+
+
+def test_trace_kernel_us_reads_the_committed_summary():
+    """The live kernel time is compared with the same kernel's average in the
+    committed rocprofv3 summary; the parser reads that file's table."""
+    us = bench.trace_kernel_us("batch8x1024_h4096_i12288", "void lacache::gemm_tiled_kernel<true")
+    assert us is not None and 100.0 < us < 5000.0
+    assert bench.trace_kernel_us("no_such_workload", "x") is None
 
 
 def test_stage_bytes_at_the_decode_block():
