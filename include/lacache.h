@@ -206,6 +206,29 @@ int lacache_ffn_fp8_ws(void* stream, const uint16_t* x, const uint16_t* norm_w, 
                        const float* wgu_s, const uint8_t* wd_q, const float* wd_s, uint16_t* out,
                        int64_t M, int64_t H, int64_t I, int group, void* workspace, size_t ws_bytes);
 
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops and harnesses that forbid hipMalloc):
+ * lacache_ffn_fp8 with its whole workspace in a fixed device array of
+ * LACACHE_NOALLOC_SCRATCH_BYTES (64 MiB) that the library's code object
+ * holds on every device it runs on until the process ends. The call
+ * allocates nothing (no hipMalloc, hipFree or allocating library routine);
+ * its first call on a device looks up the array's address on that device
+ * (hipGetSymbolAddress, no allocation). Arguments, results and errors are
+ * those of lacache_ffn_fp8, and the same kernels run, so the output bytes
+ * are identical. A shape whose workspace (lacache_ffn_workspace_bytes)
+ * exceeds the array returns LACACHE_ERR_UNSUPPORTED before anything is
+ * launched; at H = 4096, I = 12288 every M <= 1024 fits. All calls on one
+ * device share the array, which keeps the last call's contents (no part of
+ * it needs any initial value): calls that overlap in time on one device
+ * (other streams, other host threads) race on it, so the caller must
+ * serialize them.
+ */
+#define LACACHE_NOALLOC_SCRATCH_BYTES (64u << 20)
+int lacache_ffn_fp8_noalloc(void* stream, const uint16_t* x, const uint16_t* norm_w, const uint8_t* wgu_q,
+                            const float* wgu_s, const uint8_t* wd_q, const float* wd_s, uint16_t* out,
+                            int64_t M, int64_t H, int64_t I, int group);
+
 /* Residual add between stacked layers (the "Add" of the AddNorm that Sec. 3.4
  * fuses with the quantization; also available fused, see
  * lacache_add_rmsnorm_quant): x[i] = RNE_bf16(float(x[i]) + float(y[i])), i < n.

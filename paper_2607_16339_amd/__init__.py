@@ -111,6 +111,13 @@ def lacache_ffn_fp8(x, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, group=GROUP, strea
           "lacache_ffn_fp8")
 
 
+def lacache_ffn_fp8_noalloc(x, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, group=GROUP, stream=None):
+    """lacache_ffn_fp8 with its workspace in the library's fixed device array: allocates nothing."""
+    check(lib().lacache_ffn_fp8_noalloc(_stream(stream, x),
+                                        *_ffn_args(x, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, group)),
+          "lacache_ffn_fp8_noalloc")
+
+
 def lacache_ffn_fp8_addnorm(resid, y, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, group=GROUP, stream=None):
     """resid += y (in place), then out = the FP8 FFN of resid."""
     args = _ffn_args(resid, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, group)

@@ -31,6 +31,7 @@ SIGNATURES = {
     "lacache_down_proj": (_I, [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I]),
     "lacache_ffn_fp8": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I]),
     "lacache_ffn_workspace_bytes": (ctypes.c_size_t, [_I64, _I64, _I64, _I]),
+    "lacache_ffn_fp8_noalloc": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I]),
     "lacache_ffn_fp8_ws": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I, _P, ctypes.c_size_t]),
     "lacache_add_bf16": (_I, [_P, _P, _P, _I64]),
     "lacache_encode_e4m3": (_I, [_P, _P, _P, _I64]),

@@ -12,6 +12,14 @@
 #include "lacache.h"
 #include "launch.h"
 
+// Workspace of lacache_ffn_fp8_noalloc: a fixed device array that the code
+// object holds on every device the library runs on, until the process ends.
+// In host code `scratch` names a host-side stand-in, not device memory: only
+// the address that hipGetSymbolAddress returns on a device may reach a kernel
+// or a copy.
+constexpr size_t kNoAllocBytes = size_t(LACACHE_NOALLOC_SCRATCH_BYTES);
+static __device__ __align__(256) uint8_t scratch[kNoAllocBytes];
+
 namespace {
 
 using namespace lacache;
@@ -157,6 +165,29 @@ int get_workspace(hipStream_t st, size_t bytes, void** out) {
     }
   }
   *out = w.ptr;
+  return LACACHE_OK;
+}
+
+// Device address of `scratch` on the current device, looked up once per
+// device (with that device current) and kept.
+constexpr int kMaxDevices = 64;
+std::mutex g_na_mu;
+void* g_na_ptr[kMaxDevices] = {};
+
+int noalloc_scratch(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return LACACHE_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return LACACHE_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lk(g_na_mu);
+  if (g_na_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) {
+      (void)hipGetLastError();
+      return LACACHE_ERR_HIP;
+    }
+    g_na_ptr[dev] = p;
+  }
+  *out = g_na_ptr[dev];
   return LACACHE_OK;
 }
 
@@ -377,6 +408,22 @@ int lacache_ffn_fp8_ws(void* stream, const uint16_t* x, const uint16_t* norm_w, 
     return LACACHE_ERR_INVALID_ARG;
   return ffn_core(static_cast<hipStream_t>(stream), x, nullptr, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, M, H, I, path,
                   lay);
+}
+
+int lacache_ffn_fp8_noalloc(void* stream, const uint16_t* x, const uint16_t* norm_w, const uint8_t* wgu_q,
+                            const float* wgu_s, const uint8_t* wd_q, const float* wd_s, uint16_t* out, int64_t M,
+                            int64_t H, int64_t I, int group) {
+  RETURN_IF(validate_ffn(x, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, M, H, I, group));
+  Path path;
+  RETURN_IF(choose_path(M, H, I, &path));
+  if (M == 0) return LACACHE_OK;
+  if (ffn_layout(nullptr, M, H, I).total > kNoAllocBytes) return LACACHE_ERR_UNSUPPORTED;
+  void* base = nullptr;
+  RETURN_IF(noalloc_scratch(&base));
+  // every kernel writes each workspace element it reads first, so nothing in
+  // the array needs clearing
+  return ffn_core(static_cast<hipStream_t>(stream), x, nullptr, norm_w, wgu_q, wgu_s, wd_q, wd_s, out, M, H, I, path,
+                  ffn_layout(base, M, H, I));
 }
 
 // ---------------------------------------------------------------------------

@@ -219,6 +219,21 @@ def test_ws_variant_checks_workspace(L):
     assert L.lacache_ffn_fp8_ws(*args0, None, 0) == OK             # M == 0: nothing to do
 
 
+def test_noalloc_validation(L):
+    """The allocation-free FFN call validates like lacache_ffn_fp8 and refuses,
+    before any HIP call, a shape whose workspace exceeds its fixed array."""
+    f = Fake()
+    p = [f() for _ in range(8)]
+    call = lambda M, H=4096, I=12288, g=128, ps=p: L.lacache_ffn_fp8_noalloc(None, *ps[:7], M, H, I, g)
+    assert call(32, g=64) == UNSUP
+    assert call(32, H=4000) == INVALID
+    assert call(0) == OK
+    assert call(32, ps=[None] + p[1:]) == INVALID
+    assert L.lacache_ffn_workspace_bytes(8192, 4096, 12288, 128) > (64 << 20)
+    assert call(8192) == UNSUP  # 129 MiB of workspace > the 64 MiB array
+    assert all(L.lacache_ffn_workspace_bytes(M, 4096, 12288, 128) <= (64 << 20) for M in range(1, 1025))
+
+
 def test_binding_refuses_host_tensors():
     import torch
     import paper_2607_16339_amd as lc
