@@ -79,8 +79,14 @@ def parse(argv=None):
                    help="time the eager host loop instead of the HIP-graph replay of the K steps")
     p.add_argument("--profile-only", action="store_true",
                    help="run warmup + timed steps only (for rocprofv3), print the line without the CPU leg")
+    p.add_argument("--warm-s", type=float, default=WARM_S,
+                   help="seconds of untimed graph replays before the timed one (shorter under a profiler)")
     p.add_argument("--calibrate-copy", action="store_true",
                    help="also run a plain device copy of 256 MiB three times (the HBM counter calibration)")
+    p.add_argument("--counters-from", nargs=2, metavar=("COUNTER_CSV", "KERNEL_TRACE_CSV"),
+                   help="summarize a rocprofv3 --pmc counter CSV per kernel (averages per dispatch; MFMA busy "
+                        "fraction of the SIMDs' active cycles, FP8 MFMA FLOP from the MOPS counter, against the "
+                        "kernel durations of a --kernel-trace CSV of the same command), then exit")
     p.add_argument("--traffic-from", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "WORKLOAD"),
                    help="turn two rocprofv3 --pmc counter CSVs (FETCH_SIZE, WRITE_SIZE) of a --calibrate-copy "
                         "run into per-launch HBM bytes in profiles/pmc_traffic.json, then exit")
@@ -154,6 +160,69 @@ def kernel_key(name):
     return None
 
 
+CUS = 256
+SIMDS_PER_CU = 4
+
+
+def counters_from(counter_csv, trace_csv):
+    """Per-kernel averages of a rocprofv3 --pmc run (values summed over a
+    dispatch's rows, then averaged over the kernel's dispatches), with
+      mfma_busy_frac   = SQ_VALU_MFMA_BUSY_CYCLES / (4 SIMDs x SQ_BUSY_CU_CYCLES)
+      fp8_flop         = 512 x SQ_INSTS_VALU_MFMA_MOPS_F8 per dispatch
+      fp8_frac_of_peak = fp8_flop / (average duration in the kernel trace) / peak
+      implied_clock_ghz = the clock at which that busy share gives that rate
+                          (a 16x16x128 FP8 MFMA keeps a SIMD busy 32 cycles:
+                          2048 FLOP per SIMD per cycle)
+    The kernel trace is a separate --kernel-trace run of the same command
+    (counter collection serializes kernels and would lengthen them)."""
+    import csv
+    import collections
+
+    per = collections.defaultdict(lambda: collections.defaultdict(float))
+    names, res = {}, {}
+    for r in csv.DictReader(open(counter_csv)):
+        d = r["Dispatch_Id"]
+        per[d][r["Counter_Name"]] += float(r["Counter_Value"])
+        names[d] = r["Kernel_Name"]
+        res[d] = {c: int(r[c]) for c in ("VGPR_Count", "Accum_VGPR_Count", "SGPR_Count", "LDS_Block_Size",
+                                         "Scratch_Size", "Workgroup_Size", "Grid_Size") if r.get(c, "").isdigit()}
+    agg = collections.defaultdict(lambda: collections.defaultdict(list))
+    kres = {}
+    for d, cs in per.items():
+        k = kernel_key(names[d])
+        if k is None:
+            continue
+        kres[k] = res[d]
+        for c, v in cs.items():
+            agg[k][c].append(v)
+    dur = collections.defaultdict(list)
+    for r in csv.DictReader(open(trace_csv)):
+        k = kernel_key(r["Kernel_Name"])
+        if k is not None:
+            dur[k].append((float(r["End_Timestamp"]) - float(r["Start_Timestamp"])) * 1e-9)
+    out = {}
+    for k, cs in agg.items():
+        a = {c: sum(v) / len(v) for c, v in cs.items()}
+        e = {"dispatches": len(next(iter(cs.values()))), "avg": {c: round(v, 1) for c, v in sorted(a.items())},
+             "resources": kres.get(k, {})}
+        if "SQ_VALU_MFMA_BUSY_CYCLES" in a and a.get("SQ_BUSY_CU_CYCLES"):
+            # both counters summed over the CUs, in the same clock: the MFMA
+            # pipes' busy share of the cycles the CUs were busy
+            e["mfma_busy_frac"] = round(a["SQ_VALU_MFMA_BUSY_CYCLES"] / (SIMDS_PER_CU * a["SQ_BUSY_CU_CYCLES"]), 4)
+        if "SQ_INSTS_VALU_MFMA_MOPS_F8" in a:
+            e["fp8_flop"] = 512.0 * a["SQ_INSTS_VALU_MFMA_MOPS_F8"]
+            if dur.get(k):
+                t = sum(dur[k]) / len(dur[k])
+                e["trace_avg_us"] = round(t * 1e6, 2)
+                e["fp8_frac_of_peak"] = round(e["fp8_flop"] / t / 1e12 / PEAK_FP8_TFLOPS, 4)
+                if e.get("mfma_busy_frac"):
+                    # FLOP rate = busy share x SIMDs x 2048 FLOP/clk x clock: the clock it implies
+                    e["implied_clock_ghz"] = round(e["fp8_flop"] / t / (e["mfma_busy_frac"] * CUS * SIMDS_PER_CU * 2048)
+                                                   / 1e9, 3)
+        out[k] = e
+    print(json.dumps(out, indent=1, sort_keys=True))
+
+
 def traffic_from(fetch_csv, write_csv, workload):
     """Per-dispatch FETCH_SIZE / WRITE_SIZE (KiB) averaged per kernel, scaled by
     the ratio of the known bytes of a plain 256 MiB device copy to what the
@@ -205,6 +274,9 @@ def main():
     args = parse()
     if args.traffic_from:
         traffic_from(*args.traffic_from)
+        return
+    if args.counters_from:
+        counters_from(*args.counters_from)
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -429,7 +501,7 @@ def ffn_line(args, w, dev, nested=False):
         torch.cuda.synchronize()
         if not torch.equal(got, probe):
             raise RuntimeError("graph replay of the FFN step differs from the eager call")
-        tg = time_graph(g, K, stream)
+        tg = time_graph(g, K, stream, warm_s=args.warm_s)
         del g
         ms = tg["timed"]
         t_wall = tg["wall_s"]
@@ -544,7 +616,7 @@ def stage_timings(args, w, sets, out, dev):
         torch.cuda.synchronize()
         if not torch.equal(got, probe):
             raise RuntimeError("graph replay of the %s stage differs from the eager call" % name)
-        t = time_graph(g, reps, torch.cuda.current_stream(), warm_s=0.1, min_warm=2)
+        t = time_graph(g, reps, torch.cuda.current_stream(), warm_s=min(0.1, args.warm_s), min_warm=2)
         k_ms[name] = t["timed"]
         del g
     dom = "gateup"

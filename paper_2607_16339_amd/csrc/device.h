@@ -124,6 +124,28 @@ __device__ __forceinline__ float swiglu_fast(float g, float u) {
 }
 
 // ---------------------------------------------------------------------------
+// RMSNorm fused with the 1x128 quantizer, the arithmetic shared by every
+// kernel that normalizes a row (the same operations in the same order, so
+// the codes and scales are bit-identical wherever they are computed).
+// A wavefront owns a row: lane l holds the 16-byte chunks c = 64 t + l (8
+// bf16 each), so a 128-wide group is 16 consecutive lanes of one pass t.
+// ---------------------------------------------------------------------------
+// p + the squares of the chunk's 8 values in element order (each square of a
+// bf16 value is exact in fp64).
+__device__ __forceinline__ double sumsq8(double p, uint4 v);
+// r = RN32(1 / sqrt(ss / H + 1e-5)) from the row's fp64 sum of squares (ss =
+// the xor-butterfly total of the lanes' partials), every step in fp64.
+__device__ __forceinline__ float rms_inv(double ss, int H) {
+  return static_cast<float>(1.0 / __builtin_sqrt(ss / static_cast<double>(H) + 1e-5));
+}
+// y = RN32(RN32(x w) r) of a chunk's 8 values (x w is exact in fp32).
+__device__ __forceinline__ void norm8(uint4 xv, uint4 wv, float r, float (&y)[8]);
+// The 1x128 group quantizer of a chunk's 8 values y within its 16-lane group:
+// returns the group scale s = RN32(max|y| / 448) and the codes E(RN32(y / s))
+// (all 0x00 when s == 0). Every lane of the 16 must call it.
+__device__ __forceinline__ float quant8_group(const float (&y)[8], uint32_t& lo, uint32_t& hi);
+
+// ---------------------------------------------------------------------------
 // bf16 <-> fp32
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float bf16lo(uint32_t w) { return __uint_as_float(w << 16); }
@@ -241,6 +263,44 @@ __device__ __forceinline__ float max_xor(float v) {
 #pragma unroll
   for (int o = kWidth / 2; o >= 1; o >>= 1) v = __builtin_fmaxf(v, __shfl_xor(v, o, 64));
   return v;
+}
+
+// ---- definitions of the RMSNorm + quantizer helpers declared above
+
+__device__ __forceinline__ double sumsq8(double p, uint4 v) {
+  const uint32_t q[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const double a = bf16lo(q[e]), b = bf16hi(q[e]);
+    p = p + a * a;
+    p = p + b * b;
+  }
+  return p;
+}
+
+__device__ __forceinline__ void norm8(uint4 xv, uint4 wv, float r, float (&y)[8]) {
+  const uint32_t q[4] = {xv.x, xv.y, xv.z, xv.w};
+  const uint32_t g[4] = {wv.x, wv.y, wv.z, wv.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    y[2 * e] = (bf16lo(q[e]) * bf16lo(g[e])) * r;  // x*w is exact in fp32; one rounding for *r
+    y[2 * e + 1] = (bf16hi(q[e]) * bf16hi(g[e])) * r;
+  }
+}
+
+__device__ __forceinline__ float quant8_group(const float (&y)[8], uint32_t& lo, uint32_t& hi) {
+  float amax = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) amax = __builtin_fmaxf(amax, __builtin_fabsf(y[e]));
+  amax = max_xor<16>(amax);
+  const float s = amax / kE4M3Max;
+  lo = 0u;
+  hi = 0u;
+  if (s != 0.0f && !(scale_is_fast(s) && enc8_div_fast(y, fast_rcp(s), lo, hi))) {
+    lo = enc4_e4m3(qdiv(y[0], s), qdiv(y[1], s), qdiv(y[2], s), qdiv(y[3], s));
+    hi = enc4_e4m3(qdiv(y[4], s), qdiv(y[5], s), qdiv(y[6], s), qdiv(y[7], s));
+  }
+  return s;
 }
 
 }  // namespace lacache

@@ -141,18 +141,10 @@ __global__ __launch_bounds__(256) void rmsnorm_quant_kernel(uint16_t* x, const u
     if (t * 64 + lane >= nchunk) xv[t] = make_uint4(0u, 0u, 0u, 0u);
   double p = 0.0;
 #pragma unroll
-  for (int t = 0; t < T; ++t) {
-    const uint32_t q[4] = {xv[t].x, xv[t].y, xv[t].z, xv[t].w};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const double a = bf16lo(q[e]), b = bf16hi(q[e]);
-      p = p + a * a;  // the square of a bf16 value is exact in fp64
-      p = p + b * b;
-    }
-  }
+  for (int t = 0; t < T; ++t) p = sumsq8(p, xv[t]);
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) p = p + __shfl_xor(p, o, 64);
-  const float r = static_cast<float>(1.0 / __builtin_sqrt(p / static_cast<double>(H) + 1e-5));
+  const float r = rms_inv(p, H);
   if (y != nullptr) {
     // every wavefront of the row has used all of the old row (the sum above)
     // before any writes its passes of the new one; the row's wavefronts are
@@ -168,14 +160,8 @@ __global__ __launch_bounds__(256) void rmsnorm_quant_kernel(uint16_t* x, const u
     if ((t & ((1 << wpr_log2) - 1)) != part) continue;  // uniform
     const int c = t * 64 + lane;
     const bool valid = c < nchunk;  // whole 16-lane groups share validity (H % 128 == 0)
-    const uint32_t q[4] = {xv[t].x, xv[t].y, xv[t].z, xv[t].w};
-    const uint32_t g[4] = {wv[t].x, wv[t].y, wv[t].z, wv[t].w};
     float y[8];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      y[2 * e] = (bf16lo(q[e]) * bf16lo(g[e])) * r;  // x*w is exact in fp32; one rounding for *r
-      y[2 * e + 1] = (bf16hi(q[e]) * bf16hi(g[e])) * r;
-    }
+    norm8(xv[t], wv[t], r, y);
     if (kF32Out) {
       if (valid) {
         float4* d = reinterpret_cast<float4*>(yf + row * H + 8 * c);
@@ -184,16 +170,8 @@ __global__ __launch_bounds__(256) void rmsnorm_quant_kernel(uint16_t* x, const u
       }
       continue;
     }
-    float amax = 0.0f;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) amax = __builtin_fmaxf(amax, __builtin_fabsf(y[e]));
-    amax = max_xor<16>(amax);
-    const float s = amax / kE4M3Max;
-    uint32_t lo = 0u, hi = 0u;
-    if (s != 0.0f && !(scale_is_fast(s) && enc8_div_fast(y, fast_rcp(s), lo, hi))) {
-      lo = enc4_e4m3(qdiv(y[0], s), qdiv(y[1], s), qdiv(y[2], s), qdiv(y[3], s));
-      hi = enc4_e4m3(qdiv(y[4], s), qdiv(y[5], s), qdiv(y[6], s), qdiv(y[7], s));
-    }
+    uint32_t lo, hi;
+    const float s = quant8_group(y, lo, hi);
     if (valid) {
       *reinterpret_cast<uint2*>(xq + row * H + 8 * c) = make_uint2(lo, hi);
       if ((lane & 15) == 0) xs[static_cast<int64_t>(c >> 4) * M + row] = s;
