@@ -25,8 +25,8 @@ Pins (tests/test_oracle_*.py): the quantizer, norm, GEMM, SwiGLU, bf16 and
 residual steps are each checked against exact rational arithmetic, closed
 forms or PyTorch's own casts. ``ffn`` is the composition of those steps and is
 pinned only through them (the paper prints no values for a whole layer).
-``ffn_bf16_reference`` is a context figure, not a parity target: parity
-unpinned beyond a sanity band against the FP8 result.
+``ffn_bf16_reference`` is a context figure, not a parity target; its bf16
+rounding steps are pinned against exact-rational arithmetic on a tiny layer.
 """
 
 import numpy as np

@@ -152,3 +152,66 @@ def test_fp8_ffn_is_close_to_bf16_ffn_on_tiny_workload():
     gq, gs = quant_weights(wts["w_gate"])
     uq, us = quant_weights(wts["w_up"])
     assert np.array_equal(wgu_q, np.concatenate([gq, uq])) and np.array_equal(wgu_s, np.concatenate([gs, us]))
+
+
+def _rne_bf16_exact(q: Fraction) -> Fraction:
+    """Nearest bf16 value of an exact rational (ties to even), normal range."""
+    if q == 0:
+        return Fraction(0)
+    a = abs(q)
+    e = a.numerator.bit_length() - a.denominator.bit_length()
+    if Fraction(2) ** e > a:
+        e -= 1
+    elif Fraction(2) ** (e + 1) <= a:
+        e += 1
+    unit = Fraction(2) ** (e - 7)  # 8 significant bits
+    n = a / unit
+    fl = n.numerator // n.denominator
+    rem = n - fl
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and fl % 2 == 1):
+        fl += 1
+    v = fl * unit
+    return v if q > 0 else -v
+
+
+def _bits_value(bits):
+    return [Fraction(float(v)) for v in bf16_to_f32(np.asarray(bits, np.uint16)).ravel()]
+
+
+def test_ffn_bf16_reference_against_exact_rationals():
+    """The unquantized bf16 FFN (the context figure of the bench line) step by
+    step in exact rationals on a tiny layer: y rounded to bf16, g and u the
+    exact dot products rounded once to bf16, h = SiLU(g) u (exp in fp64, the
+    only inexact step) rounded to bf16, out the exact dot product rounded to
+    bf16. A variant that drops any one of the roundings must differ."""
+    rng = np.random.default_rng(21)
+    M, H, I = 2, 128, 128
+    to_bits = lambda a: torch.from_numpy(np.asarray(a, np.float32)).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    xb = to_bits(rng.standard_normal((M, H)))
+    nw = to_bits(1 + 0.02 * rng.standard_normal(H))
+    wg, wu, wd = (to_bits(rng.standard_normal(s) * 0.3) for s in ((I, H), (I, H), (H, I)))
+    got = ffn_bf16_reference(xb, nw, wg, wu, wd)
+    from oracle.ffn import rmsnorm
+    y, _ = rmsnorm(xb, nw)  # pinned separately (test_oracle_norm.py)
+    yb = [[_rne_bf16_exact(Fraction(float(v))) for v in row] for row in y]
+    Wg = np.array(_bits_value(wg), dtype=object).reshape(I, H)
+    Wu = np.array(_bits_value(wu), dtype=object).reshape(I, H)
+    Wd = np.array(_bits_value(wd), dtype=object).reshape(H, I)
+    for m in range(M):
+        g = [_rne_bf16_exact(sum(yb[m][k] * Wg[n][k] for k in range(H))) for n in range(I)]
+        u = [_rne_bf16_exact(sum(yb[m][k] * Wu[n][k] for k in range(H))) for n in range(I)]
+        h = []
+        for n in range(I):
+            gf = float(g[n])
+            silu = Fraction(gf / (1.0 + math.exp(-gf)))  # fp64; its error is far below a bf16 step
+            h.append(_rne_bf16_exact(silu * u[n]))
+        out = [_rne_bf16_exact(sum(h[k] * Wd[n][k] for k in range(I))) for n in range(H)]
+        assert [Fraction(float(v)) for v in got[m]] == out, m
+    # every rounding matters: dropping the one on g (or on h) changes the output
+    y64 = y.astype(np.float64)
+    ybf = bf16_to_f32(rne_bf16(y64)).astype(np.float64)
+    wgf, wuf, wdf = (bf16_to_f32(w).astype(np.float64) for w in (wg, wu, wd))
+    g_nr = ybf @ wgf.T
+    u_r = bf16_to_f32(rne_bf16(ybf @ wuf.T)).astype(np.float64)
+    h_nr = bf16_to_f32(rne_bf16(g_nr / (1 + np.exp(-g_nr)) * u_r)).astype(np.float64)
+    assert not np.array_equal(bf16_to_f32(rne_bf16(h_nr @ wdf.T)).astype(np.float64), got)
