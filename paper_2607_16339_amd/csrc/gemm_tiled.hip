@@ -486,9 +486,18 @@ hipError_t launch_tiled(hipStream_t st, const uint8_t* aq, const float* as, cons
   return hipGetLastError();
 }
 
-// Row-tile height: 256 when there are enough row tiles to fill the chip with
-// one workgroup per CU, else 128.
-bool use_bm256(int64_t M, int64_t col_tiles) { return ((M + 255) / 256) * col_tiles >= 512; }
+// Row-tile height, by rounds of one workgroup per CU: 256-row tiles unless
+// 128-row tiles fill no more rounds. A round of 256-row tiles (twice the
+// work) takes about 1.4-1.6 times a round of 128-row tiles over the same K,
+// so fewer rounds of the larger tile win whenever the smaller one needs more;
+// with equal rounds the smaller tile leaves fewer CUs idle (and the down GEMM
+// then splits K when it has fewer tiles than CUs).
+bool use_bm256(int64_t M, int64_t col_tiles) {
+  const int64_t cus = cu_count();
+  const int64_t r256 = (((M + 255) / 256) * col_tiles + cus - 1) / cus;
+  const int64_t r128 = (((M + 127) / 128) * col_tiles + cus - 1) / cus;
+  return r128 > r256;
+}
 
 // K splits of the down GEMM: enough workgroups for about one per CU, each
 // split at least 16 K-groups long.
@@ -508,19 +517,10 @@ size_t tiled_down_ws_bytes(int64_t M, int64_t H, int64_t I) {
   return ks > 1 ? static_cast<size_t>(ks) * static_cast<size_t>(M) * static_cast<size_t>(H) * 4 : 0;
 }
 
-// gate/up row-tile height by the number of rounds of one workgroup per CU:
-// a 256-row tile does twice the work of a 128-row one in about 1.8 times
-// the time.
-bool gateup_bm256(int64_t M, int64_t I) {
-  const int64_t cols = I / 128;
-  const int64_t r256 = (((M + 255) / 256) * cols + 255) / 256, r128 = (((M + 127) / 128) * cols + 255) / 256;
-  return 18 * r256 <= 10 * r128;
-}
-
 hipError_t launch_gateup_tiled(hipStream_t st, const uint8_t* xq, const float* xs, const uint8_t* wq,
                                const float* ws, uint8_t* hq, float* hs, float* h_tap, int64_t M, int64_t H,
                                int64_t I, const float* col_s) {
-  if (gateup_bm256(M, I))
+  if (use_bm256(M, I / 128))
     return launch_tiled<true, 256>(st, xq, xs, wq, ws, hq, hs, h_tap, nullptr, nullptr, nullptr, M, H, 2 * I, I, 1,
                                    col_s);
   return launch_tiled<true, 128>(st, xq, xs, wq, ws, hq, hs, h_tap, nullptr, nullptr, nullptr, M, H, 2 * I, I, 1,

@@ -53,6 +53,9 @@ WORKLOADS = {
     "batch8x1024_h4096_i12288": Workload(
         3, "batch8x1024_h4096_i12288", 8192, 4096, 12288, act="seq_scale", outlier_ratio=0.01, seqs=8,
         notes="8 sequences x 1024 tokens; per-sequence scale logU(0.5, 8); 1% outliers x40"),
+    "batch4x1024_h4096_i12288": Workload(
+        5, "batch4x1024_h4096_i12288", 4096, 4096, 12288, act="seq_scale", outlier_ratio=0.01, seqs=4,
+        notes="4 sequences x 1024 tokens (the smallest M of the MFMA-bound range); as batch8x1024"),
     "stack31_m512_h4096_i12288": Workload(
         4, "stack31_m512_h4096_i12288", 512, 4096, 12288, act="stack", layers=31, steps=32,
         notes="31 FFN layers with residual adds over 32 denoising steps; std 0.5->8, outliers 3%->0.5%"),

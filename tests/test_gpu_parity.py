@@ -421,6 +421,27 @@ def test_batch8192_sampled(big_layer):
     _say("batch8192: gate/up %s; down error %.2e, %.3f of the model tolerance" % (g, e, d))
 
 
+def test_batch4096_sampled(big_layer):
+    """M = 4096, the smallest M of the MFMA-bound range: 256-row tiles for both
+    GEMMs (one round of 256 down tiles over all of K), sampled rows."""
+    w = synth.WORKLOADS["batch4x1024_h4096_i12288"]
+    rows = lambda M: np.concatenate([[0, M - 1], np.sort(np.random.default_rng(6).choice(M, 6, replace=False))])
+    g, e, d = _full_size_case(big_layer, w, 0, rows, 0)
+    _say("batch4096: gate/up %s; down error %.2e, %.3f of the model tolerance" % (g, e, d))
+
+
+def test_bm256_partial_row_tile_sampled(big_layer):
+    """M = 3000: 256-row tiles for both GEMMs with a last row tile of 184 rows
+    (clamped activation rows, unstored outputs); sampled rows, all of the last
+    tile's edge included."""
+    M = 3000
+    w = synth.Workload(93, "bm256_partial", M, 4096, 12288, act="outlier", outlier_ratio=0.01)
+    rows = lambda m: np.unique(np.concatenate([[0, 255, 256, 2815, 2816, m - 2, m - 1],
+                                               np.random.default_rng(M).choice(np.arange(1, 2815), 4, replace=False)]))
+    g, e, d = _full_size_case(big_layer, w, 0, rows, 0)
+    _say("bm256 partial M=%d: gate/up %s; down error %.2e, %.3f of the model tolerance" % (M, g, e, d))
+
+
 @pytest.mark.parametrize("M,ks", [(200, 6), (700, 3), (1024, 2)])
 def test_split_k_down_sampled(big_layer, M, ks):
     """The tiled down GEMM with its K range split over KS workgroups per

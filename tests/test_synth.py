@@ -38,6 +38,10 @@ def test_step_and_sequence_scales():
     w4 = synth.WORKLOADS["batch8x1024_h4096_i12288"]
     s4 = synth.step_std(w4, 1, 0)
     assert len(np.unique(s4)) == 8 and np.all(s4[:1024] == s4[0])
+    w4b = synth.WORKLOADS["batch4x1024_h4096_i12288"]
+    s4b = synth.step_std(w4b, 1, 0)
+    assert w4b.M == 4096 and len(np.unique(s4b)) == 4 and np.all(s4b[:1024] == s4b[0])
+    assert len({w.wid for w in synth.WORKLOADS.values()}) == len(synth.WORKLOADS)
     w5 = synth.WORKLOADS["stack31_m512_h4096_i12288"]
     assert abs(synth.step_std(w5, 1, 0)[0] - 0.5) < 1e-6 and abs(synth.step_std(w5, 1, 31)[0] - 8.0) < 1e-5
     assert abs(synth.outlier_ratio(w5, 0) - 0.03) < 1e-12 and abs(synth.outlier_ratio(w5, 31) - 0.005) < 1e-12
