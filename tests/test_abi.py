@@ -66,6 +66,7 @@ def test_ffn_validation(L):
     assert _ffn(L, H=0) == INVALID
     assert _ffn(L, M=-1) == INVALID
     assert _ffn(L, H=16384 + 128) == UNSUP
+    assert _ffn(L, I=65536 + 128) == UNSUP
     assert _ffn(L, M=(1 << 24) + 1) == UNSUP
     assert _ffn(L, x=None) == INVALID
     assert _ffn(L, out=0x10000000008) == INVALID  # misaligned

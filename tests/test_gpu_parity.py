@@ -455,6 +455,51 @@ def test_split_k_down_sampled(big_layer, M, ks):
     _say("split-K M=%d: gate/up %s; down error %.2e, %.3f of the model tolerance" % (M, g, e, d))
 
 
+@pytest.mark.parametrize("M,H,I", [(5, 16384, 1024), (5, 256, 65536)])
+def test_maximum_h_and_i(M, H, I):
+    """The largest H (16384) and the largest I (65536) the library takes, each
+    with a small M: long K loops (128 K-groups in the gate/up, 512 in the
+    down), and at I = 65536 the down GEMM's widest K split (32 workgroups per
+    output tile, one tile). Every row against the oracle."""
+    _say("max sizes M=%d H=%d I=%d" % (M, H, I))
+    w = synth.Workload(92, "max_%d_%d" % (H, I), M, H, I, act="outlier", outlier_ratio=0.01)
+    lay = Layer(w, layer=1)
+    g, e, d = _full_size_case(lay, w, 0, lambda m: np.arange(m), 0)
+    _say("max sizes H=%d I=%d: gate/up %s; down error %.2e, %.3f of the model tolerance" % (H, I, g, e, d))
+
+
+def test_maximum_m():
+    """M = 2^24, the largest M the library takes (H = I = 128): every stage
+    over 16.8 M rows (the activations drawn on the GPU from a seeded
+    generator), checked against the oracle on sampled rows, the first and
+    last included."""
+    M, H, I = 1 << 24, 128, 128
+    _say("max M=%d" % M)
+    w = synth.Workload(91, "max_m", 64, H, I)  # the weights' shapes only
+    lay = Layer(w, layer=1)
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(20260716)
+    x = torch.randn((M, H), generator=gen, device=DEV, dtype=torch.float32).to(torch.bfloat16)
+    t = run_stages(x, lay, M, H, I, sentinel=False)
+    rows = np.unique(np.concatenate([[0, 1, M // 2, M - 2, M - 1], np.random.default_rng(7).choice(M, 11, replace=False)]))
+    ri = torch.from_numpy(rows).to(DEV)
+    sel = lambda name: host(t[name].index_select(0, ri))
+    selc = lambda name: host(t[name].index_select(1, ri))
+    xb = host_bf16(x.index_select(0, ri))
+    wgu_q, wgu_s, wd_q, wd_s = lay.host_weights()
+    xq, xs, hq, hs = sel("xq"), selc("xs"), sel("hq"), selc("hs")
+    check_norm_exact(xb, lay.bits["norm_w"], xq, xs)
+    check_requant_exact(sel("h_tap"), hq, hs)
+    g = check_gateup_model(xq, xs, wgu_q, wgu_s, I, sel("h_tap"), hq, hs)
+    e = check_down_same_operands(hq, hs, wd_q, wd_s, sel("out_tap"), host_bf16(t["out"].index_select(0, ri)))
+    d = check_down_model(hq, hs, wd_q, wd_s, sel("out_tap"))
+    # every row was written: the fp32 taps started as NaN
+    assert torch.isfinite(t["h_tap"]).all().item() and torch.isfinite(t["out_tap"]).all().item()
+    _say("max M: gate/up %s; down error %.2e, %.3f of the model tolerance" % (g, e, d))
+    del t, x
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("M", [50, 130])
 def test_tiled_partial_column_tile(M):
     """The tiled kernels at H = 640 (H % 256 == 128): the down GEMM's last
