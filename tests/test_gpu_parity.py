@@ -359,6 +359,49 @@ def test_stages_ragged_shapes(M, policy):
     check_down_model(host(t["hq"]), host(t["hs"]), wd_q, wd_s, host(t["out_tap"]))
 
 
+@pytest.mark.parametrize("policy", [0, 2])
+def test_zero_rows_and_zero_blocks(policy):
+    """The method's degenerate cases through the whole FFN, on both paths: an
+    all-zero input row and an all-(-0) one (r = 1/sqrt(eps), every group
+    scale 0 and every code 0x00, an all-zero h row and output row); a zero
+    128-row block of W_gate and W_up (that h-group is 0 in every row, so its
+    scale is 0 and its codes 0x00 come from the epilogue's zero-scale rule);
+    a zero 128-row block of W_down (those output columns 0). Checked against
+    the oracle like every other case, and the fused call equals the stages."""
+    lc.lacache_set_path_policy(policy)
+    M, H, I = 17, 256, 768
+    w = synth.Workload(89, "degenerate", M, H, I, act="outlier", outlier_ratio=0.02)
+    lay = Layer(w, layer=1, quantize=False)
+    b = lay.bits
+    b["w_gate"][256:384] = 0
+    b["w_up"][256:384] = 0
+    b["w_down"][128:256] = 0
+    lay.wgu_bits = np.concatenate([b["w_gate"], b["w_up"]], axis=0)
+    lay.wgu_q, lay.wgu_s = lc.quantize_weights(dev_bf16(lay.wgu_bits))
+    lay.wd_q, lay.wd_s = lc.quantize_weights(dev_bf16(b["w_down"]))
+    xb = synth.make_x(w, layer=1)
+    xb[3] = 0
+    xb[M - 1] = 0x8000
+    x = dev_bf16(xb)
+    t = run_stages(x, lay, M, H, I)
+    wgu_q, wgu_s, wd_q, wd_s = lay.host_weights()
+    xq, xs, hq, hs = host(t["xq"]), host(t["xs"]), host(t["hq"]), host(t["hs"])
+    check_norm_exact(xb, b["norm_w"], xq, xs)
+    check_requant_exact(host(t["h_tap"]), hq, hs)
+    g = check_gateup_model(xq, xs, wgu_q, wgu_s, I, host(t["h_tap"]), hq, hs)
+    check_down_same_operands(hq, hs, wd_q, wd_s, host(t["out_tap"]), host_bf16(t["out"]))
+    check_down_model(hq, hs, wd_q, wd_s, host(t["out_tap"]))
+    for r in (3, M - 1):
+        assert np.all(xq[r] == 0) and np.all(xs[:, r] == 0)
+        assert np.all(hq[r] == 0) and np.all(hs[:, r] == 0)
+    assert np.all(hq[:, 256:384] == 0) and np.all(hs[2] == 0)
+    out = host_bf16(t["out"])
+    assert np.all(out[:, 128:256] & 0x7FFF == 0) and np.all(out[[3, M - 1]] & 0x7FFF == 0)
+    fused = lc.ffn_fp8(x, lay.norm_w, lay.wgu_q, lay.wgu_s, lay.wd_q, lay.wd_s)
+    assert np.array_equal(host_bf16(fused), out)
+    _say("degenerate policy=%d: gate/up %s" % (policy, g))
+
+
 @pytest.mark.parametrize("M,H,I", [(5, 256, 384), (32, 640, 1152), (16, 8192, 256), (32, 4096, 384),
                                    (17, 1152, 2304), (3, 128, 256), (2, 256, 128), (33, 512, 384),
                                    (48, 4096, 384), (64, 1152, 256), (64, 4096, 128)])
