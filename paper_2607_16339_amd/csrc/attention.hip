@@ -29,7 +29,9 @@
 // Scheduling. Work item w = (head, query block) in head-major order, heavy
 // query blocks (those overlapping C) first within a head; consecutive work
 // items go to the same XCD (workgroups are dealt to the 8 XCDs round-robin),
-// so the query blocks of a head share that XCD's L2 copy of its K and V.
+// so the query blocks of a head share that XCD's L2 copy of its K and V. In
+// resume mode, when the grid takes more than one round, each XCD takes its
+// heavy items before its light ones.
 #include "device.h"
 #include "launch.h"
 
@@ -63,6 +65,7 @@ struct AttnArgs {
   int qbh0;     // first query block overlapping those key blocks
   int nheavy;   // query blocks overlapping them
   int total;    // workgroups
+  int heavy_first;  // resume: each XCD's heavy items before its light ones
   float scale_log2;
 };
 
@@ -84,6 +87,25 @@ __device__ __forceinline__ uint32_t pack_bf16_rne(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, v);
 }
 
+// Slot s of an XCD's chunk [lo, lo + n) of the head-major item list, with the
+// chunk's heavy items (query blocks j < nh of a head, which stream every key
+// block) first and its light ones after. Resume uses this order: a light item
+// streams only the C blocks, a heavy one all of them, and heavy items dealt
+// out late would leave their long chains to the end of the call. A bijection
+// of [lo, lo + n) for 0 < nh < nqb (else the identity).
+__device__ __forceinline__ int heavy_first(int lo, int s, int n, int nqb, int nh) {
+  if (nh <= 0 || nh >= nqb) return lo + s;
+  auto heavy_below = [&](int x) { return (x / nqb) * nh + (x % nqb < nh ? x % nqb : nh); };
+  const int h0 = heavy_below(lo), nhc = heavy_below(lo + n) - h0;
+  if (s < nhc) {
+    const int gh = h0 + s;  // global index among heavy items
+    return (gh / nh) * nqb + gh % nh;
+  }
+  const int nl = nqb - nh;
+  const int gl = (lo - h0) + (s - nhc);  // global index among light items
+  return (gl / nl) * nqb + nh + gl % nl;
+}
+
 // kMode 0: populate, 1: resume, 2: plain attention; W wavefronts, S stages
 template <int kMode, int W, int S>
 __global__ __launch_bounds__(64 * W, 2) void facache_attention_kernel(AttnArgs a) {
@@ -93,10 +115,12 @@ __global__ __launch_bounds__(64 * W, 2) void facache_attention_kernel(AttnArgs a
   const int t = threadIdx.x, lane = t & 63, wave = wave_uniform(t >> 6);
   const int g = lane >> 5, r = lane & 31;
 
-  // work item: consecutive items on one XCD
+  // work item: consecutive items on one XCD (resume: the chunk's heavy items first)
   const int bid = blockIdx.x, xcd = bid & 7, slot = bid >> 3;
   const int per = a.total >> 3, rem = a.total & 7;
-  const int w = xcd < rem ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
+  const int lo = xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per;
+  const int w = (kMode == 1 && a.heavy_first) ? heavy_first(lo, slot, xcd < rem ? per + 1 : per, a.nqb, a.nheavy)
+                                              : lo + slot;
   const int64_t h = w / a.nqb;
   const int j = w - static_cast<int>(h) * a.nqb;
   const bool heavy = j < a.nheavy;
@@ -290,6 +314,10 @@ hipError_t launch_ws(hipStream_t st, AttnArgs a, int64_t heads, int mode) {
   a.qbh0 = a.nc > 0 ? a.cb0 * kKB / WR : 0;
   a.nheavy = a.nc > 0 ? static_cast<int>(((a.cb0 + a.nc) * int64_t(kKB) - 1) / WR) - a.qbh0 + 1 : 0;
   a.total = static_cast<int>(heads * a.nqb);
+  // heavy items first only when the grid takes more than one round (two
+  // workgroups per CU): in a single round every item starts at once and the
+  // order only decides which items share a CU
+  a.heavy_first = a.total > 2 * device_cu_count() ? 1 : 0;
   const dim3 grid(static_cast<unsigned>(a.total)), block(64 * W);
   if (mode == 0)
     hipLaunchKernelGGL((facache_attention_kernel<0, W, S>), grid, block, 0, st, a);

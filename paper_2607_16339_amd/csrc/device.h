@@ -174,27 +174,6 @@ __device__ __forceinline__ v4f mfma_fp8_16x16x128(v8i a, v8i b, v4f c) {
   return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
 }
 
-// ---------------------------------------------------------------------------
-// Direct global -> LDS copies (gfx950). Lane l of the wavefront writes its
-// 16 (or 4) bytes to lds + 16*l (4*l); `lds` must be wave-uniform. Counted by
-// vmcnt. Wrapped in plain functions so that kernel templates stay valid in
-// the host compilation pass.
-// ---------------------------------------------------------------------------
-__device__ __forceinline__ void lds_dma16(const void* src, void* lds) {
-  __builtin_amdgcn_global_load_lds(src, lds, 16, 0, 0);
-}
-__device__ __forceinline__ void lds_dma4(const void* src, void* lds) {
-  __builtin_amdgcn_global_load_lds(src, lds, 4, 0, 0);
-}
-
-// L2 prefetch: a 1-byte vector load of the cache line at p into `sink`, a
-// register the caller keeps live (and never reads) until it has waited for
-// vmcnt to drain. The load is opaque to the compiler, so it neither waits for
-// it nor reuses `sink` early.
-__device__ __forceinline__ void prefetch_l2(const void* p, uint32_t& sink) {
-  asm volatile("global_load_ubyte %0, %1, off" : "+v"(sink) : "v"(p));
-}
-
 // An int the compiler can see is the same in every lane of the wavefront.
 __device__ __forceinline__ int wave_uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
@@ -212,10 +191,6 @@ __device__ __forceinline__ uint32_t lds_u32(const void* p) {
 // 16 bytes per lane global -> LDS: lane l lands at lds + 16 l (lds wave-uniform).
 __device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
-}
-// 4 bytes per lane global -> LDS: lane l lands at lds + 4 l.
-__device__ __forceinline__ void dma4(const void* g, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
 }
 // The same with a wave-uniform 64-bit base in SGPRs and a 32-bit per-lane
 // byte offset (the global instructions' scalar-base form): no 64-bit address

@@ -430,6 +430,20 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
   wait_vm<0>();  // the trailing repeat copies
 }
 
+// Compute units of the current device (the persistent grid's size), cached
+// per device; 256 when the runtime cannot tell.
+int device_cu_count() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+
 template __global__ void gemm_tiled_kernel<true, 256>(const uint8_t*, const float*, const uint8_t*, const float*,
                                                      uint8_t*, float*, float*, uint16_t*, float*, float*, const float*, int64_t,
                                                      int64_t, int64_t, int64_t, int, int);
@@ -459,20 +473,6 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restri
   if (out_tap != nullptr) *reinterpret_cast<float4*>(out_tap + e) = acc;
 }
 
-// Compute units of the current device (the persistent grid's size), cached
-// per device.
-int cu_count() {
-  static int cached[64] = {0};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cached[dev] == 0) {
-    int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-    cached[dev] = n;
-  }
-  return cached[dev];
-}
-
 template <bool kGateUp, int BM>
 hipError_t launch_tiled(hipStream_t st, const uint8_t* aq, const float* as, const uint8_t* bq, const float* bs,
                         uint8_t* hq, float* hs, float* h_tap, uint16_t* out, float* out_tap, float* part, int64_t M,
@@ -480,7 +480,7 @@ hipError_t launch_tiled(hipStream_t st, const uint8_t* aq, const float* as, cons
   const int64_t ny = kGateUp ? I / 128 : (N + BNR - 1) / BNR;
   const int W = static_cast<int>(((M + BM - 1) / BM) * ny * KS);  // work items (< 2^31 by the size limits)
   // one workgroup per CU (the LDS ring allows no more)
-  const int G = W < cu_count() ? W : cu_count();
+  const int G = W < device_cu_count() ? W : device_cu_count();
   hipLaunchKernelGGL((gemm_tiled_kernel<kGateUp, BM>), dim3(static_cast<unsigned>(G)), dim3(kTileWaves * 64), 0, st,
                      aq, as, bq, bs, hq, hs, h_tap, out, out_tap, part, col_s, M, K, N, I, KS, W);
   return hipGetLastError();
@@ -493,7 +493,7 @@ hipError_t launch_tiled(hipStream_t st, const uint8_t* aq, const float* as, cons
 // with equal rounds the smaller tile leaves fewer CUs idle (and the down GEMM
 // then splits K when it has fewer tiles than CUs).
 bool use_bm256(int64_t M, int64_t col_tiles) {
-  const int64_t cus = cu_count();
+  const int64_t cus = device_cu_count();
   const int64_t r256 = (((M + 255) / 256) * col_tiles + cus - 1) / cus;
   const int64_t r128 = (((M + 127) / 128) * col_tiles + cus - 1) / cus;
   return r128 > r256;

@@ -32,6 +32,10 @@ hipError_t launch_quant_weights_rows(hipStream_t st, const uint16_t* w, uint8_t*
 hipError_t launch_quant_groups_f32(hipStream_t st, const float* v, uint8_t* codes, float* scales, int64_t M, int64_t K);
 hipError_t launch_encode_e4m3(hipStream_t st, const float* v, uint8_t* codes, int64_t n);
 
+// Compute units of the current device, cached per device (256 when the
+// runtime cannot tell).
+int device_cu_count();
+
 // Tile (row r, column c) of workgroup `bid` in an R x C grid of output tiles.
 // Workgroups are handed out round-robin over the 8 XCDs, each with its own
 // L2, so XCD x runs workgroups x, x + 8, ... Each XCD gets a contiguous range
