@@ -15,6 +15,8 @@
 //                         rows, K split over the 4 wavefronts (private
 //                         direct-to-LDS rings), bf16 MFMAs into fp32, the four
 //                         partials added in wavefront order, bf16 out;
+//   linear_bf16_tiled_kernel  the same result for many rows, from 128 x 128
+//                         or 128 x 192 output tiles (W read once per 128 rows);
 //   rope_scatter_kernel   rotate-half RoPE of the Q and K heads from fp32 cos /
 //                         sin tables, V unrotated, scattered to each row's
 //                         position in Q, K, V.
@@ -212,6 +214,135 @@ __global__ __launch_bounds__(kLinSplit * 64) void linear_bf16_kernel(const uint1
   }
 }
 
+// out = a W^T for many rows: BM x BN output tiles, 8 wavefronts (4 bands of
+// BM/4 activation rows x 2 bands of BN/2 weight rows), one direct-to-LDS ring
+// of 3 stages shared by the workgroup (K-steps of 64 elements: BM activation
+// rows and BN weight rows a stage), so a staged activation row serves BN
+// weight rows and a staged weight row BM activation rows; with BM = 128, W
+// is read once per 128 rows instead of once per 64. Every output element gets exactly the
+// arithmetic of linear_bf16_kernel: the same four K quarters, each a chain of
+// the same 16x16x32 bf16 MFMAs on the same operand halves (K-step by K-step)
+// started from zero, and the quarter sums added in quarter order. So a row's
+// result does not depend on which of the two kernels computed it, and a
+// block update of the caches still equals a full recompute bit for bit.
+constexpr int kLtWaves = 8, kLtS = 3;
+#ifndef LACACHE_LIN_TILED_MIN_M
+#define LACACHE_LIN_TILED_MIN_M 128
+#endif
+constexpr int64_t kLinTiledMinM = LACACHE_LIN_TILED_MIN_M;  // rows above which the tiled kernel runs
+
+// BM x BN output tile; wavefront (wm, wn) of 4 x 2 owns BM/4 rows x BN/2
+// columns (MT x NT 16x16 tiles)
+template <int BM, int BN>
+__global__ __launch_bounds__(kLtWaves * 64) void linear_bf16_tiled_kernel(const uint16_t* __restrict__ a,
+                                                                        const uint16_t* __restrict__ w,
+                                                                        uint16_t* __restrict__ out,
+                                                                        float* __restrict__ out_tap, int64_t M,
+                                                                        int64_t N, int64_t K) {
+  constexpr int kStage = (BM + BN) * 128;             // bytes per stage
+  constexpr int kPer = (BM + BN) / 8 / kLtWaves;      // 1 KB copies per wavefront per stage
+  constexpr int MT = BM / 64, NT = BN / 32, WRr = BM / 4, WCc = BN / 2;
+  static_assert((BM + BN) % (8 * kLtWaves) == 0 && BM % 64 == 0 && BN % 32 == 0, "tile shape");
+  __shared__ __align__(16) uint8_t ring[kLtS][kStage];
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = wave_uniform(t >> 6);
+  const int q = lane >> 4, lr = lane & 15;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int64_t n0 = static_cast<int64_t>(blockIdx.x) * BN;
+  const int64_t m0 = static_cast<int64_t>(blockIdx.y) * BM;
+  const int KS = static_cast<int>(K / 64);
+  const uint8_t* ab = reinterpret_cast<const uint8_t*>(a);
+  const uint8_t* wb = reinterpret_cast<const uint8_t*>(w);
+
+  // copy plan: copy u of wavefront v fills stage rows 8 g .. 8 g + 7, g = v + 8 u
+  // (rows 0..BM-1 activations, then BN weight rows); lane l fills row 8 g + l/8,
+  // physical chunk l%8, i.e. logical chunk (l%8) ^ (row & 7)
+  const int crow = lane >> 3, pch = lane & 7;
+  int64_t src[kPer];
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    const int row = 8 * (wave + kLtWaves * u) + crow;
+    const int chunk = (pch ^ (row & 7)) << 4;
+    if (row < BM) {
+      const int64_t gr = m0 + row < M ? m0 + row : M - 1;
+      src[u] = gr * K * 2 + chunk;
+    } else {
+      src[u] = (n0 + row - BM) * K * 2 + chunk;
+    }
+  }
+  auto issue = [&](int ks, int st) {
+    const uint32_t base = lds_u32(&ring[st][0]);
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int g = wave + kLtWaves * u;
+      const uint8_t* b = (8 * g < BM ? ab : wb) + src[u] + static_cast<int64_t>(ks) * 128;
+      dma16(b, wave_uniform(static_cast<int>(base) + g * 1024));
+    }
+  };
+
+  v4f acc[MT][NT], tot[MT][NT];
+  const v4f zero = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int j = 0; j < NT; ++j) tot[i][j] = zero;
+#pragma unroll
+  for (int s = 0; s < kLtS - 1; ++s)
+    if (s < KS) issue(s, s);
+  int ks = 0;
+  for (int qq = 0; qq < kLinSplit; ++qq) {
+    const int k1 = (qq + 1) * KS / kLinSplit;
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int j = 0; j < NT; ++j) acc[i][j] = zero;
+    for (; ks < k1; ++ks) {
+      // this wavefront's copies of step ks have landed (later ones may fly) ...
+      if (ks + kLtS - 2 < KS)
+        wait_vm<(kLtS - 2) * kPer>();
+      else
+        wait_vm<0>();
+      bar();  // ... and every wavefront's; the stage refilled next is read by no one
+      if (ks + kLtS - 1 < KS) issue(ks + kLtS - 1, (ks + kLtS - 1) % kLtS);
+      const uint8_t* st = &ring[ks % kLtS][0];
+      bf8 alo[MT], ahi[MT];
+#pragma unroll
+      for (int i = 0; i < MT; ++i) lin_frag(st + (WRr * wm + 16 * i) * 128, lr, q, alo[i], ahi[i]);
+#pragma unroll
+      for (int j = 0; j < NT; ++j) {
+        bf8 blo, bhi;
+        lin_frag(st + (BM + WCc * wn + 16 * j) * 128, lr, q, blo, bhi);
+#pragma unroll
+        for (int i = 0; i < MT; ++i) {
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo[i], blo, acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi[i], bhi, acc[i][j], 0, 0, 0);
+        }
+      }
+    }
+    // the quarter's sum joins the total in quarter order (the first is a copy)
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int j = 0; j < NT; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) tot[i][j][r] = qq == 0 ? acc[i][j][r] : tot[i][j][r] + acc[i][j][r];
+  }
+  wait_vm<0>();
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t row = m0 + WRr * wm + 16 * i + 4 * q + r;
+      if (row >= M) continue;
+#pragma unroll
+      for (int j = 0; j < NT; ++j) {
+        const int64_t col = n0 + WCc * wn + 16 * j + lr;
+        out[row * N + col] = static_cast<uint16_t>(f32_to_bf16(tot[i][j][r]));
+        if (out_tap != nullptr) out_tap[row * N + col] = tot[i][j][r];
+      }
+    }
+}
+
 // One thread per (row r, Q/K/V part, head, pair i < 64): the pair (i, i + 64)
 // of the head's 128 values; Q and K rotated by the angle of the row's position.
 __global__ __launch_bounds__(256) void rope_scatter_kernel(const uint16_t* __restrict__ qkv,
@@ -264,6 +395,23 @@ hipError_t launch_embed_rmsnorm(hipStream_t st, const int32_t* ids, const int32_
 
 hipError_t launch_linear_bf16(hipStream_t st, const uint16_t* a, const uint16_t* w, uint16_t* out, float* out_tap,
                               int64_t M, int64_t N, int64_t K) {
+  if (M > kLinTiledMinM) {
+    // many rows: 128-row tiles (N % 128 == 0), W read once per 128 rows
+    // 128 x 192 tiles when they need fewer rounds of one workgroup per CU
+    // than 128 x 128 (measured at N = 12288, K = 4096: 52 against 72 us at
+    // M = 512, 122 against 132 us at M = 1024; at M = 256, with one round
+    // either way, 128 x 128 leaves fewer CUs idle: 39 against 47 us)
+    const int64_t rt = (M + 127) / 128, cus = device_cu_count();
+    const bool wide = N % 192 == 0 && (rt * (N / 192) + cus - 1) / cus < (rt * (N / 128) + cus - 1) / cus;
+    const dim3 block(kLtWaves * 64);
+    if (wide)
+      hipLaunchKernelGGL((linear_bf16_tiled_kernel<128, 192>), dim3(static_cast<unsigned>(N / 192), rt), block, 0, st,
+                         a, w, out, out_tap, M, N, K);
+    else
+      hipLaunchKernelGGL((linear_bf16_tiled_kernel<128, 128>), dim3(static_cast<unsigned>(N / 128), rt), block, 0, st,
+                         a, w, out, out_tap, M, N, K);
+    return hipGetLastError();
+  }
   // up to 64 rows per pass; the last pass may hold fewer slabs. Three weight
   // slabs per workgroup when that still gives a workgroup per CU (few rows),
   // else one.

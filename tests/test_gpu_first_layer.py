@@ -106,6 +106,36 @@ def test_linear_bf16(M, N, K):
     _linear_check(a, w, out, tap)
 
 
+@pytest.mark.parametrize("M,N,K", [(300, 384, 1024), (129, 256, 384), (257, 128, 128), (512, 12288, 4096),
+                                   (700, 12288, 512)])
+def test_linear_tiled_equals_streaming(M, N, K):
+    """Above 128 rows the projection runs on 128 x 128 or 128 x 192 tiles (the
+    latter at N = 12288 with 512 and 700 rows); below, W is streamed per 64
+    rows. Both must give every row the same bytes (the same
+    K quarters, MFMA chains and quarter order), so the same rows through the
+    streaming kernel (calls of at most 64 rows) equal the tiled call bit for
+    bit, including ragged M, K-step counts not divisible by four and empty
+    quarters (K = 128)."""
+    rng = np.random.default_rng(M + N + K)
+    a = to_bf16_bits(rng.standard_normal((M, K)).astype(np.float32))
+    w = to_bf16_bits((0.03 * rng.standard_normal((N, K))).astype(np.float32))
+    da, dw = dev_bf16(a), dev_bf16(w)
+    _say("tiled vs streaming M=%d N=%d K=%d" % (M, N, K))
+    out = torch.empty((M, N), dtype=torch.bfloat16, device=DEV)
+    tap = torch.full((M, N), float("nan"), dtype=torch.float32, device=DEV)
+    lc.lacache_linear_bf16(da, dw, out, tap)
+    out_s = torch.empty_like(out)
+    tap_s = torch.full_like(tap, float("nan"))
+    for r0 in range(0, M, 64):
+        r1 = min(M, r0 + 64)
+        lc.lacache_linear_bf16(da[r0:r1], dw, out_s[r0:r1], tap_s[r0:r1])
+    torch.cuda.synchronize()
+    assert torch.equal(tap.view(torch.int32), tap_s.view(torch.int32))
+    assert torch.equal(out.view(torch.int16), out_s.view(torch.int16))
+    if M * N * K <= 2 ** 28:
+        _linear_check(a, w, out, tap)
+
+
 def test_rope_scatter_bit_exact():
     heads, N, R = 3, 192, 40
     rng = np.random.default_rng(4)
