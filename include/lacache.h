@@ -389,8 +389,10 @@ int lacache_embed_rmsnorm(void* stream, const int32_t* token_ids, const int32_t*
 
 /* out [M x N] bf16 = RNE_bf16(a [M x K] W[N x K]^T), bf16 inputs, fp32
  * accumulation (bf16 MFMAs; the K range is split over four partial sums added
- * in a fixed order); out_tap (nullable) receives the fp32 result. Streams W
- * from HBM once per 64 rows of a: meant for the few rows of a block. */
+ * in a fixed order); out_tap (nullable) receives the fp32 result. Up to 128
+ * rows W is streamed from HBM once per 64 rows of a (the few rows of a block);
+ * above, 128-row output tiles read it once per 128 rows. Both give every row
+ * the same bytes, so a row's result does not depend on M. */
 int lacache_linear_bf16(void* stream, const uint16_t* a, const uint16_t* w, uint16_t* out, float* out_tap, int64_t M,
                         int64_t N, int64_t K);
 
