@@ -499,12 +499,14 @@ bool use_bm256(int64_t M, int64_t col_tiles) {
   return r128 > r256;
 }
 
-// K splits of the down GEMM: enough workgroups for about one per CU, each
-// split at least 16 K-groups long.
+// K splits of the down GEMM: as many as fit in one round of one workgroup
+// per CU, each split at least 16 K-groups long. Rounding up instead spills a
+// few items into a second round: at H = 4096, I = 12288, M = 700 (96 tiles)
+// 3 splits took 75.5 us against 56.8 us for 2.
 int down_splits(int64_t M, int64_t H, int64_t I) {
-  const int64_t tiles = ((M + 127) / 128) * ((H + BNR - 1) / BNR);
-  if (use_bm256(M, (H + BNR - 1) / BNR) || tiles >= 256) return 1;
-  int64_t ks = (256 + tiles - 1) / tiles;
+  const int64_t tiles = ((M + 127) / 128) * ((H + BNR - 1) / BNR), cus = device_cu_count();
+  if (use_bm256(M, (H + BNR - 1) / BNR) || tiles >= cus) return 1;
+  int64_t ks = cus / tiles;
   const int64_t max_ks = (I / 128) / 16;
   if (ks > max_ks) ks = max_ks;
   return ks < 1 ? 1 : static_cast<int>(ks);

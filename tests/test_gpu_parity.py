@@ -485,12 +485,18 @@ def test_bm256_partial_row_tile_sampled(big_layer):
     _say("bm256 partial M=%d: gate/up %s; down error %.2e, %.3f of the model tolerance" % (M, g, e, d))
 
 
-@pytest.mark.parametrize("M,ks", [(200, 6), (700, 3), (1024, 2)])
+@pytest.mark.parametrize("M,ks", [(200, 6), (320, 5), (576, 3), (700, 2), (1024, 2)])
 def test_split_k_down_sampled(big_layer, M, ks):
     """The tiled down GEMM with its K range split over KS workgroups per
-    output tile (KS = 6 at 200 rows, 3 at 700, 2 at 1024 for H = 4096,
+    output tile (as many as fit one round of one workgroup per CU on 256 CUs:
+    KS = 6 at 200 rows, 5 at 320, 3 at 576, 2 at 700 and 1024 for H = 4096,
     I = 12288), oracle-checked on sampled rows, the first and last included."""
     _say("split-K M=%d KS=%d" % (M, ks))
+    if torch.cuda.get_device_properties(0).multi_processor_count == 256:
+        # the workspace: the KS fp32 partials [KS][M][H], then xq [M][H] and
+        # hq [M][3H] (I = 3H), i.e. (KS + 1) M H 4 bytes, plus the scales
+        ws = lc.lacache_ffn_workspace_bytes(M, 4096, 12288)
+        assert (ks + 1) * M * 4096 * 4 <= ws < (ks + 2) * M * 4096 * 4
     w = synth.Workload(94, "splitk", M, 4096, 12288, act="outlier", outlier_ratio=0.01)
     rows = lambda m: np.concatenate([[0, m - 1], np.sort(np.random.default_rng(M).choice(np.arange(1, m - 1), 6,
                                                                                           replace=False))])
