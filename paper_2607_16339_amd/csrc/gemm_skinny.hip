@@ -7,9 +7,10 @@
 // partials are added in LDS in a fixed order.
 //
 // gate/up: a workgroup owns 3 (gate, up) slab pairs x 4 K parts (one
-//          wavefront each). The activation codes are copied into LDS once
-//          per workgroup (up to 32 rows over all of K; 33..64 rows over
-//          one half of K, the halves in two workgroups); the weights go global -> VGPRs with non-temporal
+//          wavefront each), or at 33..64 rows 6 pairs x 2 parts. The
+//          activation codes are copied into LDS once per workgroup (up to
+//          32 rows over all of K; 33..64 rows over one half of K, the halves
+//          in two workgroups); the weights go global -> VGPRs with non-temporal
 //          16-byte loads straight into the MFMA operand layout, a ring of
 //          K-groups per wavefront in straight-line code (the compiler waits
 //          for one K-group's registers at a time). The weight tile layout
@@ -56,40 +57,43 @@ __device__ __forceinline__ v8i cat_frag(u4v lo, u4v hi) {
   return f;
 }
 
-// gate/up: a workgroup owns kVuPairs (gate, up) slab pairs; each pair's K
-// range is split into kVuKq parts, one wavefront each. The workgroup first
+// gate/up: a workgroup owns PAIRS (gate, up) slab pairs; each pair's K
+// range is split into KQ parts, one wavefront each (PAIRS KQ = 12). The workgroup first
 // loads the M activation rows (codes) of its K range into LDS, rows padded by
 // 16 bytes so that the 16 rows of an operand read fall on 16 different bank
 // groups; then every wavefront streams its 32 weight rows over its K part.
-// The kVuKq fp32 partials meet in LDS and are added in part order.
+// The KQ fp32 partials meet in LDS and are added in part order.
 // NH = 1: the workgroup covers all of K and applies SwiGLU (h to hbuf).
 // NH = 2 (33..64 rows, whose codes over all of K do not fit the LDS): the
 // workgroups of blockIdx.y = 0, 1 cover the two halves of K and store their
 // gate and up sums to part[y] [M][2I]; the h-quantization kernel adds the two
 // halves in that order and applies SwiGLU.
-constexpr int kVuPairs = 3;
-constexpr int kVuKq = 4;
-constexpr int kVuWaves = kVuPairs * kVuKq;
+constexpr int kVuWaves = 12;
+#ifndef LACACHE_NH2_PAIRS
+#define LACACHE_NH2_PAIRS 6
+#endif
+constexpr int kNh2Pairs = LACACHE_NH2_PAIRS;  // slab pairs per workgroup at 33..64 rows
 constexpr int kVuXBytes = 64 * (2048 + 16);  // activation rows x (K range + 16) bytes, at most
 constexpr int kVuMaxNkb = 64;                 // K-groups of the whole K
-constexpr int kVuMaxNkw = kVuMaxNkb / kVuKq;  // K-groups of one part
 constexpr int kVuScales = 2048;               // activation scales of a workgroup's K range, at most
 
-template <int MT, int DR, int NH>
+template <int MT, int DR, int NH, int PAIRS, int KQ>
 __global__ __launch_bounds__(kVuWaves * 64) void skinny_gateup_kernel(
     const uint8_t* __restrict__ aq, const float* __restrict__ as,  // activations [M x K], scales [K/128 x M]
     const uint8_t* __restrict__ wq, const float* __restrict__ ws,  // weights [2I x K], scales [2I/128 x K/128]
     float* __restrict__ h_tap, float* __restrict__ hbuf, int64_t M, int64_t K, int64_t I) {
   constexpr int R = MT * 16;  // activation rows (padded)
   static_assert(NH == 1 || NH == 2, "K pieces");
+  static_assert(PAIRS * KQ == kVuWaves, "one wavefront per (pair, part)");
+  constexpr int kMaxNkw = kVuMaxNkb / KQ;  // K-groups of one part
   __shared__ __align__(16) uint8_t sX[kVuXBytes];  // codes [R][Kw + 16]; later the partials
   __shared__ __align__(16) float sXs[kVuScales];   // activation scales [Kw/128][R]
-  __shared__ float sWs[kVuWaves][2][kVuMaxNkw];    // each wavefront's (gate, up) block scales
+  __shared__ float sWs[kVuWaves][2][kMaxNkw];    // each wavefront's (gate, up) block scales
 
   const int t = threadIdx.x, lane = t & 63;
   const int wave = wave_uniform(t >> 6);
   const int q = lane >> 4, lr = lane & 15;
-  const int pw = wave % kVuPairs, kq = wave / kVuPairs;
+  const int pw = wave % PAIRS, kq = wave / PAIRS;
   const int KB = static_cast<int>(K / 128);
   // this workgroup's K range [kbw, kbw + KBW) and its parts
   const int kh = NH == 1 ? 0 : static_cast<int>(blockIdx.y);
@@ -97,9 +101,9 @@ __global__ __launch_bounds__(kVuWaves * 64) void skinny_gateup_kernel(
   const int64_t Kw = static_cast<int64_t>(KBW) * 128;
   const int64_t stride = Kw + 16;
   const int64_t npair = I / 16;
-  const int64_t pair = static_cast<int64_t>(blockIdx.x) * kVuPairs + pw;
+  const int64_t pair = static_cast<int64_t>(blockIdx.x) * PAIRS + pw;
   const int64_t p0 = pair < npair ? pair : npair - 1;  // past the end: a valid pair, never stored
-  const int kb0 = kbw + kq * KBW / kVuKq, kb1 = kbw + (kq + 1) * KBW / kVuKq;
+  const int kb0 = kbw + kq * KBW / KQ, kb1 = kbw + (kq + 1) * KBW / KQ;
   const int nkw = kb1 - kb0;
 
   // ---- 1. activation codes -> registers: 16-byte chunk c = t + 768 j of
@@ -182,7 +186,7 @@ __global__ __launch_bounds__(kVuWaves * 64) void skinny_gateup_kernel(
     const int i = t + j * kVuWaves * 64;
     if (i < KBW * R) sXs[i] = xv[j];
   }
-  if (sj < kVuMaxNkw) sWs[wave][sn][sj] = wv;
+  if (sj < kMaxNkw) sWs[wave][sn][sj] = wv;
   __syncthreads();  // the activation codes and the scales are in LDS
 
   float acc[MT][2][4];
@@ -241,19 +245,19 @@ __global__ __launch_bounds__(kVuWaves * 64) void skinny_gateup_kernel(
 #pragma unroll
     for (int n = 0; n < 2; ++n)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) red[((kq * kVuPairs + pw) * R + 16 * i + 4 * q + r) * 32 + 16 * n + lr] = acc[i][n][r];
+      for (int r = 0; r < 4; ++r) red[((kq * PAIRS + pw) * R + 16 * i + 4 * q + r) * 32 + 16 * n + lr] = acc[i][n][r];
   __syncthreads();
   const int per_pair = static_cast<int>(M) * 16;
-  for (int e = t; e < kVuPairs * per_pair; e += kVuWaves * 64) {
+  for (int e = t; e < PAIRS * per_pair; e += kVuWaves * 64) {
     const int pp = e / per_pair, rem = e - pp * per_pair;
     const int row = rem >> 4, col = rem & 15;
-    const int64_t pr = static_cast<int64_t>(blockIdx.x) * kVuPairs + pp;
+    const int64_t pr = static_cast<int64_t>(blockIdx.x) * PAIRS + pp;
     if (pr >= npair) continue;
     float g = red[(pp * R + row) * 32 + col], u = red[(pp * R + row) * 32 + 16 + col];
 #pragma unroll
-    for (int k = 1; k < kVuKq; ++k) {
-      g += red[((k * kVuPairs + pp) * R + row) * 32 + col];
-      u += red[((k * kVuPairs + pp) * R + row) * 32 + 16 + col];
+    for (int k = 1; k < KQ; ++k) {
+      g += red[((k * PAIRS + pp) * R + row) * 32 + col];
+      u += red[((k * PAIRS + pp) * R + row) * 32 + 16 + col];
     }
     if (NH == 1) {
       const float h = swiglu_fast(g, u);
@@ -512,20 +516,25 @@ hipError_t launch_gateup_skinny(hipStream_t st, const uint8_t* xq, const float* 
                                 const float* ws, uint8_t* hq, float* hs, float* h_tap, int64_t M, int64_t H,
                                 int64_t I, void* ws_buf) {
   float* hbuf = static_cast<float*>(ws_buf);
-  const unsigned gx = static_cast<unsigned>((I / 16 + kVuPairs - 1) / kVuPairs);
   const dim3 block(kVuWaves * 64);
   const int64_t groups = M * (I / 128);
   const dim3 qgrid(static_cast<unsigned>((groups + 15) / 16)), qblock(256);
+  // up to 32 rows: 3 slab pairs x 4 K parts per workgroup (256 workgroups at
+  // I = 12288); 33..64 rows, each workgroup on one K half: 6 pairs x 2 parts,
+  // so the two halves still make one round of one workgroup per CU
+  const unsigned gx1 = static_cast<unsigned>((I / 16 + 2) / 3), gx2 = static_cast<unsigned>((I / 16 + kNh2Pairs - 1) / kNh2Pairs);
   if (M <= 16)
-    hipLaunchKernelGGL((skinny_gateup_kernel<1, kVuDR, 1>), dim3(gx), block, 0, st, xq, xs, wq, ws, h_tap, hbuf, M, H, I);
+    hipLaunchKernelGGL((skinny_gateup_kernel<1, kVuDR, 1, 3, 4>), dim3(gx1), block, 0, st, xq, xs, wq, ws, h_tap, hbuf, M, H,
+                       I);
   else if (M <= 32)
-    hipLaunchKernelGGL((skinny_gateup_kernel<2, kVuDR, 1>), dim3(gx), block, 0, st, xq, xs, wq, ws, h_tap, hbuf, M, H, I);
+    hipLaunchKernelGGL((skinny_gateup_kernel<2, kVuDR, 1, 3, 4>), dim3(gx1), block, 0, st, xq, xs, wq, ws, h_tap, hbuf, M, H,
+                       I);
   else if (M <= 48)
-    hipLaunchKernelGGL((skinny_gateup_kernel<3, kVuDR, 2>), dim3(gx, 2), block, 0, st, xq, xs, wq, ws, h_tap, hbuf, M, H,
-                       I);
+    hipLaunchKernelGGL((skinny_gateup_kernel<3, kVuDR, 2, kNh2Pairs, kVuWaves / kNh2Pairs>), dim3(gx2, 2), block, 0, st, xq,
+                       xs, wq, ws, h_tap, hbuf, M, H, I);
   else
-    hipLaunchKernelGGL((skinny_gateup_kernel<4, kVuDR, 2>), dim3(gx, 2), block, 0, st, xq, xs, wq, ws, h_tap, hbuf, M, H,
-                       I);
+    hipLaunchKernelGGL((skinny_gateup_kernel<4, kVuDR, 2, kNh2Pairs, kVuWaves / kNh2Pairs>), dim3(gx2, 2), block, 0, st, xq,
+                       xs, wq, ws, h_tap, hbuf, M, H, I);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (M <= 32)
