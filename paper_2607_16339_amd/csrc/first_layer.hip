@@ -248,8 +248,10 @@ __global__ __launch_bounds__(kLtWaves * 64) void linear_bf16_tiled_kernel(const 
   const int wave = wave_uniform(t >> 6);
   const int q = lane >> 4, lr = lane & 15;
   const int wm = wave >> 1, wn = wave & 1;
-  const int64_t n0 = static_cast<int64_t>(blockIdx.x) * BN;
-  const int64_t m0 = static_cast<int64_t>(blockIdx.y) * BM;
+  // row tiles along x (up to 2^24 / 128 of them; gridDim.y is limited to
+  // 65536), column tiles along y
+  const int64_t m0 = static_cast<int64_t>(blockIdx.x) * BM;
+  const int64_t n0 = static_cast<int64_t>(blockIdx.y) * BN;
   const int KS = static_cast<int>(K / 64);
   const uint8_t* ab = reinterpret_cast<const uint8_t*>(a);
   const uint8_t* wb = reinterpret_cast<const uint8_t*>(w);
@@ -405,11 +407,11 @@ hipError_t launch_linear_bf16(hipStream_t st, const uint16_t* a, const uint16_t*
     const bool wide = N % 192 == 0 && (rt * (N / 192) + cus - 1) / cus < (rt * (N / 128) + cus - 1) / cus;
     const dim3 block(kLtWaves * 64);
     if (wide)
-      hipLaunchKernelGGL((linear_bf16_tiled_kernel<128, 192>), dim3(static_cast<unsigned>(N / 192), rt), block, 0, st,
-                         a, w, out, out_tap, M, N, K);
+      hipLaunchKernelGGL((linear_bf16_tiled_kernel<128, 192>), dim3(static_cast<unsigned>(rt), static_cast<unsigned>(N / 192)),
+                         block, 0, st, a, w, out, out_tap, M, N, K);
     else
-      hipLaunchKernelGGL((linear_bf16_tiled_kernel<128, 128>), dim3(static_cast<unsigned>(N / 128), rt), block, 0, st,
-                         a, w, out, out_tap, M, N, K);
+      hipLaunchKernelGGL((linear_bf16_tiled_kernel<128, 128>), dim3(static_cast<unsigned>(rt), static_cast<unsigned>(N / 128)),
+                         block, 0, st, a, w, out, out_tap, M, N, K);
     return hipGetLastError();
   }
   // up to 64 rows per pass; the last pass may hold fewer slabs. Three weight

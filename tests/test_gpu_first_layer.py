@@ -136,6 +136,36 @@ def test_linear_tiled_equals_streaming(M, N, K):
         _linear_check(a, w, out, tap)
 
 
+def test_linear_maximum_m():
+    """M = 2^24 rows, the most the library takes (131072 row tiles): every row
+    written, and sampled rows equal to the streaming kernel's bytes and within
+    the oracle's bound."""
+    M, N, K = 1 << 24, 128, 128
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(716339)
+    da = torch.randn((M, K), generator=gen, device=DEV, dtype=torch.float32).to(torch.bfloat16)
+    rng = np.random.default_rng(24)
+    w = to_bf16_bits((0.03 * rng.standard_normal((N, K))).astype(np.float32))
+    dw = dev_bf16(w)
+    _say("linear M=%d" % M)
+    out = torch.empty((M, N), dtype=torch.bfloat16, device=DEV)
+    tap = torch.full((M, N), float("nan"), dtype=torch.float32, device=DEV)
+    lc.lacache_linear_bf16(da, dw, out, tap)
+    rows = np.unique(np.concatenate([[0, 1, M // 2, M - 2, M - 1], rng.choice(M, 27, replace=False)]))
+    ri = torch.from_numpy(rows).to(DEV)
+    sub = da.index_select(0, ri).contiguous()
+    out_s = torch.empty((len(rows), N), dtype=torch.bfloat16, device=DEV)
+    tap_s = torch.empty((len(rows), N), dtype=torch.float32, device=DEV)
+    lc.lacache_linear_bf16(sub, dw, out_s, tap_s)
+    torch.cuda.synchronize()
+    assert torch.isfinite(tap).all().item()
+    assert torch.equal(tap.index_select(0, ri).view(torch.int32), tap_s.view(torch.int32))
+    assert torch.equal(out.index_select(0, ri).view(torch.int16), out_s.view(torch.int16))
+    _linear_check(host_bf16(sub), w, out_s, tap_s)
+    del da, out, tap
+    torch.cuda.empty_cache()
+
+
 def test_rope_scatter_bit_exact():
     heads, N, R = 3, 192, 40
     rng = np.random.default_rng(4)
