@@ -179,6 +179,34 @@ def test_path_policy(L):
         L.lacache_set_path_policy(prev)
 
 
+def test_down_split_count_fills_one_round(L):
+    """The tiled down GEMM's K splits (read back from the workspace size, whose
+    largest part is the KS fp32 partials [KS][M][H]): with 128-row tiles and
+    fewer tiles than the 256 CUs, as many splits as fit one round of one
+    workgroup per CU, at most 6 (16 K-groups each at I = 12288)."""
+    H, I = 4096, 12288
+
+    def a256(b):
+        return (b + 255) // 256 * 256
+    for M in list(range(65, 2049, 37)) + [200, 320, 512, 576, 700, 1024, 1536]:
+        rest = a256(M * H) + a256(H // 128 * M * 4) + a256(M * I) + a256(I // 128 * M * 4)
+        scratch = L.lacache_ffn_workspace_bytes(M, H, I, 128) - rest
+        ks = scratch // (M * H * 4)
+        tiles = ((M + 127) // 128) * (H // 256)
+        r256 = (((M + 255) // 256) * 16 + 255) // 256
+        r128 = (((M + 127) // 128) * 16 + 255) // 256
+        if r128 > r256 or tiles >= 256:
+            assert scratch == 0, M  # 256-row tiles, or one round without a split
+            continue
+        if scratch == 0:
+            ks = 1  # not split: no partials
+        else:
+            assert scratch == a256(ks * M * H * 4), M
+        # the most splits that fit one round (capped at 6), never a second round
+        assert 1 <= ks <= 6 and ks * tiles <= 256, (M, ks, tiles)
+        assert ks == 6 or (ks + 1) * tiles > 256, (M, ks, tiles)
+
+
 def test_workspace_bytes_and_status_strings(L):
     def a256(b):
         return (b + 255) // 256 * 256
