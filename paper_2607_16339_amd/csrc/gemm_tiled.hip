@@ -31,6 +31,8 @@
 // the WC/2 matching up rows, so SwiGLU pairs values held by one lane, and the
 // row amax over the 128-wide h-group meets in LDS across the wavefronts of a
 // row band. h never reaches memory.
+#include <atomic>
+
 #include "device.h"
 #include "launch.h"
 
@@ -433,15 +435,15 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
 // Compute units of the current device (the persistent grid's size), cached
 // per device; 256 when the runtime cannot tell.
 int device_cu_count() {
-  static int cached[64] = {0};
+  static std::atomic<int> cached[64];  // 0: not looked up yet (zero-initialized)
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cached[dev] == 0) {
-    int n = 0;
+  int n = cached[dev].load(std::memory_order_relaxed);
+  if (n == 0) {
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-    cached[dev] = n;
+    cached[dev].store(n, std::memory_order_relaxed);
   }
-  return cached[dev];
+  return n;
 }
 
 template __global__ void gemm_tiled_kernel<true, 256>(const uint8_t*, const float*, const uint8_t*, const float*,
