@@ -22,8 +22,9 @@
 //          SwiGLU). A second kernel quantizes h per 1x128 group (a group's columns come from several workgroups,
 //          and stream order is the cheapest way to make all of them visible:
 //          device-scope fences inside the kernel cost more than the stream).
-// down:    16 output columns per workgroup, 4 K parts, direct-to-LDS copies
-//          of both operands (see the kernel).
+// down:    16 output columns per workgroup, 8 K parts (up to 32 rows and 96
+//          K-groups) or 4, direct-to-LDS copies of both operands (see the
+//          kernel).
 #include "device.h"
 #include "launch.h"
 
@@ -271,7 +272,7 @@ __global__ __launch_bounds__(kVuWaves * 64) void skinny_gateup_kernel(
   }
 }
 
-// down: 16 output columns per workgroup; its kDnSplit wavefronts take a part
+// down: 16 output columns per workgroup; its SPLIT wavefronts take a part
 // of K each and stream their part of the h codes (the M rows) and the 16
 // weight rows into a private LDS ring with direct-to-LDS copies, one K-group
 // per slot, so the streaming needs no workgroup barrier; the fp32 partials
@@ -286,36 +287,47 @@ __global__ __launch_bounds__(kVuWaves * 64) void skinny_gateup_kernel(
 // chunk c of row r at c ^ ((r / 4) mod 4). Either way the 16 rows of an
 // operand read fall on different bank groups. A weight half is one copy
 // instruction reading 1 KB contiguous of the tile.
-constexpr int kDnSplit = 4;     // wavefronts (K parts) per workgroup
-constexpr int kDnMaxNkbW = 32;  // K-groups per wavefront (scales staged in LDS)
+//
+// Up to 32 rows and 96 K-groups (I <= 12288) a workgroup runs 8 wavefronts of
+// at most 12 K-groups each, with rings of 4 (16 rows) or 3 (32 rows) slots;
+// otherwise 4 wavefronts of at most 32. The same bytes are in flight per CU
+// either way, and the 8-wavefront form streams faster: at H = 4096,
+// I = 12288 the whole FFN step took 37.75 against 38.56 us at 32 rows and
+// 33.80 against 34.66 us at one row.
+constexpr int kDnSplit = 4;     // wavefronts (K parts) per workgroup (the general case)
+constexpr int kDnMaxNkbW = 32;  // ... and their K-groups each, at most (scales staged in LDS)
 
-template <int MT>
+// SPLIT wavefronts of NKW K-groups each, at most; the ring as deep as the LDS allows
+template <int MT, int SPLIT, int NKW>
 struct DnCfg {
   static constexpr int RA = MT * 16;        // activation rows in a slot (padded)
   static constexpr int kA = RA * 128;       // activation bytes per slot
   static constexpr int kSlot = kA + 2048;
   static constexpr int AI = RA / 8;         // 1 KB copies of activations per slot
   static constexpr int PER = AI + 2;        // copies per slot (activations + the two weight halves)
-  static constexpr int D = MT == 1 ? 8 : (MT == 2 ? 5 : (MT == 3 ? 4 : 3));  // ring depth that fits the LDS
+  static constexpr int kFree = 163840 - SPLIT * NKW * (RA + 1) * 4;
+  static constexpr int D0 = kFree / (SPLIT * kSlot);
+  static constexpr int D = D0 > 8 ? 8 : D0;  // ring depth that fits the LDS
+  static_assert(D >= 2, "ring depth");
 };
 
-template <int MT>
-__global__ __launch_bounds__(kDnSplit * 64) void skinny_down_kernel(
+template <int MT, int SPLIT, int NKW>
+__global__ __launch_bounds__(SPLIT * 64) void skinny_down_kernel(
     const uint8_t* __restrict__ aq, const float* __restrict__ as,  // h codes [M x K], scales [K/128 x M]
     const uint8_t* __restrict__ wq, const float* __restrict__ ws,  // W_down codes (tile layout), scales [N/128 x K/128]
     uint16_t* __restrict__ out, float* __restrict__ out_tap, int64_t M, int64_t K, int64_t N) {
-  using C = DnCfg<MT>;
+  using C = DnCfg<MT, SPLIT, NKW>;
   constexpr int D = C::D, RA = C::RA;
-  __shared__ __align__(16) uint8_t ring[kDnSplit][D * C::kSlot];
-  __shared__ __align__(16) float sXs[kDnSplit][kDnMaxNkbW * RA];
-  __shared__ float sWs[kDnSplit][kDnMaxNkbW];
+  __shared__ __align__(16) uint8_t ring[SPLIT][D * C::kSlot];
+  __shared__ __align__(16) float sXs[SPLIT][NKW * RA];
+  __shared__ float sWs[SPLIT][NKW];
 
   const int t = threadIdx.x, lane = t & 63;
   const int wave = wave_uniform(t >> 6);
   const int q = lane >> 4, lr = lane & 15;
   const int64_t KB = K / 128;
   const int64_t n0 = static_cast<int64_t>(blockIdx.x) * 16;
-  const int64_t kb0 = wave * KB / kDnSplit, kb1 = (wave + 1) * KB / kDnSplit;
+  const int64_t kb0 = wave * KB / SPLIT, kb1 = (wave + 1) * KB / SPLIT;
   const int nkb = static_cast<int>(kb1 - kb0);  // 0 when K has fewer groups than wavefronts
   uint8_t* my = ring[wave];
 
@@ -349,7 +361,7 @@ __global__ __launch_bounds__(kDnSplit * 64) void skinny_down_kernel(
 
   // ---- this wavefront's scales, staged in LDS (loaded after the first copies)
   {
-    constexpr int XPT = kDnMaxNkbW * RA / 64;
+    constexpr int XPT = NKW * RA / 64;
     float xv[XPT];
 #pragma unroll
     for (int j = 0; j < XPT; ++j) {
@@ -403,11 +415,11 @@ __global__ __launch_bounds__(kDnSplit * 64) void skinny_down_kernel(
 #pragma unroll
     for (int r = 0; r < 4; ++r) red[(wave * RA + 16 * i + 4 * q + r) * 16 + lr] = acc[i][r];
   __syncthreads();
-  for (int e = t; e < M * 16; e += kDnSplit * 64) {
+  for (int e = t; e < M * 16; e += SPLIT * 64) {
     const int row = e >> 4, col = e & 15;
     float sum = red[row * 16 + col];
 #pragma unroll
-    for (int w = 1; w < kDnSplit; ++w) sum += red[(w * RA + row) * 16 + col];
+    for (int w = 1; w < SPLIT; ++w) sum += red[(w * RA + row) * 16 + col];
     out[row * N + n0 + col] = static_cast<uint16_t>(f32_to_bf16(sum));
     if (out_tap != nullptr) out_tap[row * N + n0 + col] = sum;
   }
@@ -555,14 +567,28 @@ hipError_t launch_quant_groups_f32(hipStream_t st, const float* v, uint8_t* code
 hipError_t launch_down_skinny(hipStream_t st, const uint8_t* hq, const float* hs, const uint8_t* wq, const float* ws,
                               uint16_t* out, float* out_tap, int64_t M, int64_t H, int64_t I) {
   const dim3 grid(static_cast<unsigned>(H / 16)), block(kDnSplit * 64);
-  if (M <= 16)
-    hipLaunchKernelGGL(skinny_down_kernel<1>, grid, block, 0, st, hq, hs, wq, ws, out, out_tap, M, I, H);
-  else if (M <= 32)
-    hipLaunchKernelGGL(skinny_down_kernel<2>, grid, block, 0, st, hq, hs, wq, ws, out, out_tap, M, I, H);
-  else if (M <= 48)
-    hipLaunchKernelGGL(skinny_down_kernel<3>, grid, block, 0, st, hq, hs, wq, ws, out, out_tap, M, I, H);
-  else
-    hipLaunchKernelGGL(skinny_down_kernel<4>, grid, block, 0, st, hq, hs, wq, ws, out, out_tap, M, I, H);
+  // up to 32 rows and I <= 12288: 8 wavefronts of at most 12 K-groups each
+  const bool wide = M <= 32 && I / 128 <= 8 * 12;
+  const dim3 block8(8 * 64);
+  if (M <= 16) {
+    if (wide)
+      hipLaunchKernelGGL((skinny_down_kernel<1, 8, 12>), grid, block8, 0, st, hq, hs, wq, ws, out, out_tap, M, I, H);
+    else
+      hipLaunchKernelGGL((skinny_down_kernel<1, kDnSplit, kDnMaxNkbW>), grid, block, 0, st, hq, hs, wq, ws, out, out_tap,
+                         M, I, H);
+  } else if (M <= 32) {
+    if (wide)
+      hipLaunchKernelGGL((skinny_down_kernel<2, 8, 12>), grid, block8, 0, st, hq, hs, wq, ws, out, out_tap, M, I, H);
+    else
+      hipLaunchKernelGGL((skinny_down_kernel<2, kDnSplit, kDnMaxNkbW>), grid, block, 0, st, hq, hs, wq, ws, out, out_tap,
+                         M, I, H);
+  } else if (M <= 48) {
+    hipLaunchKernelGGL((skinny_down_kernel<3, kDnSplit, kDnMaxNkbW>), grid, block, 0, st, hq, hs, wq, ws, out, out_tap, M,
+                       I, H);
+  } else {
+    hipLaunchKernelGGL((skinny_down_kernel<4, kDnSplit, kDnMaxNkbW>), grid, block, 0, st, hq, hs, wq, ws, out, out_tap, M,
+                       I, H);
+  }
   return hipGetLastError();
 }
 

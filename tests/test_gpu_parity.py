@@ -404,14 +404,17 @@ def test_zero_rows_and_zero_blocks(policy):
 
 @pytest.mark.parametrize("M,H,I", [(5, 256, 384), (32, 640, 1152), (16, 8192, 256), (32, 4096, 384),
                                    (17, 1152, 2304), (3, 128, 256), (2, 256, 128), (33, 512, 384),
-                                   (48, 4096, 384), (64, 1152, 256), (64, 4096, 128)])
+                                   (48, 4096, 384), (64, 1152, 256), (64, 4096, 128), (9, 256, 16384),
+                                   (32, 384, 12416)])
 def test_skinny_k_parts(M, H, I):
     """Skinny kernels at K ranges that split unevenly over their K parts: fewer
     K-groups than parts (H = 256, I = 384; a single K-group at H = 128), a part
     one group longer than the others (H = 640), the longest K the gate/up
     kernel's LDS holds (H = 8192 at M = 16; 4096 at M = 32), I = 128 (8 slab
-    pairs: the last workgroup has an idle pair), and 33..64 rows, where the
-    gate/up workgroups take one half of K each (odd K-group counts: H = 1152)."""
+    pairs: the last workgroup has an idle pair), 33..64 rows, where the
+    gate/up workgroups take one half of K each (odd K-group counts: H = 1152),
+    and down K ranges past the 8-part kernel's 96 K-groups at up to 32 rows
+    (I = 16384, and 12416: 97 groups over 4 parts)."""
     _say("skinny M=%d H=%d I=%d" % (M, H, I))
     lc.lacache_set_path_policy(1)
     w = synth.Workload(91, "kparts", M, H, I, act="outlier", outlier_ratio=0.02)
