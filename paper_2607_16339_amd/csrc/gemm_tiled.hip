@@ -32,6 +32,7 @@
 // row amax over the 128-wide h-group meets in LDS across the wavefronts of a
 // row band. h never reaches memory.
 #include <atomic>
+#include <type_traits>
 
 #include "device.h"
 #include "launch.h"
@@ -131,305 +132,317 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
   const int C = static_cast<int>(kGateUp ? I / 128 : (N + BNR - 1) / BNR);
   const int G = static_cast<int>(gridDim.x);
 
-  // ---- direct-to-LDS copy plan. Only the first kCopyWaves wavefronts (one
-  // per SIMD) copy: a wavefront stalls while the memory pipeline takes its
-  // copy instructions, and the other wavefront of its SIMD keeps the matrix
-  // core busy meanwhile (all eight copying at once left it idle). A copy
-  // instruction fills 64 consecutive 16-byte LDS slots (8 tile rows); lane l
-  // fills slot l, i.e. row 8g + l/8, physical chunk l%8, so it fetches logical
-  // chunk (l%8) ^ swz(row) of that row. Rows past M (or N) fetch a clamped
-  // row; their results are never stored. Scales: each copy wavefront copies
-  // the activation scales of rows 64 (w mod BM/64) .. + 63 (one float per
-  // lane; copies beyond the first go to the spare slots) and the two
-  // weight-block scales (lane 0 the first block, the others the second).
   constexpr int kCopyWaves = 4;
-  constexpr int kAInst = BM / 8 / kCopyWaves;  // per copy wavefront
-  constexpr int kBInst = BNR / 8 / kCopyWaves;
-  constexpr int kPer = kAInst + kBInst + 2;  // copies per copy wavefront per K-group
-  const bool copy_wave = wave < kCopyWaves;
-  const int xband = wave % (BM / 64);
-  const int xs_dst = wave < BM / 64 ? wave * 64 : BM + 64;
 
-  // issue cursor: the item whose K-groups are being copied
-  int iw = blockIdx.x, ikb = 0, ikb1 = 0;
-  const uint8_t* a_base = aq;
-  const uint8_t* b_base = bq;
-  const uint8_t* b_base_hi = bq;
-  const float* x_base = as;  // activation scales of the tile's rows (wave-uniform)
-  uint32_t x_off = 0;        // ... this lane's byte offset (stride M floats per K-group)
-  uint32_t w_off = 0;        // this lane's weight-block scale row, as a byte offset into bs
-  uint32_t a_off[kAInst], b_off[kBInst];
-  auto enter = [&](int w) {
-    const Item it = item_at(w, R, C, KS, KB, BM);
-    ikb = it.kb0;
-    ikb1 = it.kb1;
-    a_base = aq + static_cast<int64_t>(it.m0) * K;
-    const int alim = static_cast<int>(M) - 1 - it.m0;  // last valid row of the tile
-#pragma unroll
-    for (int u = 0; u < kAInst; ++u) {
-      const int row = (wave * kAInst + u) * 8 + (lane >> 3);
-      const int r = row < alim ? row : alim;
-      a_off[u] = static_cast<uint32_t>(r) * static_cast<uint32_t>(K) + ((lane & 7) ^ swz(row)) * 16;
-    }
-    // gate/up: tile rows 0..127 come from the gate block, 128..255 from the up
-    // block (base b_base_hi); down: one contiguous 256-row block
-    const int n0 = kGateUp ? 0 : it.col * BNR;
-    const int blim = kGateUp ? BNR : static_cast<int>(N) - 1 - n0;
-    b_base = kGateUp ? bq + static_cast<int64_t>(it.col) * 128 * K : bq + static_cast<int64_t>(n0) * K;
-    b_base_hi = kGateUp ? bq + (I + static_cast<int64_t>(it.col) * 128 - 128) * K : b_base;
-    // (weights in the tile layout of wtile_off: the slab bases above are the
-    // same as row-major, the offsets within and the K-group step are not)
-#pragma unroll
-    for (int u = 0; u < kBInst; ++u) {
-      const int row = (wave * kBInst + u) * 8 + (lane >> 3);
-      const int r = row < blim ? row : blim;
-      b_off[u] = static_cast<uint32_t>(wtile_off(r, ((lane & 7) ^ swz(row)) * 16, K));
-    }
-    {
-      const int row = xband * 64 + lane;
-      x_base = as + it.m0;
-      x_off = static_cast<uint32_t>(row < alim ? row : alim) * 4u;
-      // gate/up: {gate block, up block}; down: {block of columns n0.., the next
-      // one (or the same past N)}
-      const int r0 = kGateUp ? it.col : n0 / 128;
-      const int r1 = kGateUp ? static_cast<int>(I / 128) + it.col : (n0 + 128 < N ? n0 / 128 + 1 : r0);
-      w_off = static_cast<uint32_t>((lane == 0 ? r0 : r1) * KB) * 4u;
-    }
-  };
-  // Copies of K-group kb of the cursor's item into stage dst (asynchronous).
-  auto issue_group = [&](int kb, Stage<BM>* dst) {
-    if (!copy_wave) return;
-    const int64_t ko = static_cast<int64_t>(kb) * 128;
-    const int la = static_cast<int>(lds_u32(dst->a)), lb = static_cast<int>(lds_u32(dst->b));
-#pragma unroll
-    for (int u = 0; u < kAInst; ++u) dma16s(a_base + ko, a_off[u], wave_uniform(la + (wave * kAInst + u) * 1024));
-#pragma unroll
-    for (int u = 0; u < kBInst; ++u) {
-      const uint8_t* base = (kGateUp && (wave * kBInst + u) * 8 >= 128) ? b_base_hi : b_base;
-      dma16s(base + ko * 16, b_off[u], wave_uniform(lb + (wave * kBInst + u) * 1024));
-    }
-    const int lx = static_cast<int>(lds_u32(dst->xs));
-    dma4s(x_base + static_cast<int64_t>(kb) * M, x_off, wave_uniform(lx + xs_dst * 4));
-    dma4s(bs + kb, w_off, wave_uniform(lx + BM * 4));
-  };
-  // The next K-group in the workgroup's sequence. Past the last one the last
-  // group is copied again into the idle stage (never read), so every step
-  // waits for the same count.
-  auto issue_next = [&](Stage<BM>* dst) {
-    issue_group(ikb < ikb1 ? ikb : ikb1 - 1, dst);
-    if (ikb < ikb1 && ++ikb == ikb1 && iw + G < W) {
-      iw += G;
-      enter(iw);
-    }
-  };
+  // The copy wavefronts and the others run the same stream as two instances
+  // of one loop: only the copy wavefronts' instance holds the copy cursor
+  // (item, K-group, per-lane offsets) and issues the copies, so the other
+  // wavefronts spend neither instructions nor registers on it.
+  auto run = [&](auto copy_tag) {
+    constexpr bool kCopy = decltype(copy_tag)::value;
+    // ---- direct-to-LDS copy plan. Only the first kCopyWaves wavefronts (one
+    // per SIMD) copy: a wavefront stalls while the memory pipeline takes its
+    // copy instructions, and the other wavefront of its SIMD keeps the matrix
+    // core busy meanwhile (all eight copying at once left it idle). A copy
+    // instruction fills 64 consecutive 16-byte LDS slots (8 tile rows); lane l
+    // fills slot l, i.e. row 8g + l/8, physical chunk l%8, so it fetches logical
+    // chunk (l%8) ^ swz(row) of that row. Rows past M (or N) fetch a clamped
+    // row; their results are never stored. Scales: each copy wavefront copies
+    // the activation scales of rows 64 (w mod BM/64) .. + 63 (one float per
+    // lane; copies beyond the first go to the spare slots) and the two
+    // weight-block scales (lane 0 the first block, the others the second).
+    constexpr int kAInst = BM / 8 / kCopyWaves;  // per copy wavefront
+    constexpr int kBInst = BNR / 8 / kCopyWaves;
+    constexpr int kPer = kAInst + kBInst + 2;  // copies per copy wavefront per K-group
+    const int xband = wave % (BM / 64);
+    const int xs_dst = wave < BM / 64 ? wave * 64 : BM + 64;
 
-  float acc[4][NJ][4];
-
-  // Multiplies the K-group in stage cur into acc.
-  auto compute = [&](const Stage<BM>* cur) {
-    auto brow = [&](int j) {
-      return kGateUp ? (j < NJ / 2 ? (WC / 2) * wn + 16 * j : 128 + (WC / 2) * wn + 16 * (j - NJ / 2)) : WC * wn + 16 * j;
-    };
-    // Every LDS read the first MFMAs and FMAs need is issued up front, in the
-    // order they are needed (LDS reads complete in order): the first B slab,
-    // the scales, then the four A slabs. MFMA i waits only for its own
-    // operands, and the scale products are formed after MFMA 1, when the
-    // first FMAs need them, instead of holding MFMA 0 back by a round trip.
-    v8i bb[2];
-    bb[0] = load_frag(cur->b, brow(0) + lr, q);
-    __builtin_amdgcn_sched_barrier(0);
-    float xv[4];
+    // issue cursor: the item whose K-groups are being copied
+    int iw = blockIdx.x, ikb = 0, ikb1 = 0;
+    const uint8_t* a_base = aq;
+    const uint8_t* b_base = bq;
+    const uint8_t* b_base_hi = bq;
+    const float* x_base = as;  // activation scales of the tile's rows (wave-uniform)
+    uint32_t x_off = 0;        // ... this lane's byte offset (stride M floats per K-group)
+    uint32_t w_off = 0;        // this lane's weight-block scale row, as a byte offset into bs
+    uint32_t a_off[kCopy ? kAInst : 1], b_off[kCopy ? kBInst : 1];
+    auto enter = [&](int w) {
+      const Item it = item_at(w, R, C, KS, KB, BM);
+      ikb = it.kb0;
+      ikb1 = it.kb1;
+      a_base = aq + static_cast<int64_t>(it.m0) * K;
+      const int alim = static_cast<int>(M) - 1 - it.m0;  // last valid row of the tile
 #pragma unroll
-    for (int i = 0; i < 4; ++i) xv[i] = cur->xs[64 * wm + 16 * i + lr];
-    // gate/up: slabs 0..NJ/2-1 are gate rows (block scale in slot BM), the
-    // rest the matching up rows (slot BM + 1); down: the wave's columns lie in
-    // one block, slot BM + (WC wn) / 128
-    const float w0 = cur->xs[BM + (kGateUp ? 0 : (WC * wn) / 128)];
-    const float w1 = cur->xs[BM + 1];
-    __builtin_amdgcn_sched_barrier(0);
-    v8i af[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) af[i] = load_frag(cur->a, 64 * wm + 16 * i + lr, q);
-    __builtin_amdgcn_sched_barrier(0);
-    float sc[kGateUp ? 2 : 1][4];  // RN32(x_scale * w_scale) of this lane's row
-    // Software pipeline over the 4 NJ sub-tiles s = 4 j + i: MFMA s, then the
-    // scale FMAs of MFMA s - 2; the B operand of slab j + 1 is read while slab
-    // j multiplies.
-    v4f pr[3];
-#pragma unroll
-    for (int s = 0; s < 4 * NJ; ++s) {
-      const int j = s >> 2, i = s & 3;
-      if (i == 0 && j < NJ - 1) bb[(j + 1) & 1] = load_frag(cur->b, brow(j + 1) + lr, q);
-      const v4f zero = {0.0f, 0.0f, 0.0f, 0.0f};
-      pr[s % 3] = mfma_fp8_16x16x128(bb[j & 1], af[i], zero);
-      // keep MFMA s ahead of the FMAs below: they read a result two MFMAs
-      // old, so they neither wait for the matrix core nor delay the next MFMA
-      __builtin_amdgcn_sched_barrier(0);
-      if (s == 1) {
-#pragma unroll
-        for (int i2 = 0; i2 < 4; ++i2) {
-          sc[0][i2] = xv[i2] * w0;
-          if (kGateUp) sc[kGateUp ? 1 : 0][i2] = xv[i2] * w1;
-        }
+      for (int u = 0; u < (kCopy ? kAInst : 0); ++u) {
+        const int row = (wave * kAInst + u) * 8 + (lane >> 3);
+        const int r = row < alim ? row : alim;
+        a_off[u] = static_cast<uint32_t>(r) * static_cast<uint32_t>(K) + ((lane & 7) ^ swz(row)) * 16;
       }
-      if (s >= 2) {
-        const int ps = s - 2;
-        const int blk = (kGateUp && (ps >> 2) >= NJ / 2) ? 1 : 0;
+      // gate/up: tile rows 0..127 come from the gate block, 128..255 from the up
+      // block (base b_base_hi); down: one contiguous 256-row block
+      const int n0 = kGateUp ? 0 : it.col * BNR;
+      const int blim = kGateUp ? BNR : static_cast<int>(N) - 1 - n0;
+      b_base = kGateUp ? bq + static_cast<int64_t>(it.col) * 128 * K : bq + static_cast<int64_t>(n0) * K;
+      b_base_hi = kGateUp ? bq + (I + static_cast<int64_t>(it.col) * 128 - 128) * K : b_base;
+      // (weights in the tile layout of wtile_off: the slab bases above are the
+      // same as row-major, the offsets within and the K-group step are not)
+#pragma unroll
+      for (int u = 0; u < (kCopy ? kBInst : 0); ++u) {
+        const int row = (wave * kBInst + u) * 8 + (lane >> 3);
+        const int r = row < blim ? row : blim;
+        b_off[u] = static_cast<uint32_t>(wtile_off(r, ((lane & 7) ^ swz(row)) * 16, K));
+      }
+      {
+        const int row = xband * 64 + lane;
+        x_base = as + it.m0;
+        x_off = static_cast<uint32_t>(row < alim ? row : alim) * 4u;
+        // gate/up: {gate block, up block}; down: {block of columns n0.., the next
+        // one (or the same past N)}
+        const int r0 = kGateUp ? it.col : n0 / 128;
+        const int r1 = kGateUp ? static_cast<int>(I / 128) + it.col : (n0 + 128 < N ? n0 / 128 + 1 : r0);
+        w_off = static_cast<uint32_t>((lane == 0 ? r0 : r1) * KB) * 4u;
+      }
+    };
+    // Copies of K-group kb of the cursor's item into stage dst (asynchronous).
+    auto issue_group = [&](int kb, Stage<BM>* dst) {
+      const int64_t ko = static_cast<int64_t>(kb) * 128;
+      const int la = static_cast<int>(lds_u32(dst->a)), lb = static_cast<int>(lds_u32(dst->b));
+#pragma unroll
+      for (int u = 0; u < (kCopy ? kAInst : 0); ++u) dma16s(a_base + ko, a_off[u], wave_uniform(la + (wave * kAInst + u) * 1024));
+#pragma unroll
+      for (int u = 0; u < (kCopy ? kBInst : 0); ++u) {
+        const uint8_t* base = (kGateUp && (wave * kBInst + u) * 8 >= 128) ? b_base_hi : b_base;
+        dma16s(base + ko * 16, b_off[u], wave_uniform(lb + (wave * kBInst + u) * 1024));
+      }
+      const int lx = static_cast<int>(lds_u32(dst->xs));
+      dma4s(x_base + static_cast<int64_t>(kb) * M, x_off, wave_uniform(lx + xs_dst * 4));
+      dma4s(bs + kb, w_off, wave_uniform(lx + BM * 4));
+    };
+    // The next K-group in the workgroup's sequence. Past the last one the last
+    // group is copied again into the idle stage (never read), so every step
+    // waits for the same count.
+    auto issue_next = [&](Stage<BM>* dst) {
+      issue_group(ikb < ikb1 ? ikb : ikb1 - 1, dst);
+      if (ikb < ikb1 && ++ikb == ikb1 && iw + G < W) {
+        iw += G;
+        enter(iw);
+      }
+    };
+
+    float acc[4][NJ][4];
+
+    // Multiplies the K-group in stage cur into acc.
+    auto compute = [&](const Stage<BM>* cur) {
+      auto brow = [&](int j) {
+        return kGateUp ? (j < NJ / 2 ? (WC / 2) * wn + 16 * j : 128 + (WC / 2) * wn + 16 * (j - NJ / 2)) : WC * wn + 16 * j;
+      };
+      // Every LDS read the first MFMAs and FMAs need is issued up front, in the
+      // order they are needed (LDS reads complete in order): the first B slab,
+      // the scales, then the four A slabs. MFMA i waits only for its own
+      // operands, and the scale products are formed after MFMA 1, when the
+      // first FMAs need them, instead of holding MFMA 0 back by a round trip.
+      v8i bb[2];
+      bb[0] = load_frag(cur->b, brow(0) + lr, q);
+      __builtin_amdgcn_sched_barrier(0);
+      float xv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) xv[i] = cur->xs[64 * wm + 16 * i + lr];
+      // gate/up: slabs 0..NJ/2-1 are gate rows (block scale in slot BM), the
+      // rest the matching up rows (slot BM + 1); down: the wave's columns lie in
+      // one block, slot BM + (WC wn) / 128
+      const float w0 = cur->xs[BM + (kGateUp ? 0 : (WC * wn) / 128)];
+      const float w1 = cur->xs[BM + 1];
+      __builtin_amdgcn_sched_barrier(0);
+      v8i af[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) af[i] = load_frag(cur->a, 64 * wm + 16 * i + lr, q);
+      __builtin_amdgcn_sched_barrier(0);
+      float sc[kGateUp ? 2 : 1][4];  // RN32(x_scale * w_scale) of this lane's row
+      // Software pipeline over the 4 NJ sub-tiles s = 4 j + i: MFMA s, then the
+      // scale FMAs of MFMA s - 2; the B operand of slab j + 1 is read while slab
+      // j multiplies.
+      v4f pr[3];
+#pragma unroll
+      for (int s = 0; s < 4 * NJ; ++s) {
+        const int j = s >> 2, i = s & 3;
+        if (i == 0 && j < NJ - 1) bb[(j + 1) & 1] = load_frag(cur->b, brow(j + 1) + lr, q);
+        const v4f zero = {0.0f, 0.0f, 0.0f, 0.0f};
+        pr[s % 3] = mfma_fp8_16x16x128(bb[j & 1], af[i], zero);
+        // keep MFMA s ahead of the FMAs below: they read a result two MFMAs
+        // old, so they neither wait for the matrix core nor delay the next MFMA
+        __builtin_amdgcn_sched_barrier(0);
+        if (s == 1) {
+#pragma unroll
+          for (int i2 = 0; i2 < 4; ++i2) {
+            sc[0][i2] = xv[i2] * w0;
+            if (kGateUp) sc[kGateUp ? 1 : 0][i2] = xv[i2] * w1;
+          }
+        }
+        if (s >= 2) {
+          const int ps = s - 2;
+          const int blk = (kGateUp && (ps >> 2) >= NJ / 2) ? 1 : 0;
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            acc[ps & 3][ps >> 2][r] = __builtin_fmaf(pr[ps % 3][r], sc[blk][ps & 3], acc[ps & 3][ps >> 2][r]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+#pragma unroll
+      for (int ps = 4 * NJ - 2; ps < 4 * NJ; ++ps)
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          acc[ps & 3][ps >> 2][r] = __builtin_fmaf(pr[ps % 3][r], sc[blk][ps & 3], acc[ps & 3][ps >> 2][r]);
-      }
-      __builtin_amdgcn_sched_barrier(0);
+          acc[ps & 3][ps >> 2][r] = __builtin_fmaf(pr[ps % 3][r], sc[kGateUp ? 1 : 0][ps & 3], acc[ps & 3][ps >> 2][r]);
+    };
+
+    // ---- the stream: S - 1 K-groups ahead of the multiply, across items
+    if (kCopy) {
+      enter(iw);
+#pragma unroll
+      for (int s = 0; s < S - 1; ++s) issue_next(&stg[s]);
     }
-#pragma unroll
-    for (int ps = 4 * NJ - 2; ps < 4 * NJ; ++ps)
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        acc[ps & 3][ps >> 2][r] = __builtin_fmaf(pr[ps % 3][r], sc[kGateUp ? 1 : 0][ps & 3], acc[ps & 3][ps >> 2][r]);
-  };
+    int cur = 0;  // stage of the K-group being multiplied
 
-  // ---- the stream: S - 1 K-groups ahead of the multiply, across items
-  enter(iw);
+    for (int w = blockIdx.x; w < W; w += G) {
+      const Item it = item_at(w, R, C, KS, KB, BM);
 #pragma unroll
-  for (int s = 0; s < S - 1; ++s) issue_next(&stg[s]);
-  int cur = 0;  // stage of the K-group being multiplied
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) acc[i][j][r] = 0.0f;
 
-  for (int w = blockIdx.x; w < W; w += G) {
-    const Item it = item_at(w, R, C, KS, KB, BM);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < NJ; ++j)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) acc[i][j][r] = 0.0f;
+      for (int kb = it.kb0; kb < it.kb1; ++kb) {
+        // a copy wave's copies of the group have landed (later ones may still
+        // fly; loads retire in issue order, so epilogue stores in between only
+        // make the wait longer) ...
+        if (kCopy)
+          wait_vm_lds<(S - 2) * kPer>();
+        else
+          wait_lds();
+        bar();  // ... and every wave's; and the stage of the previous group is read by no one
+        if (kCopy) issue_next(&stg[cur == 0 ? S - 1 : cur - 1]);  // into the stage freed by the previous group
+        compute(&stg[cur]);
+        cur = cur + 1 == S ? 0 : cur + 1;
+      }
 
-    for (int kb = it.kb0; kb < it.kb1; ++kb) {
-      // a copy wave's copies of the group have landed (later ones may still
-      // fly; loads retire in issue order, so epilogue stores in between only
-      // make the wait longer) ...
-      if (copy_wave)
-        wait_vm_lds<(S - 2) * kPer>();
-      else
-        wait_lds();
-      bar();  // ... and every wave's; and the stage of the previous group is read by no one
-      issue_next(&stg[cur == 0 ? S - 1 : cur - 1]);  // into the stage freed by the previous group
-      compute(&stg[cur]);
-      cur = cur + 1 == S ? 0 : cur + 1;
-    }
-
-    if (col_s != nullptr) {
-      // per-channel weight scales: output column n times col_s[n]
-#pragma unroll
-      for (int j = 0; j < NJ; ++j) {
-        const int64_t n = kGateUp ? (j < NJ / 2 ? 0 : I) + static_cast<int64_t>(it.col) * 128 + (WC / 2) * wn +
-                                        16 * (j < NJ / 2 ? j : j - NJ / 2) + 4 * q
-                                  : static_cast<int64_t>(it.col) * BNR + WC * wn + 16 * j + 4 * q;
-        const float4 cs = (kGateUp || n < N) ? *reinterpret_cast<const float4*>(col_s + n) : make_float4(0, 0, 0, 0);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          acc[i][j][0] *= cs.x;
-          acc[i][j][1] *= cs.y;
-          acc[i][j][2] *= cs.z;
-          acc[i][j][3] *= cs.w;
-        }
-      }
-    }
-    if (kGateUp) {
-      // ---- SwiGLU: h = SiLU(g) * u; lanes hold matching gate (j) and up
-      // (j + NJ/2) values; h replaces g in acc
-      float am[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float a = 0.0f;
-#pragma unroll
-        for (int j = 0; j < NJ / 2; ++j)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float v = swiglu_fast(acc[i][j][r], acc[i][j + NJ / 2][r]);
-            acc[i][j][r] = v;
-            a = __builtin_fmaxf(a, __builtin_fabsf(v));
-          }
-        // over the four lanes that hold the row's other columns
-        a = __builtin_fmaxf(a, __shfl_xor(a, 16, 64));
-        a = __builtin_fmaxf(a, __shfl_xor(a, 32, 64));
-        am[i] = a;
-      }
-      if (q == 0) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) sRed[wn][64 * wm + 16 * i + lr] = am[i];
-      }
-      wait_lds();
-      bar();  // the row amax of every wavefront of the band is in LDS
-      // ---- 1x128 quantization of each row's h-group (without hq: h only)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        if (hq == nullptr) {
-          const int64_t grow = static_cast<int64_t>(it.m0) + 64 * wm + 16 * i + lr;
-          if (grow < M) {
-#pragma unroll
-            for (int j = 0; j < NJ / 2; ++j)
-              *reinterpret_cast<float4*>(h_tap + grow * I + static_cast<int64_t>(it.col) * 128 + (WC / 2) * wn +
-                                         16 * j + 4 * q) =
-                  make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
-          }
-          continue;
-        }
-        const int row = 64 * wm + 16 * i + lr;
-        const int64_t grow = static_cast<int64_t>(it.m0) + row;
-        float amax = sRed[0][row];
-#pragma unroll
-        for (int c = 1; c < NCW; ++c) amax = __builtin_fmaxf(amax, sRed[c][row]);
-        const float s = amax / kE4M3Max;
-        const FastQuant fq = fast_quant(s);
-        const bool fast = scale_is_fast(s);
-        const bool ok = grow < M;
-#pragma unroll
-        for (int j = 0; j < NJ / 2; ++j) {
-          // E(RN32(h / s)) by the bracket where it decides, else by the division
-          uint32_t code;
-          const bool agree = enc4_bracket(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3], fq, code);
-          if (s == 0.0f)
-            code = 0u;
-          else if (!(fast && agree))
-            code = enc4_e4m3(qdiv(acc[i][j][0], s), qdiv(acc[i][j][1], s), qdiv(acc[i][j][2], s),
-                             qdiv(acc[i][j][3], s));
-          const int64_t col = static_cast<int64_t>(it.col) * 128 + (WC / 2) * wn + 16 * j + 4 * q;
-          if (ok) {
-            *reinterpret_cast<uint32_t*>(hq + grow * I + col) = code;
-            if (h_tap != nullptr)
-              *reinterpret_cast<float4*>(h_tap + grow * I + col) =
-                  make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
-          }
-        }
-        if (wn == 0 && q == 0 && ok) hs[it.col * M + grow] = s;
-      }
-    } else {
-      // ---- bf16 output (nearest-even from the fp32 accumulator), or the fp32
-      // partial sum of this K split
-      const int64_t n0 = static_cast<int64_t>(it.col) * BNR;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int64_t row = static_cast<int64_t>(it.m0) + 64 * wm + 16 * i + lr;
-        if (row >= M) continue;
+      if (col_s != nullptr) {
+        // per-channel weight scales: output column n times col_s[n]
 #pragma unroll
         for (int j = 0; j < NJ; ++j) {
-          const int64_t col = n0 + WC * wn + 16 * j + 4 * q;
-          if (col >= N) continue;
-          if (KS > 1) {
-            *reinterpret_cast<float4*>(part + (it.split * M + row) * N + col) =
-                make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
-          } else {
-            *reinterpret_cast<uint2*>(out + row * N + col) =
-                make_uint2(pack_bf16x2(acc[i][j][0], acc[i][j][1]), pack_bf16x2(acc[i][j][2], acc[i][j][3]));
-            if (out_tap != nullptr)
-              *reinterpret_cast<float4*>(out_tap + row * N + col) =
+          const int64_t n = kGateUp ? (j < NJ / 2 ? 0 : I) + static_cast<int64_t>(it.col) * 128 + (WC / 2) * wn +
+                                          16 * (j < NJ / 2 ? j : j - NJ / 2) + 4 * q
+                                    : static_cast<int64_t>(it.col) * BNR + WC * wn + 16 * j + 4 * q;
+          const float4 cs = (kGateUp || n < N) ? *reinterpret_cast<const float4*>(col_s + n) : make_float4(0, 0, 0, 0);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            acc[i][j][0] *= cs.x;
+            acc[i][j][1] *= cs.y;
+            acc[i][j][2] *= cs.z;
+            acc[i][j][3] *= cs.w;
+          }
+        }
+      }
+      if (kGateUp) {
+        // ---- SwiGLU: h = SiLU(g) * u; lanes hold matching gate (j) and up
+        // (j + NJ/2) values; h replaces g in acc
+        float am[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float a = 0.0f;
+#pragma unroll
+          for (int j = 0; j < NJ / 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const float v = swiglu_fast(acc[i][j][r], acc[i][j + NJ / 2][r]);
+              acc[i][j][r] = v;
+              a = __builtin_fmaxf(a, __builtin_fabsf(v));
+            }
+          // over the four lanes that hold the row's other columns
+          a = __builtin_fmaxf(a, __shfl_xor(a, 16, 64));
+          a = __builtin_fmaxf(a, __shfl_xor(a, 32, 64));
+          am[i] = a;
+        }
+        if (q == 0) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) sRed[wn][64 * wm + 16 * i + lr] = am[i];
+        }
+        wait_lds();
+        bar();  // the row amax of every wavefront of the band is in LDS
+        // ---- 1x128 quantization of each row's h-group (without hq: h only)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if (hq == nullptr) {
+            const int64_t grow = static_cast<int64_t>(it.m0) + 64 * wm + 16 * i + lr;
+            if (grow < M) {
+#pragma unroll
+              for (int j = 0; j < NJ / 2; ++j)
+                *reinterpret_cast<float4*>(h_tap + grow * I + static_cast<int64_t>(it.col) * 128 + (WC / 2) * wn +
+                                           16 * j + 4 * q) =
+                    make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+            }
+            continue;
+          }
+          const int row = 64 * wm + 16 * i + lr;
+          const int64_t grow = static_cast<int64_t>(it.m0) + row;
+          float amax = sRed[0][row];
+#pragma unroll
+          for (int c = 1; c < NCW; ++c) amax = __builtin_fmaxf(amax, sRed[c][row]);
+          const float s = amax / kE4M3Max;
+          const FastQuant fq = fast_quant(s);
+          const bool fast = scale_is_fast(s);
+          const bool ok = grow < M;
+#pragma unroll
+          for (int j = 0; j < NJ / 2; ++j) {
+            // E(RN32(h / s)) by the bracket where it decides, else by the division
+            uint32_t code;
+            const bool agree = enc4_bracket(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3], fq, code);
+            if (s == 0.0f)
+              code = 0u;
+            else if (!(fast && agree))
+              code = enc4_e4m3(qdiv(acc[i][j][0], s), qdiv(acc[i][j][1], s), qdiv(acc[i][j][2], s),
+                               qdiv(acc[i][j][3], s));
+            const int64_t col = static_cast<int64_t>(it.col) * 128 + (WC / 2) * wn + 16 * j + 4 * q;
+            if (ok) {
+              *reinterpret_cast<uint32_t*>(hq + grow * I + col) = code;
+              if (h_tap != nullptr)
+                *reinterpret_cast<float4*>(h_tap + grow * I + col) =
+                    make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+            }
+          }
+          if (wn == 0 && q == 0 && ok) hs[it.col * M + grow] = s;
+        }
+      } else {
+        // ---- bf16 output (nearest-even from the fp32 accumulator), or the fp32
+        // partial sum of this K split
+        const int64_t n0 = static_cast<int64_t>(it.col) * BNR;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int64_t row = static_cast<int64_t>(it.m0) + 64 * wm + 16 * i + lr;
+          if (row >= M) continue;
+#pragma unroll
+          for (int j = 0; j < NJ; ++j) {
+            const int64_t col = n0 + WC * wn + 16 * j + 4 * q;
+            if (col >= N) continue;
+            if (KS > 1) {
+              *reinterpret_cast<float4*>(part + (it.split * M + row) * N + col) =
                   make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+            } else {
+              *reinterpret_cast<uint2*>(out + row * N + col) =
+                  make_uint2(pack_bf16x2(acc[i][j][0], acc[i][j][1]), pack_bf16x2(acc[i][j][2], acc[i][j][3]));
+              if (out_tap != nullptr)
+                *reinterpret_cast<float4*>(out_tap + row * N + col) =
+                    make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+            }
           }
         }
       }
     }
-  }
-  wait_vm<0>();  // the trailing repeat copies
+    if (kCopy) wait_vm<0>();  // the trailing repeat copies
+  };
+  if (wave < kCopyWaves)
+    run(std::true_type{});
+  else
+    run(std::false_type{});
 }
 
 // Compute units of the current device (the persistent grid's size), cached
