@@ -571,6 +571,22 @@ def test_tiled_partial_column_tile(M):
     check_down_model(host(t["hq"]), host(t["hs"]), wd_q, wd_s, host(t["out_tap"]))
 
 
+def test_bm256_partial_row_and_column_tiles():
+    """256-row tiles with both tails: M = 12000 at H = 640, I = 1152 takes
+    256-row tiles in both GEMMs (128-row ones would need more rounds of one
+    workgroup per CU), the last row tile holds 224 rows, and the down GEMM's
+    last 256-column tile holds 128 valid columns. Sampled rows, both tails'
+    rows included, against the oracle."""
+    M, H, I = 12000, 640, 1152
+    _say("bm256 partial row and column tiles M=%d H=%d" % (M, H))
+    w = synth.Workload(97, "bm256_tails", M, H, I, act="outlier", outlier_ratio=0.02)
+    lay = Layer(w, layer=1)
+    pick = lambda m: np.unique(np.concatenate([[0, 255, 256, m - 224, m - 2, m - 1],
+                                               np.random.default_rng(11).choice(m, 24, replace=False)]))
+    g, e, d = _full_size_case(lay, w, 0, pick, 0)
+    _say("bm256 tails: gate/up %s; down error %.2e, %.3f of the model tolerance" % (g, e, d))
+
+
 @pytest.mark.parametrize("step", [0, 31])
 def test_stack_layers_with_residual_adds(step):
     """Three consecutive layers of the 31-layer stack (own weights per layer)
