@@ -99,8 +99,8 @@ hipError_t launch_pack_weights(hipStream_t st, const uint8_t* w, uint8_t* wt, in
 // the old row. With kF32Out the normalized row goes to
 // yf (fp32) instead of being quantized (the coarse-granularity paths).
 // ---------------------------------------------------------------------------
-template <int T, bool kF32Out = false>
-__global__ __launch_bounds__(256) void rmsnorm_quant_kernel(uint16_t* x, const uint16_t* __restrict__ y,
+template <int T, bool kF32Out = false, bool kAdd = false>
+__global__ __launch_bounds__(256, T <= 8 && !kAdd ? 4 : 1) void rmsnorm_quant_kernel(uint16_t* x, const uint16_t* __restrict__ y,
                                                             const uint16_t* __restrict__ nw,
                                                             uint8_t* __restrict__ xq, float* __restrict__ xs,
                                                             int64_t M, int H, int wpr_log2, float* __restrict__ yf) {
@@ -118,16 +118,16 @@ __global__ __launch_bounds__(256) void rmsnorm_quant_kernel(uint16_t* x, const u
   // every load of the row and of the norm weight is issued before any is
   // used (clamped indices keep them unconditional), so the wavefront waits
   // for memory once
-  uint4 xv[T], wv[T], yv[T];
+  uint4 xv[T], wv[T], yv[kAdd ? T : 1];
 #pragma unroll
   for (int t = 0; t < T; ++t) {
     const int c = t * 64 + lane;
     const int cc = c < nchunk ? c : nchunk - 1;
     xv[t] = xr[cc];
     wv[t] = wr[cc];
-    if (y != nullptr) yv[t] = reinterpret_cast<const uint4*>(y + row * H)[cc];
+    if constexpr (kAdd) yv[t] = reinterpret_cast<const uint4*>(y + row * H)[cc];
   }
-  if (y != nullptr) {  // the residual add, in registers (written back below)
+  if constexpr (kAdd) {  // the residual add, in registers (written back below)
 #pragma unroll
     for (int t = 0; t < T; ++t) {
       uint32_t* a = reinterpret_cast<uint32_t*>(&xv[t]);
@@ -145,7 +145,7 @@ __global__ __launch_bounds__(256) void rmsnorm_quant_kernel(uint16_t* x, const u
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) p = p + __shfl_xor(p, o, 64);
   const float r = rms_inv(p, H);
-  if (y != nullptr) {
+  if constexpr (kAdd) {
     // every wavefront of the row has used all of the old row (the sum above)
     // before any writes its passes of the new one; the row's wavefronts are
     // one workgroup (wpr_log2 > 0) or a single wavefront
@@ -190,7 +190,15 @@ hipError_t launch_rmsnorm_quant(hipStream_t st, uint16_t* x, const uint16_t* nw,
   const int per_block = wl > 0 ? (1 << wl) : 4;
   dim3 grid(static_cast<unsigned>((waves + per_block - 1) / per_block)), block(64 * per_block);
   const int h = static_cast<int>(H);
-#define NQ(T_) hipLaunchKernelGGL(rmsnorm_quant_kernel<T_>, grid, block, 0, st, x, y, nw, xq, xs, M, h, wl, nullptr)
+#define NQ(T_)                                                                                                    \
+  do {                                                                                                            \
+    if (y != nullptr)                                                                                             \
+      hipLaunchKernelGGL((rmsnorm_quant_kernel<T_, false, true>), grid, block, 0, st, x, y, nw, xq, xs, M, h, wl,  \
+                         nullptr);                                                                                \
+    else                                                                                                          \
+      hipLaunchKernelGGL((rmsnorm_quant_kernel<T_, false, false>), grid, block, 0, st, x, y, nw, xq, xs, M, h, wl, \
+                         nullptr);                                                                                \
+  } while (0)
   if (T <= 1) NQ(1);
   else if (T <= 2) NQ(2);
   else if (T <= 4) NQ(4);
