@@ -283,12 +283,13 @@ def test_rmsnorm_quant_bit_exact(M, H):
     check_norm_exact(xb, wb, host(xq), host(xs))
 
 
-@pytest.mark.parametrize("M,H", [(5, 256), (9, 1024), (17, 2176), (64, 16384), (1030, 512)])
+@pytest.mark.parametrize("M,H", [(5, 256), (9, 1024), (17, 2176), (64, 16384), (1030, 512), (1100, 4096)])
 def test_add_rmsnorm_quant_bit_exact(M, H):
     """The AddNorm kernel at 1, 2 and 4 wavefronts per row (H = 256, 1024,
     >= 2048 at M <= 1024; 2176 leaves the last pass ragged) and at one
-    wavefront per row (M > 1024): resid = RNE(resid + y) in place, then the
-    norm and quantization of the new resid, all bit-exact."""
+    wavefront per row (M > 1024, one and eight passes): resid = RNE(resid + y)
+    in place, then the norm and quantization of the new resid, all
+    bit-exact."""
     _say("add_rmsnorm M=%d H=%d" % (M, H))
     rng = np.random.default_rng(M * 11 + H)
     x = rng.standard_normal((M, H)).astype(np.float32) * np.exp(rng.uniform(-3, 3, (M, 1))).astype(np.float32)
