@@ -142,10 +142,8 @@ __global__ __launch_bounds__(kTileWaves * 64) void gemm_tiled_kernel(
     constexpr bool kCopy = decltype(copy_tag)::value;
     // ---- direct-to-LDS copy plan. Only the first kCopyWaves wavefronts (one
     // per SIMD) copy: a wavefront stalls while the memory pipeline takes its
-    // copy instructions, and the other wavefront of its SIMD keeps multiplying
-    // meanwhile (all eight copying at once left the matrix core idle; one
-    // wavefront alone cannot hide its own scale FMAs, so it runs the core at
-    // well under the rate of two). A copy
+    // copy instructions, and the other wavefront of its SIMD keeps the matrix
+    // core busy meanwhile (all eight copying at once left it idle). A copy
     // instruction fills 64 consecutive 16-byte LDS slots (8 tile rows); lane l
     // fills slot l, i.e. row 8g + l/8, physical chunk l%8, so it fetches logical
     // chunk (l%8) ^ swz(row) of that row. Rows past M (or N) fetch a clamped
